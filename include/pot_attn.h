@@ -1,0 +1,215 @@
+/*
+ * pot_attn.h -- C ABI of libpotattn: single-token decode attention over a key
+ * cache stored as signed power-of-two (PoT) fixed-point codes, for AMD MI355X
+ * (gfx950).
+ *
+ * Method: "Shift-Accumulate Attention: Multiplier-Free Query-Key Products for
+ * Transformer Decoding" (arXiv 2609.09208).
+ *   - key code and query quantiser ............ Sec. II-A, eq. (pot)
+ *   - shift-accumulate (SAC) score ............. Sec. II-B, eq. (sac)
+ *   - exactness by head-room F >= E ............ Sec. II-C, eq. (exact)
+ *   - mantissa family PoT-Mk ................... Sec. II-D, eq. (mant)
+ *   - integer-log2 online softmax max .......... Sec. II-E, eq. (logsm)
+ *   - fused split decode kernel, code-only cache Sec. II-F
+ *   - Hadamard (score-preserving) rotation ..... Sec. I-A and Sec. V-A
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - All tensor pointers are DEVICE pointers (hipMalloc'd or torch-owned
+ *    device memory) unless the argument says "host". The caller owns every
+ *    buffer; the library never allocates or frees device memory.
+ *  - Work is enqueued asynchronously on `stream` (a hipStream_t passed as
+ *    void*, NULL = the legacy default stream). No entry point synchronises
+ *    the host.
+ *  - Every argument check runs on the host before any HIP call, so invalid
+ *    arguments return an error without touching the GPU. Errors are returned,
+ *    never thrown; pot_last_error() gives a human-readable detail for the
+ *    calling thread.
+ *  - Inputs are read-only; outputs must not alias inputs. Codes, V, K and q
+ *    pointers must be 16-byte aligned.
+ *  - Head dimension d is 64.
+ *
+ * Key cache layout ("row" = one (batch b, kv-head h, position t)):
+ *    row(b, h, t) = (b * Hkv + h) * t_cap + t,   0 <= t < t_cap
+ *  codes_se  uint8 [rows][d/2]   sign/exponent nibbles. Byte i holds element
+ *                                2i in its low nibble and 2i+1 in its high
+ *                                nibble. nibble = (neg << 3) | e with
+ *                                e in 0..E a magnitude 2^-e and e = E+1 = 7
+ *                                the exact zero (stored with neg = 0, j = 0).
+ *  codes_m   uint8 [rows][8*k]   k mantissa bit-planes of 64 bits each
+ *                                (little-endian). Bit m of plane b is bit b of
+ *                                the mantissa j_m of element m. NULL if k = 0.
+ *  key_scale float [rows]        per-key-vector scale s_j (Sec. II-A).
+ *  v         fp16  [rows][d]     value cache, row-major.
+ *
+ * Decoded key element (eq. pot and eq. mant):
+ *    K^_m = s * sigma_m * (1 + j_m / 2^k) * 2^-e_m,   or 0 for the zero code.
+ */
+#ifndef POT_ATTN_H
+#define POT_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define POT_HEAD_DIM 64
+#define POT_ABI_VERSION 1
+
+typedef enum pot_status {
+  POT_OK = 0,
+  POT_ERR_INVALID_ARG = 1, /* null pointer, bad size, F < E, T out of range  */
+  POT_ERR_UNSUPPORTED = 2, /* d != 64, unsupported field widths, head map     */
+  POT_ERR_WORKSPACE = 3,   /* workspace too small                             */
+  POT_ERR_HIP = 4          /* a HIP runtime or launch error (see last_error)  */
+} pot_status;
+
+/* Key-code format (Sec. II-A, II-D).
+ *  head_dim  : d, must be 64.
+ *  exp_bits  : exponent field width; only 3 is supported, giving E = 6 and the
+ *              field value 7 as exact zero (b = 4 bits with the sign).
+ *  mant_bits : k in 0..4. 0 is PoT-4, k > 0 is PoT-Mk (4 + k stored bits).
+ *  frac_bits : fixed-point head-room F of eq. (sac). Must satisfy F >= E
+ *              (eq. exact: every shift F - e is then a non-negative left shift)
+ *              and F <= 12 (keeps the int32 accumulator exact for k <= 4).
+ *              The paper's example is F = 7.
+ *  hadamard  : 1 to rotate keys and queries by the orthonormal 64x64
+ *              Sylvester-Hadamard matrix H/8 before quantisation; 0 otherwise.
+ */
+typedef struct pot_format {
+  int32_t head_dim;
+  int32_t exp_bits;
+  int32_t mant_bits;
+  int32_t frac_bits;
+  int32_t hadamard;
+} pot_format;
+
+/* Optional debug taps of pot_decode_attention / pot_int8_decode_attention.
+ * Every pointer may be NULL (tap off). When any tap is non-NULL the call runs
+ * an instrumented build of the same kernel source.
+ *  qhat     int8  [B][Hq][d]  quantised (rotated) query q^ (eq. pot)
+ *  delta    float [B][Hq]     query step Delta_i
+ *  scores   int32 [B][Hq][T]  exact integer accumulator of eq. (sac) at
+ *                             head-room F (for k > 0 at scale 2^-(F+k))
+ *  m_final  int32 [B][Hq]     integer log2-domain maximum M of eq. (logsm)
+ *  m_split  int32 [B][Hq][n_splits] per-split maxima
+ *  force_splits (in)  if > 0, use this many key splits instead of the planner
+ *  n_splits     (out) the number of key splits used (written on the host)
+ *  split_len    (out) keys per split (the last split may be shorter)
+ */
+typedef struct pot_debug {
+  int8_t* qhat;
+  float* delta;
+  int32_t* scores;
+  int32_t* m_final;
+  int32_t* m_split;
+  int32_t force_splits;
+  int32_t n_splits;
+  int32_t split_len;
+} pot_debug;
+
+/* Static string for a status code. Never NULL. */
+const char* pot_status_string(pot_status status);
+
+/* Detail of the last error raised on the calling thread ("" if none). */
+const char* pot_last_error(void);
+
+/* Bytes of codes_se + codes_m per cache row for `fmt` (32 + 8k for d = 64),
+ * or 0 if the format is invalid. Host-only, no HIP call. */
+size_t pot_code_bytes_per_row(const pot_format* fmt);
+
+/* Encode fp16 keys to PoT / PoT-Mk codes (Sec. II-A, II-D).
+ *  k_fp16         [n_rows][d] fp16, dense, device.
+ *  n_rows         number of key vectors (>= 0; 0 is a no-op).
+ *  out_row_stride output row r is written at cache row r * out_row_stride
+ *                 (1 for a dense block; t_cap to append one token to each of
+ *                 n_rows sequences, with the output pointers offset by t rows).
+ *  scale_mode     0: s = max_m |K'_m| (per key vector, written to key_scale);
+ *                 1: s is read from key_scale (caller-given, e.g. one value
+ *                    per head); ratios above the top code saturate.
+ *  Per element: u = fl32(|K'_m| / s), rounded to the grid value
+ *  (1 + j/2^k) 2^-e nearest in log2 distance; u below 2^-(E+1/2) becomes the
+ *  exact zero code. K' = K, or fl32(H K / 8) when fmt->hadamard.
+ *  codes_se [rows][32], codes_m [rows][8k] (NULL iff k = 0), key_scale [rows].
+ */
+pot_status pot_encode_keys(const pot_format* fmt, const uint16_t* k_fp16,
+                           int64_t n_rows, int64_t out_row_stride,
+                           int32_t scale_mode, float* key_scale,
+                           uint8_t* codes_se, uint8_t* codes_m, void* stream);
+
+/* Workspace bytes pot_decode_attention needs for this problem shape (the
+ * split partials and the split-completion counters). Host-only. Returns 0 for
+ * invalid shapes. The same figure serves pot_int8_decode_attention and
+ * pot_fp16_decode_attention. */
+size_t pot_decode_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv,
+                                  int32_t T);
+
+/* Zero the completion counters of a freshly allocated workspace (a fill
+ * kernel on `stream`). Needed once per workspace allocation: every decode
+ * call leaves the counters at zero again when it completes. */
+pot_status pot_workspace_init(void* workspace, size_t ws_bytes, void* stream);
+
+/* Single-token decode attention with PoT keys (Sec. II-B, II-E, II-F).
+ *  q            [B][Hq][d] fp32 query (post-RoPE).
+ *  codes_se, codes_m, key_scale, v_fp16: cache as laid out above, t_cap rows
+ *               per (b, kv-head) sequence.
+ *  kv_head_of_q HOST int32 [Hq]: kv head serving each query head (GQA). Every
+ *               kv head must serve the same number G = Hq/Hkv of query heads,
+ *               G in {1, 2, 4, 8}.
+ *  T            keys attended, 1 <= T <= t_cap.
+ *  out          [B][Hq][d] fp32: O = softmax(S^ / sqrt(d)) V.
+ *  workspace    >= pot_decode_workspace_bytes(B, Hq, Hkv, T) bytes, counters
+ *               zeroed once by pot_workspace_init. Calls that share a
+ *               workspace must not overlap in time.
+ * Steps: q is rotated (if hadamard) and quantised to int8 with step
+ * Delta = amax/127; each score is the exact int32 sum of sign-flipped left
+ * shifts of q^ (eq. sac); x = acc * s * Delta * log2(e) * 2^-(F+k) / 8 in a
+ * fixed fp32 order; the running maximum is the integer M = ceil(max x)
+ * (eq. logsm) so rescales are exact powers of two; weights 2^(x-M) multiply
+ * the fp16 V rows with fp32 accumulation; key splits are merged with exact
+ * 2^(M_s - M) factors.
+ */
+pot_status pot_decode_attention(const pot_format* fmt, const float* q,
+                                const uint8_t* codes_se,
+                                const uint8_t* codes_m, const float* key_scale,
+                                const uint16_t* v_fp16, int64_t t_cap,
+                                const int32_t* kv_head_of_q, int32_t B,
+                                int32_t Hq, int32_t Hkv, int32_t T, float* out,
+                                void* workspace, size_t ws_bytes,
+                                pot_debug* dbg, void* stream);
+
+/* ---- comparison paths on the same cache skeleton --------------------- */
+
+/* INT8 uniform key codes (the multiply-accumulate comparator of Sec. III and
+ * Sec. VI): per key vector s = amax/127, k^ = clamp(rne(K' * (127/amax))).
+ *  codes int8 [rows][d], key_scale float [rows]. hadamard as in pot_format. */
+pot_status pot_int8_encode_keys(const uint16_t* k_fp16, int64_t n_rows,
+                                int64_t out_row_stride, int32_t hadamard,
+                                float* key_scale, int8_t* codes, void* stream);
+
+/* Decode attention with INT8 keys: scores by 4-way int8 dot products
+ * (v_dot4), the same query quantiser, integer-M softmax and fp16 A.V. */
+pot_status pot_int8_decode_attention(
+    const float* q, const int8_t* codes, const float* key_scale,
+    const uint16_t* v_fp16, int64_t t_cap, const int32_t* kv_head_of_q,
+    int32_t B, int32_t Hq, int32_t Hkv, int32_t T, int32_t hadamard,
+    float* out, void* workspace, size_t ws_bytes, pot_debug* dbg,
+    void* stream);
+
+/* Decode attention on an unquantised fp16 cache (the FP16 baseline of
+ * Sec. IV): q is rounded to fp16, scores accumulate in fp32.
+ *  k_fp16, v_fp16 [rows][d] fp16. */
+pot_status pot_fp16_decode_attention(const float* q, const uint16_t* k_fp16,
+                                     const uint16_t* v_fp16, int64_t t_cap,
+                                     const int32_t* kv_head_of_q, int32_t B,
+                                     int32_t Hq, int32_t Hkv, int32_t T,
+                                     float* out, void* workspace,
+                                     size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* POT_ATTN_H */
