@@ -146,6 +146,12 @@ pot_status pot_encode_keys(const pot_format* fmt, const uint16_t* k_fp16,
 size_t pot_decode_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv,
                                   int32_t T);
 
+/* Workspace bytes for a given split count (as forced through
+ * pot_debug.force_splits; the count is clamped as the decode call clamps it).
+ * Host-only. Returns 0 for invalid shapes. */
+size_t pot_decode_workspace_bytes_for_splits(int32_t B, int32_t Hq, int32_t Hkv,
+                                             int32_t T, int32_t n_splits);
+
 /* Zero the completion counters of a freshly allocated workspace (a fill
  * kernel on `stream`). Needed once per workspace allocation: every decode
  * call leaves the counters at zero again when it completes. */

@@ -175,7 +175,15 @@ typedef struct {
   int neg, e, j, zero;
 } elem_code;
 
-static elem_code encode_element(float x, float s, int k) {
+/* log2 of every grid value (1 + j/2^k) 2^-e, index e * 2^k + j. */
+static void grid_log2(int k, double* out) {
+  int nj = 1 << k;
+  for (int e = 0; e <= EXP_MAX; ++e)
+    for (int j = 0; j < nj; ++j)
+      out[e * nj + j] = log2((1.0 + (double)j / nj) * ldexp(1.0, -e));
+}
+
+static elem_code encode_element(float x, float s, int k, const double* glog) {
   elem_code c = {0, ZERO_FIELD, 0, 1};
   if (!(s > 0.0f)) return c;           /* no scale: everything is zero     */
   if (x == 0.0f || isnan(x)) return c; /* exact zero (or undefined input)  */
@@ -189,8 +197,7 @@ static elem_code encode_element(float x, float s, int k) {
     double best = INFINITY;
     for (int e = 0; e <= EXP_MAX; ++e) {
       for (int j = 0; j < nj; ++j) {
-        double g = (1.0 + (double)j / nj) * ldexp(1.0, -e);
-        double dist = fabs(lu - log2(g));
+        double dist = fabs(lu - glog[e * nj + j]);
         if (dist < best) {
           best = dist;
           best_e = e;
@@ -210,6 +217,8 @@ int oracle_encode_keys(int mant_bits, int hadamard, const uint16_t* k_fp16,
                        int64_t n_rows, int scale_mode, float* key_scale,
                        uint8_t* codes_se, uint8_t* codes_m) {
   if (mant_bits < 0 || mant_bits > 4) return -1;
+  double glog[(EXP_MAX + 1) * 16];
+  grid_log2(mant_bits, glog);
   for (int64_t r = 0; r < n_rows; ++r) {
     float kf[DIM], kr[DIM];
     for (int m = 0; m < DIM; ++m) kf[m] = oracle_half_to_float(k_fp16[r * DIM + m]);
@@ -231,7 +240,7 @@ int oracle_encode_keys(int mant_bits, int hadamard, const uint16_t* k_fp16,
     uint8_t* mp = mant_bits ? codes_m + r * 8 * mant_bits : NULL;
     if (mp) memset(mp, 0, (size_t)8 * mant_bits);
     for (int m = 0; m < DIM; ++m) {
-      elem_code c = encode_element(kr[m], s, mant_bits);
+      elem_code c = encode_element(kr[m], s, mant_bits, glog);
       int nib = c.zero ? ZERO_FIELD : ((c.neg << 3) | c.e);
       se[m / 2] |= (uint8_t)(nib << (4 * (m % 2)));
       for (int b = 0; b < mant_bits; ++b)

@@ -1,0 +1,327 @@
+// C ABI of libpotattn (declared in include/pot_attn.h).
+//
+// Every check runs on the host before any HIP call; a rejected call touches
+// neither the device nor the stream. Launches are asynchronous on the
+// caller's stream and allocate nothing.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+#include <vector>
+
+#include "pot_attn.h"
+#include "pot_device.hpp"
+#include "pot_launch.hpp"
+
+using namespace potattn;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+pot_status fail(pot_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+pot_status ok() {
+  g_last_error.clear();
+  return POT_OK;
+}
+
+pot_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ok();
+  return fail(POT_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+constexpr int kE = 6;
+constexpr int kMaxF = 12;
+constexpr int kTargetGroups = 1024;  // 4 workgroups per CU on a 256-CU MI355X
+
+pot_status check_format(const pot_format* f) {
+  if (!f) return fail(POT_ERR_INVALID_ARG, "fmt is NULL");
+  if (f->head_dim != 64) return fail(POT_ERR_UNSUPPORTED, "head_dim %d (only 64)", f->head_dim);
+  if (f->exp_bits != 3) return fail(POT_ERR_UNSUPPORTED, "exp_bits %d (only 3)", f->exp_bits);
+  if (f->mant_bits < 0 || f->mant_bits > 4)
+    return fail(POT_ERR_UNSUPPORTED, "mant_bits %d (0..4)", f->mant_bits);
+  if (f->frac_bits < kE)
+    return fail(POT_ERR_INVALID_ARG,
+                "frac_bits %d < E = %d: a shift F - e would be a right shift", f->frac_bits, kE);
+  if (f->frac_bits > kMaxF)
+    return fail(POT_ERR_UNSUPPORTED, "frac_bits %d > %d (int32 head-room)", f->frac_bits, kMaxF);
+  if (f->hadamard != 0 && f->hadamard != 1)
+    return fail(POT_ERR_INVALID_ARG, "hadamard %d (0 or 1)", f->hadamard);
+  return POT_OK;
+}
+
+struct Plan {
+  int n_splits, split_len;
+};
+
+Plan plan_splits(int B, int Hkv, int T, int force) {
+  const int tiles = (T + kTile - 1) / kTile;
+  int S;
+  if (force > 0) {
+    S = std::min(force, tiles);
+  } else {
+    const long units = (long)B * Hkv;
+    S = (int)std::min<long>((kTargetGroups + units - 1) / units, tiles);
+    S = std::max(S, 1);
+  }
+  const int tiles_per_split = (tiles + S - 1) / S;
+  Plan p;
+  p.split_len = tiles_per_split * kTile;
+  p.n_splits = (T + p.split_len - 1) / p.split_len;
+  return p;
+}
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+struct WsLayout {
+  size_t counters, part_m, part_l, part_o, total;
+};
+
+WsLayout ws_layout(long B, long Hq, long Hkv, long S) {
+  WsLayout w;
+  w.counters = 0;
+  w.part_m = align_up((size_t)(B * Hkv) * 4, 256);
+  w.part_l = w.part_m + align_up((size_t)(B * Hq * S) * 4, 256);
+  w.part_o = w.part_l + align_up((size_t)(B * Hq * S) * 4, 256);
+  w.total = w.part_o + align_up((size_t)(B * Hq * S) * 64 * 4, 256);
+  return w;
+}
+
+bool shape_ok(int B, int Hq, int Hkv, int T) {
+  return B >= 1 && Hq >= 1 && Hkv >= 1 && T >= 1 && Hq % Hkv == 0;
+}
+
+// Validates the GQA head map and fills DecodeArgs::q_of_kv ([Hkv][G]).
+pot_status check_heads(const int32_t* map, int Hq, int Hkv, DecodeArgs* a, int* G_out) {
+  if (!map) return fail(POT_ERR_INVALID_ARG, "kv_head_of_q is NULL");
+  if (Hq > kMaxHqArg) return fail(POT_ERR_UNSUPPORTED, "Hq %d > %d", Hq, kMaxHqArg);
+  if (Hq % Hkv) return fail(POT_ERR_UNSUPPORTED, "Hq %d not a multiple of Hkv %d", Hq, Hkv);
+  const int G = Hq / Hkv;
+  if (G != 1 && G != 2 && G != 4 && G != 8)
+    return fail(POT_ERR_UNSUPPORTED, "group size %d (1, 2, 4 or 8)", G);
+  std::vector<int> fill(Hkv, 0);
+  for (int i = 0; i < Hq; ++i) {
+    const int h = map[i];
+    if (h < 0 || h >= Hkv)
+      return fail(POT_ERR_INVALID_ARG, "kv_head_of_q[%d] = %d outside [0, %d)", i, h, Hkv);
+    if (fill[h] >= G)
+      return fail(POT_ERR_UNSUPPORTED, "kv head %d serves more than %d query heads", h, G);
+    a->q_of_kv[h * G + fill[h]++] = i;
+  }
+  *G_out = G;
+  return POT_OK;
+}
+
+// Shared tail of the three decode entry points.
+pot_status decode_common(int mode, int mant_bits, DecodeArgs& a, const int32_t* map, int B,
+                         int Hq, int Hkv, int T, int64_t t_cap, void* workspace,
+                         size_t ws_bytes, pot_debug* dbg, void* stream) {
+  if (!shape_ok(B, Hq, Hkv, T))
+    return fail(POT_ERR_INVALID_ARG, "bad shape B=%d Hq=%d Hkv=%d T=%d", B, Hq, Hkv, T);
+  if (t_cap < T) return fail(POT_ERR_INVALID_ARG, "T %d > t_cap %lld", T, (long long)t_cap);
+  if (!a.q || !a.v || !a.out) return fail(POT_ERR_INVALID_ARG, "q, v or out is NULL");
+  if (!aligned(a.q, 16) || !aligned(a.v, 16) || !aligned(a.out, 16))
+    return fail(POT_ERR_INVALID_ARG, "q, v and out must be 16-byte aligned");
+  if (!workspace) return fail(POT_ERR_INVALID_ARG, "workspace is NULL");
+  if (!aligned(workspace, 256)) return fail(POT_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  int G = 0;
+  pot_status st = check_heads(map, Hq, Hkv, &a, &G);
+  if (st != POT_OK) return st;
+  const int force = dbg ? dbg->force_splits : 0;
+  if (force < 0) return fail(POT_ERR_INVALID_ARG, "force_splits %d < 0", force);
+  const Plan p = plan_splits(B, Hkv, T, force);
+  const WsLayout w = ws_layout(B, Hq, Hkv, p.n_splits);
+  if (ws_bytes < w.total)
+    return fail(POT_ERR_WORKSPACE, "workspace %zu bytes < %zu needed for %d splits", ws_bytes,
+                w.total, p.n_splits);
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  a.counters = reinterpret_cast<uint32_t*>(ws + w.counters);
+  a.part_m = reinterpret_cast<int32_t*>(ws + w.part_m);
+  a.part_l = reinterpret_cast<float*>(ws + w.part_l);
+  a.part_o = reinterpret_cast<float*>(ws + w.part_o);
+  a.t_cap = t_cap;
+  a.B = B;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.T = T;
+  a.n_splits = p.n_splits;
+  a.split_len = p.split_len;
+  bool debug = false;
+  if (dbg) {
+    a.dbg_qhat = dbg->qhat;
+    a.dbg_delta = dbg->delta;
+    a.dbg_scores = dbg->scores;
+    a.dbg_m_final = dbg->m_final;
+    a.dbg_m_split = dbg->m_split;
+    debug = dbg->qhat || dbg->delta || dbg->scores || dbg->m_final || dbg->m_split;
+    dbg->n_splits = p.n_splits;
+    dbg->split_len = p.split_len;
+    if (debug && mode == kScoreFp16)
+      return fail(POT_ERR_UNSUPPORTED, "debug taps are not available on the fp16 path");
+  }
+  return hip_status(launch_decode(mode, G, mant_bits, debug, a, static_cast<hipStream_t>(stream)),
+                    "decode launch");
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* pot_status_string(pot_status s) {
+  switch (s) {
+    case POT_OK: return "POT_OK";
+    case POT_ERR_INVALID_ARG: return "POT_ERR_INVALID_ARG";
+    case POT_ERR_UNSUPPORTED: return "POT_ERR_UNSUPPORTED";
+    case POT_ERR_WORKSPACE: return "POT_ERR_WORKSPACE";
+    case POT_ERR_HIP: return "POT_ERR_HIP";
+  }
+  return "POT_ERR_UNKNOWN";
+}
+
+const char* pot_last_error(void) { return g_last_error.c_str(); }
+
+size_t pot_code_bytes_per_row(const pot_format* fmt) {
+  if (check_format(fmt) != POT_OK) return 0;
+  return 32 + 8 * (size_t)fmt->mant_bits;
+}
+
+pot_status pot_encode_keys(const pot_format* fmt, const uint16_t* k_fp16, int64_t n_rows,
+                           int64_t out_row_stride, int32_t scale_mode, float* key_scale,
+                           uint8_t* codes_se, uint8_t* codes_m, void* stream) {
+  pot_status st = check_format(fmt);
+  if (st != POT_OK) return st;
+  if (n_rows < 0) return fail(POT_ERR_INVALID_ARG, "n_rows %lld < 0", (long long)n_rows);
+  if (out_row_stride < 1)
+    return fail(POT_ERR_INVALID_ARG, "out_row_stride %lld < 1", (long long)out_row_stride);
+  if (scale_mode != 0 && scale_mode != 1)
+    return fail(POT_ERR_INVALID_ARG, "scale_mode %d (0 or 1)", scale_mode);
+  if (n_rows == 0) return ok();
+  if (!k_fp16 || !key_scale || !codes_se)
+    return fail(POT_ERR_INVALID_ARG, "k_fp16, key_scale or codes_se is NULL");
+  if ((fmt->mant_bits > 0) != (codes_m != nullptr))
+    return fail(POT_ERR_INVALID_ARG, "codes_m must be non-NULL exactly when mant_bits > 0");
+  if (!aligned(k_fp16, 16) || !aligned(codes_se, 16) || !aligned(key_scale, 4) ||
+      (codes_m && !aligned(codes_m, 8)))
+    return fail(POT_ERR_INVALID_ARG, "misaligned k_fp16 / codes_se / key_scale / codes_m");
+  if (n_rows > (int64_t)1 << 36) return fail(POT_ERR_INVALID_ARG, "n_rows too large");
+  const EncodeTables tab = make_encode_tables(fmt->mant_bits);
+  return hip_status(launch_encode_pot(k_fp16, n_rows, out_row_stride, scale_mode, fmt->hadamard,
+                                      key_scale, codes_se, codes_m, tab,
+                                      static_cast<hipStream_t>(stream)),
+                    "encode launch");
+}
+
+size_t pot_decode_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv, int32_t T) {
+  if (!shape_ok(B, Hq, Hkv, T)) return 0;
+  const Plan p = plan_splits(B, Hkv, T, 0);
+  return ws_layout(B, Hq, Hkv, p.n_splits).total;
+}
+
+size_t pot_decode_workspace_bytes_for_splits(int32_t B, int32_t Hq, int32_t Hkv, int32_t T,
+                                             int32_t n_splits) {
+  if (!shape_ok(B, Hq, Hkv, T) || n_splits < 0) return 0;
+  const Plan p = plan_splits(B, Hkv, T, n_splits);
+  return ws_layout(B, Hq, Hkv, p.n_splits).total;
+}
+
+pot_status pot_workspace_init(void* workspace, size_t ws_bytes, void* stream) {
+  if (!workspace) return fail(POT_ERR_INVALID_ARG, "workspace is NULL");
+  return hip_status(launch_fill_zero(workspace, ws_bytes, static_cast<hipStream_t>(stream)),
+                    "workspace init");
+}
+
+pot_status pot_decode_attention(const pot_format* fmt, const float* q, const uint8_t* codes_se,
+                                const uint8_t* codes_m, const float* key_scale,
+                                const uint16_t* v_fp16, int64_t t_cap,
+                                const int32_t* kv_head_of_q, int32_t B, int32_t Hq, int32_t Hkv,
+                                int32_t T, float* out, void* workspace, size_t ws_bytes,
+                                pot_debug* dbg, void* stream) {
+  pot_status st = check_format(fmt);
+  if (st != POT_OK) return st;
+  if (!codes_se || !key_scale) return fail(POT_ERR_INVALID_ARG, "codes_se or key_scale is NULL");
+  if ((fmt->mant_bits > 0) != (codes_m != nullptr))
+    return fail(POT_ERR_INVALID_ARG, "codes_m must be non-NULL exactly when mant_bits > 0");
+  if (!aligned(codes_se, 16) || !aligned(key_scale, 4) || (codes_m && !aligned(codes_m, 8)))
+    return fail(POT_ERR_INVALID_ARG, "misaligned codes_se / key_scale / codes_m");
+  DecodeArgs a{};
+  a.q = q;
+  a.codes_se = codes_se;
+  a.codes_m = codes_m;
+  a.key_scale = key_scale;
+  a.v = v_fp16;
+  a.out = out;
+  a.frac_bits = fmt->frac_bits;
+  a.hadamard = fmt->hadamard;
+  return decode_common(kScorePot, fmt->mant_bits, a, kv_head_of_q, B, Hq, Hkv, T, t_cap,
+                       workspace, ws_bytes, dbg, stream);
+}
+
+pot_status pot_int8_encode_keys(const uint16_t* k_fp16, int64_t n_rows, int64_t out_row_stride,
+                                int32_t hadamard, float* key_scale, int8_t* codes, void* stream) {
+  if (n_rows < 0) return fail(POT_ERR_INVALID_ARG, "n_rows %lld < 0", (long long)n_rows);
+  if (out_row_stride < 1)
+    return fail(POT_ERR_INVALID_ARG, "out_row_stride %lld < 1", (long long)out_row_stride);
+  if (hadamard != 0 && hadamard != 1)
+    return fail(POT_ERR_INVALID_ARG, "hadamard %d (0 or 1)", hadamard);
+  if (n_rows == 0) return ok();
+  if (!k_fp16 || !key_scale || !codes)
+    return fail(POT_ERR_INVALID_ARG, "k_fp16, key_scale or codes is NULL");
+  if (!aligned(k_fp16, 16) || !aligned(codes, 16) || !aligned(key_scale, 4))
+    return fail(POT_ERR_INVALID_ARG, "misaligned k_fp16 / codes / key_scale");
+  return hip_status(launch_encode_int8(k_fp16, n_rows, out_row_stride, hadamard, key_scale,
+                                       codes, static_cast<hipStream_t>(stream)),
+                    "int8 encode launch");
+}
+
+pot_status pot_int8_decode_attention(const float* q, const int8_t* codes, const float* key_scale,
+                                     const uint16_t* v_fp16, int64_t t_cap,
+                                     const int32_t* kv_head_of_q, int32_t B, int32_t Hq,
+                                     int32_t Hkv, int32_t T, int32_t hadamard, float* out,
+                                     void* workspace, size_t ws_bytes, pot_debug* dbg,
+                                     void* stream) {
+  if (hadamard != 0 && hadamard != 1)
+    return fail(POT_ERR_INVALID_ARG, "hadamard %d (0 or 1)", hadamard);
+  if (!codes || !key_scale) return fail(POT_ERR_INVALID_ARG, "codes or key_scale is NULL");
+  if (!aligned(codes, 16) || !aligned(key_scale, 4))
+    return fail(POT_ERR_INVALID_ARG, "misaligned codes / key_scale");
+  DecodeArgs a{};
+  a.q = q;
+  a.codes_i8 = codes;
+  a.key_scale = key_scale;
+  a.v = v_fp16;
+  a.out = out;
+  a.hadamard = hadamard;
+  return decode_common(kScoreInt8, 0, a, kv_head_of_q, B, Hq, Hkv, T, t_cap, workspace, ws_bytes,
+                       dbg, stream);
+}
+
+pot_status pot_fp16_decode_attention(const float* q, const uint16_t* k_fp16,
+                                     const uint16_t* v_fp16, int64_t t_cap,
+                                     const int32_t* kv_head_of_q, int32_t B, int32_t Hq,
+                                     int32_t Hkv, int32_t T, float* out, void* workspace,
+                                     size_t ws_bytes, void* stream) {
+  if (!k_fp16) return fail(POT_ERR_INVALID_ARG, "k_fp16 is NULL");
+  if (!aligned(k_fp16, 16)) return fail(POT_ERR_INVALID_ARG, "k_fp16 must be 16-byte aligned");
+  DecodeArgs a{};
+  a.q = q;
+  a.k_f16 = k_fp16;
+  a.v = v_fp16;
+  a.out = out;
+  return decode_common(kScoreFp16, 0, a, kv_head_of_q, B, Hq, Hkv, T, t_cap, workspace, ws_bytes,
+                       nullptr, stream);
+}
+
+}  // extern "C"

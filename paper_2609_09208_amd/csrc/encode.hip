@@ -1,0 +1,171 @@
+// Key encoders for gfx950: fp16 key rows -> PoT / PoT-Mk codes (Sec. II-A,
+// II-D) and -> INT8 uniform codes (the multiply-accumulate comparator).
+//
+// One wavefront encodes one 64-element key row, one element per lane: a
+// 128-byte coalesced fp16 load, an optional exact fp64 Walsh-Hadamard
+// butterfly across lanes, a wave max for the per-row scale, a per-lane
+// log-nearest decision against fp32 cut points, and packing by lane shuffles
+// (sign/exponent nibbles) and ballots (mantissa bit-planes).
+#include <hip/hip_fp16.h>
+
+#include <cmath>
+
+#include "pot_device.hpp"
+#include "pot_launch.hpp"
+
+namespace potattn {
+
+namespace {
+
+// Largest fp32 strictly below sqrt(num / den^2) for num not a perfect square,
+// with num / den^2 in [1, 4): the value is M * 2^-23 with M the integer part
+// of sqrt(num * 2^46 / den^2) (exact integer square root).
+float rd_sqrt_ratio(uint64_t num, uint64_t den) {
+  // R * 2^46 = num * 2^46 / den^2; den is a power of two <= 16 so the
+  // division is exact.
+  unsigned __int128 v = ((unsigned __int128)num << 46) / ((unsigned __int128)den * den);
+  uint64_t m = (uint64_t)std::sqrt((long double)v);
+  while ((unsigned __int128)m * m > v) --m;
+  while ((unsigned __int128)(m + 1) * (m + 1) <= v) ++m;
+  return std::ldexp((float)m, -23);  // m < 2^25 so exact in fp32
+}
+
+}  // namespace
+
+EncodeTables make_encode_tables(int mant_bits) {
+  EncodeTables t{};
+  const uint64_t n = 1ull << mant_bits;
+  for (uint64_t i = 0; i < n; ++i) t.cut[i] = rd_sqrt_ratio((n + i) * (n + i + 1), n);
+  for (uint64_t i = n; i < 16; ++i) t.cut[i] = INFINITY;
+  // 2^-(E+1/2) = sqrt(2) * 2^-7: RD of sqrt(2) scaled by an exact power of two.
+  t.zero_cut = std::ldexp(rd_sqrt_ratio(2, 1), -(kExpMax + 1));
+  t.mant_bits = mant_bits;
+  return t;
+}
+
+// Log-nearest PoT-Mk code of one element. Returns the nibble (neg<<3 | e, or
+// 7 for zero) and the mantissa j.
+__device__ __forceinline__ int classify(float x, float s, const EncodeTables& tab, int* j_out) {
+  *j_out = 0;
+  if (!(s > 0.0f) || x == 0.0f || x != x) return kZeroField;
+  const float u = fabsf(x) / s;  // one correctly rounded division
+  if (!(u > tab.zero_cut)) return kZeroField;
+  const int n = 1 << tab.mant_bits;
+  const uint32_t ub = __float_as_uint(u);
+  const int e2 = (int)((ub >> 23) & 0xFF) - 127;         // u > 2^-7: normal
+  const float m = __uint_as_float((ub & 0x007FFFFFu) | 0x3F800000u);  // [1, 2)
+  int c = 0;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) c += (i < n && m > tab.cut[i]) ? 1 : 0;
+  int e, j;
+  if (e2 >= 0) {  // u >= 1: the top binade, saturating at its largest value
+    e = 0;
+    j = (e2 > 0) ? n - 1 : min(c, n - 1);
+  } else if (c == n) {  // rounds up to the next binade's first value
+    e = -e2 - 1;
+    j = 0;
+  } else {
+    e = -e2;
+    j = c;
+  }
+  if (e > kExpMax) {  // between the zero cut and 2^-E: the smallest magnitude
+    e = kExpMax;
+    j = 0;
+  }
+  *j_out = j;
+  return ((x < 0.0f) ? 8 : 0) | e;
+}
+
+__global__ __launch_bounds__(kBlock) void encode_pot_kernel(
+    const __half* __restrict__ k, int64_t n_rows, int64_t out_stride, int scale_mode,
+    int hadamard, float* __restrict__ key_scale, uint8_t* __restrict__ codes_se,
+    uint8_t* __restrict__ codes_m, EncodeTables tab) {
+  const int lane = lane_id();
+  const int64_t row = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
+  if (row >= n_rows) return;  // uniform per wave
+  float x = __half2float(k[row * kDim + lane]);
+  if (hadamard) x = (float)(wave_fwht64((double)x) * 0.125);
+  const int64_t orow = row * out_stride;
+  float s;
+  if (scale_mode == 0) {
+    s = wave_max(fabsf(x));
+    if (lane == 0) key_scale[orow] = s;
+  } else {
+    s = key_scale[orow];
+  }
+  int j;
+  const int nib = classify(x, s, tab, &j);
+  // sign/exponent nibbles: element m at bit 4*(m%8) of dword m/8
+  uint32_t w = (uint32_t)nib << (4 * (lane & 7));
+  w |= __shfl_xor(w, 1, 64);
+  w |= __shfl_xor(w, 2, 64);
+  w |= __shfl_xor(w, 4, 64);
+  if ((lane & 7) == 0) reinterpret_cast<uint32_t*>(codes_se + orow * (kDim / 2))[lane >> 3] = w;
+  // mantissa bit-planes: bit m of plane b is bit b of j_m
+  for (int b = 0; b < tab.mant_bits; ++b) {
+    const unsigned long long plane = __ballot((j >> b) & 1);
+    if (lane == 0)
+      reinterpret_cast<unsigned long long*>(codes_m + orow * 8 * tab.mant_bits)[b] = plane;
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void encode_int8_kernel(
+    const __half* __restrict__ k, int64_t n_rows, int64_t out_stride, int hadamard,
+    float* __restrict__ key_scale, int8_t* __restrict__ codes) {
+  const int lane = lane_id();
+  const int64_t row = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
+  if (row >= n_rows) return;
+  float x = __half2float(k[row * kDim + lane]);
+  if (hadamard) x = (float)(wave_fwht64((double)x) * 0.125);
+  float step;
+  const int c = wave_quantize_int8(x, &step);
+  const int64_t orow = row * out_stride;
+  codes[orow * kDim + lane] = (int8_t)c;
+  if (lane == 0) key_scale[orow] = step;
+}
+
+__global__ void fill_zero_kernel(uint32_t* __restrict__ p, size_t n_words, uint8_t* tail,
+                                 size_t tail_bytes) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n_words) p[i] = 0u;
+  if (i < tail_bytes) tail[i] = 0;
+}
+
+hipError_t launch_encode_pot(const uint16_t* k, int64_t n_rows, int64_t out_stride,
+                             int scale_mode, int hadamard, float* key_scale,
+                             uint8_t* codes_se, uint8_t* codes_m, const EncodeTables& tab,
+                             hipStream_t stream) {
+  if (n_rows == 0) return hipSuccess;
+  const int64_t rows_per_block = kBlock / 64;
+  const int64_t grid = (n_rows + rows_per_block - 1) / rows_per_block;
+  hipLaunchKernelGGL(encode_pot_kernel, dim3((uint32_t)grid), dim3(kBlock), 0, stream,
+                     reinterpret_cast<const __half*>(k), n_rows, out_stride, scale_mode,
+                     hadamard, key_scale, codes_se, codes_m, tab);
+  return hipGetLastError();
+}
+
+hipError_t launch_encode_int8(const uint16_t* k, int64_t n_rows, int64_t out_stride,
+                              int hadamard, float* key_scale, int8_t* codes,
+                              hipStream_t stream) {
+  if (n_rows == 0) return hipSuccess;
+  const int64_t rows_per_block = kBlock / 64;
+  const int64_t grid = (n_rows + rows_per_block - 1) / rows_per_block;
+  hipLaunchKernelGGL(encode_int8_kernel, dim3((uint32_t)grid), dim3(kBlock), 0, stream,
+                     reinterpret_cast<const __half*>(k), n_rows, out_stride, hadamard,
+                     key_scale, codes);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream) {
+  if (bytes == 0) return hipSuccess;
+  const size_t n_words = bytes / 4;
+  const size_t tail = bytes - n_words * 4;
+  const size_t n = n_words > tail ? n_words : tail;
+  const size_t grid = (n + 255) / 256;
+  hipLaunchKernelGGL(fill_zero_kernel, dim3((uint32_t)grid), dim3(256), 0, stream,
+                     reinterpret_cast<uint32_t*>(ptr), n_words,
+                     reinterpret_cast<uint8_t*>(ptr) + n_words * 4, tail);
+  return hipGetLastError();
+}
+
+}  // namespace potattn

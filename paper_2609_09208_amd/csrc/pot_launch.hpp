@@ -1,0 +1,70 @@
+// Host-side launch interface between the C ABI layer (api.cpp) and the
+// kernel translation units. Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace potattn {
+
+constexpr int kMaxHqArg = 128;  // query heads addressable through kernel args
+
+// Encoder tables passed by value as kernel arguments (no device globals).
+struct EncodeTables {
+  // Cut points between consecutive mantissa grid values inside one binade,
+  // scaled to [1, 2): cut[i] = RD_fp32(sqrt((n+i)(n+i+1)) / n), n = 2^k,
+  // i = 0..n-1 (the last one separates the binade top from the next binade).
+  float cut[16];
+  // RD_fp32(2^-(E + 1/2)): ratios at or below it become the exact zero.
+  float zero_cut;
+  int32_t mant_bits;
+};
+
+// Computes EncodeTables for mantissa width k with exact integer square roots.
+EncodeTables make_encode_tables(int mant_bits);
+
+hipError_t launch_encode_pot(const uint16_t* k, int64_t n_rows, int64_t out_stride,
+                             int scale_mode, int hadamard, float* key_scale,
+                             uint8_t* codes_se, uint8_t* codes_m,
+                             const EncodeTables& tab, hipStream_t stream);
+
+hipError_t launch_encode_int8(const uint16_t* k, int64_t n_rows, int64_t out_stride,
+                              int hadamard, float* key_scale, int8_t* codes,
+                              hipStream_t stream);
+
+hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream);
+
+enum ScoreMode : int { kScorePot = 0, kScoreInt8 = 1, kScoreFp16 = 2 };
+
+// Everything one decode launch needs. Passed by value as the kernel argument.
+struct DecodeArgs {
+  const float* q;
+  const uint8_t* codes_se;   // PoT
+  const uint8_t* codes_m;    // PoT-Mk planes
+  const int8_t* codes_i8;    // INT8 keys
+  const uint16_t* k_f16;     // fp16 keys
+  const float* key_scale;
+  const uint16_t* v;
+  float* out;
+  // workspace
+  uint32_t* counters;        // [B*Hkv]
+  int32_t* part_m;           // [B*Hq*S]
+  float* part_l;             // [B*Hq*S]
+  float* part_o;             // [B*Hq*S*64]
+  // debug taps (nullable)
+  int8_t* dbg_qhat;
+  float* dbg_delta;
+  int32_t* dbg_scores;
+  int32_t* dbg_m_final;
+  int32_t* dbg_m_split;
+  int64_t t_cap;
+  int32_t B, Hq, Hkv, T;
+  int32_t n_splits, split_len;
+  int32_t frac_bits, hadamard;
+  int32_t q_of_kv[kMaxHqArg];  // [Hkv][G] query heads served by each kv head
+};
+
+hipError_t launch_decode(int mode, int G, int mant_bits, bool debug,
+                         const DecodeArgs& a, hipStream_t stream);
+
+}  // namespace potattn

@@ -1,0 +1,280 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Bar: codes, key scales, q^, Delta, int32 scores and integer maxima (final and
+per split) bit-exact; O within max-abs 2e-3 (fp32 accumulation). Workloads
+follow the paper's TinyLlama-1.1B decode shape (32 query heads, 4 kv heads,
+d = 64) with seeded synthetic inputs (workloads.py)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_09208_amd as pa
+from parity_util import (DEV, O_TOL, assert_pot_parity, gpu_encode, gpu_pot_decode,
+                         oracle_pot, to_dev)
+from workloads import head_map, make_decode_inputs, make_decode_inputs_device
+
+pytestmark = pytest.mark.gpu
+
+
+def _all_fp16_rows():
+    return np.arange(65536, dtype=np.uint32).astype(np.uint16).reshape(1024, 64)
+
+
+# ---- encoder ----------------------------------------------------------------
+@pytest.mark.parametrize("k", [0, 1, 2, 3, 4])
+def test_encode_every_fp16_pattern(k):
+    rows = _all_fp16_rows()
+    for s in (1.0, 0.001, 3.7, 65504.0, 2.0 ** -20, 0.0):
+        sc = np.full(1024, s, np.float32)
+        g = gpu_encode(rows, k, key_scale=sc)
+        o = oracle.encode_keys(rows, mant_bits=k, key_scale=sc)
+        assert np.array_equal(g[0], o[0]), (k, s)
+        if k:
+            assert np.array_equal(g[1], o[1]), (k, s)
+
+
+@pytest.mark.parametrize("k,had", [(0, False), (1, False), (4, False), (0, True),
+                                   (1, True), (4, True)])
+def test_encode_absmax_rows(k, had):
+    d = make_decode_inputs(100 + k, B=2, Hq=8, Hkv=4, T=1000)
+    rows = d["k_bits"].reshape(-1, 64)
+    g = gpu_encode(rows, k, had)
+    o = oracle.encode_keys(rows, mant_bits=k, hadamard=had)
+    assert np.array_equal(g[0], o[0])
+    if k:
+        assert np.array_equal(g[1], o[1])
+    assert np.array_equal(g[2].view(np.uint32), o[2].view(np.uint32))
+
+
+def test_encode_append_with_row_stride():
+    # append one token (position t) to each of B*Hkv sequences of a t_cap cache
+    B, Hkv, t_cap, t, k = 3, 4, 50, 17, 2
+    rng = np.random.default_rng(5)
+    new = rng.standard_normal((B * Hkv, 64)).astype(np.float16).view(np.uint16)
+    fmt = pa.make_format(k)
+    cache = pa.alloc_pot_cache(B, Hkv, t_cap, k, DEV)
+    kd = to_dev(new).view(torch.float16)
+    se, cm, sc = cache["codes_se"], cache["codes_m"], cache["key_scale"]
+    pa.pot_encode_keys(fmt, kd, B * Hkv, t_cap, 0,
+                       sc.view(-1)[t:], se.view(-1, 32)[t:], cm.view(-1, 8 * k)[t:])
+    torch.cuda.synchronize()
+    o_se, o_cm, o_sc = oracle.encode_keys(new, mant_bits=k)
+    g_se = se.cpu().numpy().reshape(B * Hkv, t_cap, 32)
+    g_cm = cm.cpu().numpy().reshape(B * Hkv, t_cap, 8 * k)
+    g_sc = sc.cpu().numpy().reshape(B * Hkv, t_cap)
+    assert np.array_equal(g_se[:, t], o_se) and np.array_equal(g_cm[:, t], o_cm)
+    assert np.array_equal(g_sc[:, t], o_sc)
+    # nothing else written
+    others = np.ones(t_cap, bool)
+    others[t] = False
+    assert not g_se[:, others].any() and not g_sc[:, others].any()
+
+
+@pytest.mark.parametrize("had", [False, True])
+def test_int8_encode(had):
+    d = make_decode_inputs(7, B=1, Hq=8, Hkv=4, T=700)
+    rows = d["k_bits"].reshape(-1, 64)
+    n = rows.shape[0]
+    codes = torch.empty((n, 64), dtype=torch.int8, device=DEV)
+    sc = torch.empty(n, dtype=torch.float32, device=DEV)
+    pa.pot_int8_encode_keys(to_dev(rows).view(torch.float16), n, 1, int(had), sc, codes)
+    torch.cuda.synchronize()
+    oc, osc = oracle.int8_encode_keys(rows, hadamard=had)
+    assert np.array_equal(codes.cpu().numpy(), oc)
+    assert np.array_equal(sc.cpu().numpy().view(np.uint32), osc.view(np.uint32))
+
+
+# ---- decode: the paper's configurations ---------------------------------------
+def test_tiny_single_head_pot4():
+    # d = 64, T = 256, batch 1, one head; K and q N(0, 1), V fp16 N(0, 1)
+    d = make_decode_inputs(0, B=1, Hq=1, Hkv=1, T=256, channel_scale=False)
+    err, _ = assert_pot_parity(d)
+    print(f"tiny PoT-4 O max-abs err {err:.3e}")
+
+
+def test_tiny_single_head_head_wide_scale():
+    # one caller-given scale per head (scale mode 1): the head's absmax
+    d = make_decode_inputs(1, B=1, Hq=1, Hkv=1, T=256, channel_scale=False)
+    kf = d["k_bits"].view(np.float16).astype(np.float32)
+    s = np.full(256, np.abs(kf).max(), np.float32)
+    err, _ = assert_pot_parity(d, key_scale=s)
+    print(f"tiny head-scale O max-abs err {err:.3e}")
+
+
+def test_tinyllama_layer_t4096_pot4():
+    d = make_decode_inputs(2, B=1, Hq=32, Hkv=4, T=4096)
+    err, g = assert_pot_parity(d)
+    print(f"T=4096 PoT-4 splits={g['n_splits']} O err {err:.3e}")
+
+
+def test_tinyllama_layer_t32768_potm1():
+    d = make_decode_inputs(3, B=1, Hq=32, Hkv=4, T=32768)
+    err, g = assert_pot_parity(d, mant_bits=1)
+    print(f"T=32768 PoT-M1 splits={g['n_splits']} O err {err:.3e}")
+
+
+def test_batch8_hadamard_potm4_reduced_T():
+    d = make_decode_inputs(4, B=8, Hq=32, Hkv=4, T=2048)
+    err, g = assert_pot_parity(d, mant_bits=4, hadamard=True)
+    print(f"B=8 T=2048 H+PoT-M4 O err {err:.3e}")
+
+
+def _sampled_full_size(B, T, mant_bits, hadamard, samples, seed):
+    """Full-size launch as the benchmark times it (planner splits, no taps);
+    sampled (b, kv-head) slices checked against the oracle."""
+    Hq, Hkv = 32, 4
+    d = make_decode_inputs_device(seed, B, Hq, Hkv, T, DEV)
+    fmt = pa.make_format(mant_bits, 7, hadamard)
+    cache = pa.alloc_pot_cache(B, Hkv, T, mant_bits, DEV)
+    rows = B * Hkv * T
+    pa.pot_encode_keys(fmt, d["k"], rows, 1, 0, cache["key_scale"], cache["codes_se"],
+                       cache["codes_m"])
+    out = torch.empty((B, Hq, 64), dtype=torch.float32, device=DEV)
+    ws = pa.alloc_workspace(pa.pot_decode_workspace_bytes(B, Hq, Hkv, T), DEV)
+    pa.pot_decode_attention(fmt, d["q"], cache["codes_se"], cache["codes_m"],
+                            cache["key_scale"], d["v"], T, d["kv_head_of_q"], B, Hq, Hkv,
+                            T, out, ws)
+    torch.cuda.synchronize()
+    G = Hq // Hkv
+    worst = 0.0
+    for (b, h) in samples:
+        kb = d["k"][b, h].view(torch.uint16).cpu().numpy()
+        vb = d["v"][b, h].view(torch.uint16).cpu().numpy()
+        qs = d["q"][b, h * G:(h + 1) * G].cpu().numpy()
+        o_se, o_cm, o_sc = oracle.encode_keys(kb, mant_bits=mant_bits, hadamard=hadamard)
+        assert np.array_equal(cache["codes_se"][b, h].cpu().numpy(), o_se)
+        if mant_bits:
+            assert np.array_equal(cache["codes_m"][b, h].cpu().numpy(), o_cm)
+        assert np.array_equal(cache["key_scale"][b, h].cpu().numpy(), o_sc)
+        r = oracle.pot_decode(qs[None], o_se, o_cm, o_sc, vb, T, np.zeros(G, np.int32),
+                              1, G, 1, T, mant_bits=mant_bits, hadamard=hadamard)
+        err = float(np.abs(out[b, h * G:(h + 1) * G].cpu().numpy() - r["out"][0]).max())
+        worst = max(worst, err)
+    assert worst <= O_TOL, worst
+    return worst
+
+
+def test_full_size_b64_t32768_pot4_sampled():
+    err = _sampled_full_size(64, 32768, 0, False, [(0, 0), (17, 3), (63, 2)], 10)
+    print(f"B=64 T=32768 PoT-4 sampled O err {err:.3e}")
+
+
+def test_full_size_b8_t32768_hadamard_potm4_sampled():
+    err = _sampled_full_size(8, 32768, 4, True, [(0, 1), (7, 3)], 11)
+    print(f"B=8 T=32768 H+PoT-M4 sampled O err {err:.3e}")
+
+
+# ---- edge cases ------------------------------------------------------------------
+@pytest.mark.parametrize("T,t_cap", [(1, 1), (5, 9), (255, 255), (257, 300), (1000, 1031)])
+def test_ragged_lengths_and_padding(T, t_cap):
+    d = make_decode_inputs(20 + T, B=2, Hq=8, Hkv=2, T=T, t_cap=t_cap)
+    assert_pot_parity(d, mant_bits=1)
+
+
+@pytest.mark.parametrize("Hq,Hkv", [(1, 1), (4, 2), (8, 2), (32, 4), (16, 16)])
+def test_group_sizes(Hq, Hkv):
+    d = make_decode_inputs(30 + Hq, B=2, Hq=Hq, Hkv=Hkv, T=300)
+    assert_pot_parity(d)
+
+
+def test_interleaved_head_map():
+    d = make_decode_inputs(41, B=2, Hq=8, Hkv=2, T=300)
+    d["kv_head_of_q"] = (np.arange(8) % 2).astype(np.int32)
+    assert_pot_parity(d, mant_bits=2)
+
+
+@pytest.mark.parametrize("F", [6, 12])
+def test_head_room(F):
+    d = make_decode_inputs(42, B=1, Hq=8, Hkv=1, T=600)
+    assert_pot_parity(d, mant_bits=4 if F == 12 else 0, frac_bits=F)
+
+
+def test_degenerate_rows_and_query():
+    d = make_decode_inputs(43, B=2, Hq=8, Hkv=2, T=300)
+    k = d["k_bits"].view(np.float16)
+    k[0, 0, 10] = 0            # all-zero key row: s = 0, every code zero
+    k[1, 1, 50:60] = 0
+    k[0, 1, 7, :32] = 0        # half-zero row
+    d["q"][1, 3] = 0           # zero query: Delta = 0, uniform weights
+    assert_pot_parity(d, mant_bits=1)
+
+
+@pytest.mark.parametrize("S", [1, 2, 3, 7, 16])
+def test_forced_splits(S):
+    d = make_decode_inputs(44, B=1, Hq=32, Hkv=4, T=4000)
+    err, g = assert_pot_parity(d, force_splits=S)
+    assert g["n_splits"] == min(S, 16)
+
+
+def test_split_invariance_and_determinism():
+    d = make_decode_inputs(45, B=2, Hq=32, Hkv=4, T=3000)
+    se, cm, sc = gpu_encode(d["k_bits"].reshape(-1, 64), 0)
+    ms = []
+    outs = []
+    for S in (1, 4, 12, 12):
+        g = gpu_pot_decode(d, se, cm, sc, force_splits=S)
+        ms.append(g["m_final"])
+        outs.append(g["out"])
+    for m in ms[1:]:
+        assert np.array_equal(m, ms[0])
+    assert np.array_equal(outs[2], outs[3])  # run to run bit-identical
+    assert np.abs(outs[0] - outs[1]).max() < 1e-5
+
+
+# ---- comparison kernels ------------------------------------------------------------
+@pytest.mark.parametrize("had", [False, True])
+def test_int8_decode_parity(had):
+    d = make_decode_inputs(50, B=2, Hq=32, Hkv=4, T=2500)
+    rows = d["k_bits"].reshape(-1, 64)
+    n = rows.shape[0]
+    codes = torch.empty((n, 64), dtype=torch.int8, device=DEV)
+    sc = torch.empty(n, dtype=torch.float32, device=DEV)
+    pa.pot_int8_encode_keys(to_dev(rows).view(torch.float16), n, 1, int(had), sc, codes)
+    B, Hq, Hkv, T = 2, 32, 4, 2500
+    out = torch.empty((B, Hq, 64), dtype=torch.float32, device=DEV)
+    ws = pa.alloc_workspace(pa.pot_decode_workspace_bytes(B, Hq, Hkv, T), DEV)
+    dbg = pa.pot_debug()
+    taps = dict(qhat=torch.empty((B, Hq, 64), dtype=torch.int8, device=DEV),
+                delta=torch.empty((B, Hq), dtype=torch.float32, device=DEV),
+                scores=torch.empty((B, Hq, T), dtype=torch.int32, device=DEV),
+                m_final=torch.empty((B, Hq), dtype=torch.int32, device=DEV))
+    for k_, t_ in taps.items():
+        setattr(dbg, k_, t_.data_ptr())
+    pa.pot_int8_decode_attention(to_dev(d["q"]), codes, sc, to_dev(d["v_bits"]).view(torch.float16),
+                                 T, d["kv_head_of_q"], B, Hq, Hkv, T, int(had), out, ws, dbg=dbg)
+    torch.cuda.synchronize()
+    oc, osc = oracle.int8_encode_keys(rows, hadamard=had)
+    r = oracle.int8_decode(d["q"], oc, osc, d["v_bits"], T, d["kv_head_of_q"], B, Hq, Hkv, T,
+                           hadamard=had)
+    assert np.array_equal(taps["qhat"].cpu().numpy(), r["qhat"])
+    assert np.array_equal(taps["scores"].cpu().numpy(), r["scores"])
+    assert np.array_equal(taps["m_final"].cpu().numpy(), r["m_final"])
+    assert np.abs(out.cpu().numpy() - r["out"]).max() <= O_TOL
+
+
+def test_fp16_decode_parity():
+    d = make_decode_inputs(51, B=2, Hq=32, Hkv=4, T=2500, t_cap=2600)
+    B, Hq, Hkv, T = 2, 32, 4, 2500
+    out = torch.empty((B, Hq, 64), dtype=torch.float32, device=DEV)
+    ws = pa.alloc_workspace(pa.pot_decode_workspace_bytes(B, Hq, Hkv, T), DEV)
+    pa.pot_fp16_decode_attention(to_dev(d["q"]), to_dev(d["k_bits"]).view(torch.float16),
+                                 to_dev(d["v_bits"]).view(torch.float16), 2600,
+                                 d["kv_head_of_q"], B, Hq, Hkv, T, out, ws)
+    torch.cuda.synchronize()
+    r = oracle.fp16_decode(d["q"], d["k_bits"], d["v_bits"], 2600, d["kv_head_of_q"], B, Hq,
+                           Hkv, T)
+    err = float(np.abs(out.cpu().numpy() - r).max())
+    assert err <= O_TOL, err
+    print(f"fp16 O err {err:.3e}")
+
+
+def test_status_errors_do_not_launch():
+    # invalid arguments are rejected on the host even with real buffers
+    d = make_decode_inputs(52, B=1, Hq=8, Hkv=1, T=10)
+    q = to_dev(d["q"])
+    with pytest.raises(pa.PotError) as ei:
+        pa.pot_decode_attention(pa.make_format(frac_bits=3), q, q, None, q, q, 10,
+                                d["kv_head_of_q"], 1, 8, 1, 10, q,
+                                pa.alloc_workspace(1 << 16, DEV))
+    assert ei.value.status == pa.POT_ERR_INVALID_ARG
