@@ -50,6 +50,11 @@ def make_format(mant_bits: int = 0, frac_bits: int = 7, hadamard: bool = False,
 
 
 def _load_library():
+    # torch ships its own HIP runtime with the same soname as ROCm's; load it
+    # first so that this library binds to the one runtime torch uses for the
+    # device memory and streams it hands over (two runtimes in one process do
+    # not share devices).
+    import torch  # noqa: F401
     if not os.path.exists(_LIB_PATH):
         raise ImportError(
             f"{_LIB_PATH} is not built; run __graft_entry__.build() (hipcc, gfx950)")

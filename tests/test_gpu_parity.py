@@ -204,7 +204,9 @@ def test_degenerate_rows_and_query():
 def test_forced_splits(S):
     d = make_decode_inputs(44, B=1, Hq=32, Hkv=4, T=4000)
     err, g = assert_pot_parity(d, force_splits=S)
-    assert g["n_splits"] == min(S, 16)
+    tiles = -(-4000 // 256)
+    split_len = -(-tiles // min(S, tiles)) * 256  # whole tiles per split
+    assert g["split_len"] == split_len and g["n_splits"] == -(-4000 // split_len)
 
 
 def test_split_invariance_and_determinism():
