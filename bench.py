@@ -1,8 +1,9 @@
 """Benchmark: TinyLlama-1.1B-shaped decode step with PoT-4 key caches.
 
-One step = 22 layers, each: append the new token's key to that layer's PoT-4
-cache (pot_encode_keys, one row per (batch, kv head)) and run single-token
-decode attention over T keys (pot_decode_attention). 32 query heads, 4 kv
+One step = 22 layers, each: append the new token's key and value to that
+layer's cache (pot_encode_keys and pot_store_values, one row per (batch, kv
+head)) and run single-token decode attention over T keys
+(pot_decode_attention). 32 query heads, 4 kv
 heads, d = 64, fp16 values, synthetic seeded inputs resident in HBM before the
 timed region. Every layer has its own cache, so consecutive calls never hit
 the previous layer's data in the 256 MB last-level cache.
@@ -128,9 +129,13 @@ def main() -> int:
         cache = pa.alloc_pot_cache(B, HKV, T, k, dev)
         pa.pot_encode_keys(fmt, d["k"], B * HKV * T, 1, 0, cache["key_scale"],
                            cache["codes_se"], cache["codes_m"])
+        vcache = pa.alloc_value_cache(B, HKV, T, dev)
+        pa.pot_store_values(d["v"], B * HKV, T, T, 0, vcache)
         new_k = d["k"][:, :, T - 1].contiguous()  # the appended token's key
+        new_v = d["v"][:, :, T - 1].contiguous()  # and value
         keep_k16 = d["k"] if (not args.no_compare and layer < 4) else None
-        layers.append(dict(q=d["q"], v=d["v"], new_k=new_k, k16=keep_k16, **cache))
+        layers.append(dict(q=d["q"], v=vcache, new_k=new_k, new_v=new_v, k16=keep_k16,
+                           **cache))
         del d
     heads = np.arange(HQ, dtype=np.int32) // G
     out = torch.empty((B, HQ, D), dtype=torch.float32, device=dev)
@@ -143,6 +148,7 @@ def main() -> int:
             pa.pot_encode_keys(fmt, c["new_k"], B * HKV, T, 0, c["key_scale"].view(-1)[pos:],
                                c["codes_se"].view(-1, 32)[pos:],
                                c["codes_m"].view(-1, 8 * k)[pos:] if k else None)
+            pa.pot_store_values(c["new_v"], B * HKV, 1, T, pos, c["v"])
             if events is not None:
                 events[i][0].record()
             pa.pot_decode_attention(fmt, c["q"], c["codes_se"], c["codes_m"], c["key_scale"],

@@ -40,7 +40,14 @@
  *                                (little-endian). Bit m of plane b is bit b of
  *                                the mantissa j_m of element m. NULL if k = 0.
  *  key_scale float [rows]        per-key-vector scale s_j (Sec. II-A).
- *  v         fp16  [rows][d]     value cache, row-major.
+ *  v_cache   fp16                value cache, token-interleaved in groups of
+ *                                8: token t, dim m of sequence q = b*Hkv + h
+ *                                is the half at
+ *                                  (q*t_cap + (t/8)*8) * d + m*8 + t%8,
+ *                                so 8 consecutive tokens of one dim are one
+ *                                16-byte word (the matrix-core operand of the
+ *                                A.V product). Written by pot_store_values.
+ *                                t_cap must be a multiple of 8.
  *
  * Decoded key element (eq. pot and eq. mant):
  *    K^_m = s * sigma_m * (1 + j_m / 2^k) * 2^-e_m,   or 0 for the zero code.
@@ -139,6 +146,19 @@ pot_status pot_encode_keys(const pot_format* fmt, const uint16_t* k_fp16,
                            int32_t scale_mode, float* key_scale,
                            uint8_t* codes_se, uint8_t* codes_m, void* stream);
 
+/* Store fp16 values into the token-interleaved value cache.
+ *  v_fp16   [n_seq][n_tok][d] fp16, dense, device (token-major rows).
+ *  n_seq    sequences (b*Hkv + h order, consecutive from v_cache).
+ *  n_tok    tokens per sequence to write, at positions t0 .. t0+n_tok-1
+ *           (n_tok = 1 appends one decoded token).
+ *  t_cap    cache capacity per sequence, a positive multiple of 8.
+ *  Tokens outside [t0, t0+n_tok) are left untouched. Errors: negative sizes,
+ *  t_cap not a multiple of 8, the range outside [0, t_cap), NULL or
+ *  misaligned pointers (INVALID_ARG). */
+pot_status pot_store_values(const uint16_t* v_fp16, int64_t n_seq, int64_t n_tok,
+                            int64_t t_cap, int64_t t0, uint16_t* v_cache,
+                            void* stream);
+
 /* Workspace bytes pot_decode_attention needs for this problem shape (the
  * split partials and the split-completion counters). Host-only. Returns 0 for
  * invalid shapes. The same figure serves pot_int8_decode_attention and
@@ -159,8 +179,8 @@ pot_status pot_workspace_init(void* workspace, size_t ws_bytes, void* stream);
 
 /* Single-token decode attention with PoT keys (Sec. II-B, II-E, II-F).
  *  q            [B][Hq][d] fp32 query (post-RoPE).
- *  codes_se, codes_m, key_scale, v_fp16: cache as laid out above, t_cap rows
- *               per (b, kv-head) sequence.
+ *  codes_se, codes_m, key_scale, v_cache: cache as laid out above, t_cap
+ *               rows per (b, kv-head) sequence (t_cap a multiple of 8).
  *  kv_head_of_q HOST int32 [Hq]: kv head serving each query head (GQA). Every
  *               kv head must serve the same number G = Hq/Hkv of query heads,
  *               G in {1, 2, 4, 8}.
@@ -174,13 +194,14 @@ pot_status pot_workspace_init(void* workspace, size_t ws_bytes, void* stream);
  * shifts of q^ (eq. sac); x = acc * s * Delta * log2(e) * 2^-(F+k) / 8 in a
  * fixed fp32 order; the running maximum is the integer M = ceil(max x)
  * (eq. logsm) so rescales are exact powers of two; weights 2^(x-M) multiply
- * the fp16 V rows with fp32 accumulation; key splits are merged with exact
- * 2^(M_s - M) factors.
+ * the fp16 values with fp32 accumulation (matrix cores, weights split into
+ * fp16 high and low parts); key splits are merged with exact 2^(M_s - M)
+ * factors.
  */
 pot_status pot_decode_attention(const pot_format* fmt, const float* q,
                                 const uint8_t* codes_se,
                                 const uint8_t* codes_m, const float* key_scale,
-                                const uint16_t* v_fp16, int64_t t_cap,
+                                const uint16_t* v_cache, int64_t t_cap,
                                 const int32_t* kv_head_of_q, int32_t B,
                                 int32_t Hq, int32_t Hkv, int32_t T, float* out,
                                 void* workspace, size_t ws_bytes,
@@ -199,16 +220,16 @@ pot_status pot_int8_encode_keys(const uint16_t* k_fp16, int64_t n_rows,
  * (v_dot4), the same query quantiser, integer-M softmax and fp16 A.V. */
 pot_status pot_int8_decode_attention(
     const float* q, const int8_t* codes, const float* key_scale,
-    const uint16_t* v_fp16, int64_t t_cap, const int32_t* kv_head_of_q,
+    const uint16_t* v_cache, int64_t t_cap, const int32_t* kv_head_of_q,
     int32_t B, int32_t Hq, int32_t Hkv, int32_t T, int32_t hadamard,
     float* out, void* workspace, size_t ws_bytes, pot_debug* dbg,
     void* stream);
 
 /* Decode attention on an unquantised fp16 cache (the FP16 baseline of
  * Sec. IV): q is rounded to fp16, scores accumulate in fp32.
- *  k_fp16, v_fp16 [rows][d] fp16. */
+ *  k_fp16 [rows][d] fp16 row-major keys; v_cache as above. */
 pot_status pot_fp16_decode_attention(const float* q, const uint16_t* k_fp16,
-                                     const uint16_t* v_fp16, int64_t t_cap,
+                                     const uint16_t* v_cache, int64_t t_cap,
                                      const int32_t* kv_head_of_q, int32_t B,
                                      int32_t Hq, int32_t Hkv, int32_t T,
                                      float* out, void* workspace,

@@ -71,6 +71,7 @@ def _load_library():
         "pot_decode_workspace_bytes": (S, [i32, i32, i32, i32]),
         "pot_decode_workspace_bytes_for_splits": (S, [i32, i32, i32, i32, i32]),
         "pot_workspace_init": (i32, [P, S, P]),
+        "pot_store_values": (i32, [P, i64, i64, i64, i64, P, P]),
         "pot_decode_attention": (i32, [fmt_p, P, P, P, P, P, i64, P, i32, i32,
                                        i32, i32, P, P, S, dbg_p, P]),
         "pot_int8_encode_keys": (i32, [P, i64, i64, i32, P, P, P]),
@@ -146,6 +147,12 @@ def pot_workspace_init(workspace, ws_bytes: int | None = None, stream=None) -> N
     _check(_lib.pot_workspace_init(_ptr(workspace), nbytes, _stream(stream)))
 
 
+def pot_store_values(v_fp16, n_seq: int, n_tok: int, t_cap: int, t0: int, v_cache,
+                     stream=None) -> None:
+    _check(_lib.pot_store_values(_ptr(v_fp16), int(n_seq), int(n_tok), int(t_cap),
+                                 int(t0), _ptr(v_cache), _stream(stream)))
+
+
 def pot_encode_keys(fmt: pot_format, k_fp16, n_rows: int, out_row_stride: int,
                     scale_mode: int, key_scale, codes_se, codes_m=None,
                     stream=None) -> None:
@@ -210,6 +217,12 @@ def alloc_pot_cache(B: int, Hkv: int, t_cap: int, mant_bits: int, device):
           if mant_bits else None)
     sc = torch.zeros((B, Hkv, t_cap), dtype=torch.float32, device=device)
     return dict(codes_se=se, codes_m=cm, key_scale=sc)
+
+
+def alloc_value_cache(B: int, Hkv: int, t_cap: int, device):
+    """Value cache of B*Hkv sequences of t_cap tokens (token-interleaved)."""
+    import torch
+    return torch.zeros((B, Hkv, t_cap, HEAD_DIM), dtype=torch.float16, device=device)
 
 
 def alloc_workspace(nbytes: int, device):

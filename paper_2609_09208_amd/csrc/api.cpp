@@ -132,6 +132,9 @@ pot_status decode_common(int mode, int mant_bits, DecodeArgs& a, const int32_t* 
   if (!shape_ok(B, Hq, Hkv, T))
     return fail(POT_ERR_INVALID_ARG, "bad shape B=%d Hq=%d Hkv=%d T=%d", B, Hq, Hkv, T);
   if (t_cap < T) return fail(POT_ERR_INVALID_ARG, "T %d > t_cap %lld", T, (long long)t_cap);
+  if (t_cap % 8)
+    return fail(POT_ERR_INVALID_ARG, "t_cap %lld is not a multiple of 8 (value-cache groups)",
+                (long long)t_cap);
   if (!a.q || !a.v || !a.out) return fail(POT_ERR_INVALID_ARG, "q, v or out is NULL");
   if (!aligned(a.q, 16) || !aligned(a.v, 16) || !aligned(a.out, 16))
     return fail(POT_ERR_INVALID_ARG, "q, v and out must be 16-byte aligned");
@@ -224,6 +227,26 @@ pot_status pot_encode_keys(const pot_format* fmt, const uint16_t* k_fp16, int64_
                     "encode launch");
 }
 
+pot_status pot_store_values(const uint16_t* v_fp16, int64_t n_seq, int64_t n_tok, int64_t t_cap,
+                            int64_t t0, uint16_t* v_cache, void* stream) {
+  if (n_seq < 0 || n_tok < 0)
+    return fail(POT_ERR_INVALID_ARG, "n_seq %lld / n_tok %lld < 0", (long long)n_seq,
+                (long long)n_tok);
+  if (t_cap < 8 || t_cap % 8)
+    return fail(POT_ERR_INVALID_ARG, "t_cap %lld is not a positive multiple of 8",
+                (long long)t_cap);
+  if (t0 < 0 || t0 + n_tok > t_cap)
+    return fail(POT_ERR_INVALID_ARG, "tokens [%lld, %lld) outside [0, t_cap = %lld)",
+                (long long)t0, (long long)(t0 + n_tok), (long long)t_cap);
+  if (n_seq == 0 || n_tok == 0) return ok();
+  if (!v_fp16 || !v_cache) return fail(POT_ERR_INVALID_ARG, "v_fp16 or v_cache is NULL");
+  if (!aligned(v_fp16, 16) || !aligned(v_cache, 16))
+    return fail(POT_ERR_INVALID_ARG, "v_fp16 and v_cache must be 16-byte aligned");
+  return hip_status(launch_store_values(v_fp16, n_seq, n_tok, t_cap, t0, v_cache,
+                                        static_cast<hipStream_t>(stream)),
+                    "store values launch");
+}
+
 size_t pot_decode_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv, int32_t T) {
   if (!shape_ok(B, Hq, Hkv, T)) return 0;
   const Plan p = plan_splits(B, Hkv, T, 0);
@@ -245,7 +268,7 @@ pot_status pot_workspace_init(void* workspace, size_t ws_bytes, void* stream) {
 
 pot_status pot_decode_attention(const pot_format* fmt, const float* q, const uint8_t* codes_se,
                                 const uint8_t* codes_m, const float* key_scale,
-                                const uint16_t* v_fp16, int64_t t_cap,
+                                const uint16_t* v_cache, int64_t t_cap,
                                 const int32_t* kv_head_of_q, int32_t B, int32_t Hq, int32_t Hkv,
                                 int32_t T, float* out, void* workspace, size_t ws_bytes,
                                 pot_debug* dbg, void* stream) {
@@ -261,7 +284,7 @@ pot_status pot_decode_attention(const pot_format* fmt, const float* q, const uin
   a.codes_se = codes_se;
   a.codes_m = codes_m;
   a.key_scale = key_scale;
-  a.v = v_fp16;
+  a.v = v_cache;
   a.out = out;
   a.frac_bits = fmt->frac_bits;
   a.hadamard = fmt->hadamard;
@@ -287,7 +310,7 @@ pot_status pot_int8_encode_keys(const uint16_t* k_fp16, int64_t n_rows, int64_t 
 }
 
 pot_status pot_int8_decode_attention(const float* q, const int8_t* codes, const float* key_scale,
-                                     const uint16_t* v_fp16, int64_t t_cap,
+                                     const uint16_t* v_cache, int64_t t_cap,
                                      const int32_t* kv_head_of_q, int32_t B, int32_t Hq,
                                      int32_t Hkv, int32_t T, int32_t hadamard, float* out,
                                      void* workspace, size_t ws_bytes, pot_debug* dbg,
@@ -301,7 +324,7 @@ pot_status pot_int8_decode_attention(const float* q, const int8_t* codes, const 
   a.q = q;
   a.codes_i8 = codes;
   a.key_scale = key_scale;
-  a.v = v_fp16;
+  a.v = v_cache;
   a.out = out;
   a.hadamard = hadamard;
   return decode_common(kScoreInt8, 0, a, kv_head_of_q, B, Hq, Hkv, T, t_cap, workspace, ws_bytes,
@@ -309,7 +332,7 @@ pot_status pot_int8_decode_attention(const float* q, const int8_t* codes, const 
 }
 
 pot_status pot_fp16_decode_attention(const float* q, const uint16_t* k_fp16,
-                                     const uint16_t* v_fp16, int64_t t_cap,
+                                     const uint16_t* v_cache, int64_t t_cap,
                                      const int32_t* kv_head_of_q, int32_t B, int32_t Hq,
                                      int32_t Hkv, int32_t T, float* out, void* workspace,
                                      size_t ws_bytes, void* stream) {
@@ -318,7 +341,7 @@ pot_status pot_fp16_decode_attention(const float* q, const uint16_t* k_fp16,
   DecodeArgs a{};
   a.q = q;
   a.k_f16 = k_fp16;
-  a.v = v_fp16;
+  a.v = v_cache;
   a.out = out;
   return decode_common(kScoreFp16, 0, a, kv_head_of_q, B, Hq, Hkv, T, t_cap, workspace, ws_bytes,
                        nullptr, stream);

@@ -1,30 +1,39 @@
 // Split-K decode attention for gfx950 over a PoT / INT8 / fp16 key cache.
 //
-// Grid (n_splits, Hkv, B), 256 threads (4 wave64). A workgroup owns one key
-// range of one (batch, kv-head) sequence and all G query heads that share the
-// kv head (GQA), so every code byte and value byte is read from HBM once per
-// workgroup and reused G times.
+// Grid (n_splits, Hkv, B), 256 threads = 4 wave64. A workgroup owns one key
+// range of one (batch, kv-head) sequence and all G query heads sharing that
+// kv head (GQA), so every code and value byte is read from HBM once and used
+// G times. Inside the workgroup each wave streams its own 64-key tiles
+// (tile j of the range goes to wave j % 4) with the next tile's codes and
+// value fragments prefetched into registers while the current one is
+// processed; waves only meet at the end to merge their partial sums.
 //
-// Per tile of 256 keys:
-//  1. score: thread t owns key t. PoT (Sec. II-B eq. sac): the row's 32 code
-//     bytes arrive as two 16-byte loads; per element the exponent gives the
-//     funnel-shift amount sh = e + 25, so v_alignbit(q, 0, sh) = q << (7 - e)
-//     for e <= 6 and 0 for the zero code e = 7 (sh = 32 = 0 mod 32). The sign
-//     is applied as (t ^ s) + acc (v_xad_u32) with s in {0, -1}, and the
-//     missing +1 per negative element is added once per key from a popcount
-//     of the sign bits. Mantissa bit b of PoT-Mk adds alignbit(q << b, 0,
-//     sh & -bit). Every shift is a left shift (eq. exact) and the int32 sum is
-//     exact; it is taken at internal head-room 7 and rescaled exactly to F.
-//  2. log2 domain: x = fl32(fl32(float(acc) * s) * c), c = fl32(fl32(Delta *
-//     log2 e) * 2^-(F+k+3)), in this fixed fp32 order.
-//  3. integer running maximum M = max(M, ceil(max x)) per head (eq. logsm);
-//     a rise rescales the running sums by the exact power of two 2^(M_old -
-//     M_new).
-//  4. A.V: weights p = 2^(x - M) staged in LDS; thread (key group, 8 dims)
-//     streams 16-byte fp16 value loads and accumulates G x 8 fp32 sums.
-// After its range, a workgroup writes (M_s, l_s, o_s) per head; the last
-// workgroup of a (batch, kv-head) to finish (split-completion counter) merges
-// the splits with exact 2^(M_s - M) weights and resets the counter.
+// Per 64-key tile and wave:
+//  1. Scores, one key per lane (Sec. II-B eq. sac). PoT-4: the key's 32 code
+//     bytes arrive as two 16-byte loads. Each exponent e gives a funnel-shift
+//     amount sh = e + 25, so v_alignbit(q, 0, sh) = q << (7 - e) for e <= 6
+//     and 0 for the zero code e = 7 (sh = 32 = 0 mod 32); every shift is a
+//     left shift (eq. exact). Two query heads share one 32-bit register as
+//     q_a + 2^16 q_b, so one alignbit shifts both; v_xad_u32 applies the sign
+//     as (t ^ s) + acc with s in {0, -1}, and the missing +1 per negative
+//     element is added once per key from a popcount of the sign bits. After
+//     every 2 elements the 16-bit fields (each at most 2 * 127 * 2^7 in
+//     magnitude, kept non-negative by a 2^15 bias) are added into two int32
+//     accumulators by SDWA word adds, so the sums stay exact. PoT-Mk and the
+//     single-head case use one int32 accumulator per head with one more
+//     alignbit per mantissa bit.
+//  2. x = fl32(fl32(float(acc) * s) * c), c = fl32(fl32(Delta * log2 e) *
+//     2^-(F+k+3)) in this order; x is staged transposed in wave-private LDS.
+//  3. Integer running maximum M = max(M, ceil(max x)) per head (eq. logsm);
+//     when it rises the accumulators are rescaled by the exact power of two
+//     2^(M_old - M_new).
+//  4. A.V on the matrix cores: P (16 rows = 8 heads x {fp16 high part, fp16
+//     low part} of p = 2^(x - M + 12)) times V (fp16) with
+//     v_mfma_f32_16x16x32_f16, fp32 accumulation; a fifth column block of
+//     ones yields the row sums l. The value cache is stored token-interleaved
+//     ([t/8][d][t%8]) so a lane's 16-byte load is exactly its B fragment.
+// The last workgroup of a (batch, kv-head) to finish (completion counter)
+// merges the key splits with exact 2^(M_s - M) weights.
 #include <hip/hip_fp16.h>
 
 #include <climits>
@@ -34,57 +43,183 @@
 
 namespace potattn {
 
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef _Float16 half2v __attribute__((ext_vector_type(2)));
+typedef float float4v __attribute__((ext_vector_type(4)));
+
+constexpr int kWaves = kBlock / 64;
+constexpr int kWTile = 64;    // keys per wave tile
+constexpr int kXRow = 68;     // floats per head row of the transposed score tile
+constexpr float kPScale = 12.0f;  // p is formed as 2^(x - M + 12) (fp16-normal range)
+
+// ---- VALU forms the compiler does not pick by itself ------------------------
+__device__ __forceinline__ uint32_t xad_u32(uint32_t a, uint32_t b, uint32_t c) {
+  uint32_t r;
+  asm("v_xad_u32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+// acc + (p & 0xffff)
+__device__ __forceinline__ uint32_t add_lo16(uint32_t acc, uint32_t p) {
+  uint32_t r;
+  asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 "
+      "src1_sel:DWORD"
+      : "=v"(r)
+      : "v"(p), "v"(acc));
+  return r;
+}
+// acc + sign_extend(p >> 16)
+__device__ __forceinline__ uint32_t add_hi16s(uint32_t acc, uint32_t p) {
+  uint32_t r;
+  asm("v_add_u32_sdwa %0, sext(%1), %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_1 "
+      "src1_sel:DWORD"
+      : "=v"(r)
+      : "v"(p), "v"(acc));
+  return r;
+}
+
+__device__ __forceinline__ void wave_sync_lds() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// ---- per-tile register payloads -----------------------------------------------
+template <int MODE, int K>
+struct KeyRegs;
+template <int K>
+struct KeyRegs<kScorePot, K> {
+  uint4 c0, c1;
+  uint2 pl[K > 0 ? K : 1];
+  float s;
+};
+template <int K>
+struct KeyRegs<kScoreInt8, K> {
+  int4 k[4];
+  float s;
+};
+template <int K>
+struct KeyRegs<kScoreFp16, K> {
+  uint4 k[8];
+};
+
+struct ValRegs {
+  uint4 f[2][4];  // [K-block of 32 keys][16-dim block]
+};
 
 template <int MODE, int K>
-struct QLayout {
-  // 32-bit query words per element-group and head held in LDS.
-  static constexpr int kWords = MODE == kScorePot ? (K + 1) * kDim
-                                : MODE == kScoreInt8 ? kDim / 4
-                                                     : kDim / 2;
+__device__ __forceinline__ void load_keys(const DecodeArgs& a, int64_t row, bool valid,
+                                          KeyRegs<MODE, K>& r) {
+  if constexpr (MODE == kScorePot) {
+    if (valid) {
+      const uint4* cp = reinterpret_cast<const uint4*>(a.codes_se + row * (kDim / 2));
+      r.c0 = cp[0];
+      r.c1 = cp[1];
+#pragma unroll
+      for (int bb = 0; bb < K; ++bb)
+        r.pl[bb] = reinterpret_cast<const uint2*>(a.codes_m + row * 8 * K)[bb];
+      r.s = a.key_scale[row];
+    } else {
+      r.c0 = r.c1 = make_uint4(0x77777777u, 0x77777777u, 0x77777777u, 0x77777777u);
+#pragma unroll
+      for (int bb = 0; bb < K; ++bb) r.pl[bb] = make_uint2(0u, 0u);
+      r.s = 0.0f;
+    }
+  } else if constexpr (MODE == kScoreInt8) {
+    const int4* kp = reinterpret_cast<const int4*>(a.codes_i8 + row * kDim);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) r.k[i] = valid ? kp[i] : make_int4(0, 0, 0, 0);
+    r.s = valid ? a.key_scale[row] : 0.0f;
+  } else {
+    const uint4* kp = reinterpret_cast<const uint4*>(a.k_f16 + row * kDim);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) r.k[i] = valid ? kp[i] : make_uint4(0u, 0u, 0u, 0u);
+  }
+}
+
+// B fragments of one 64-key tile: lane l takes keys t0 + 32*kb + 8*(l/16) ..+7
+// of dim 16*nb + l%16, one 16-byte load each from the token-interleaved cache.
+__device__ __forceinline__ void load_values(const uint16_t* vseq, int t0, int t_end, int lane,
+                                            ValRegs& v) {
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    const int g8 = t0 + 32 * kb + 8 * (lane >> 4);
+    const bool ok = g8 < t_end;
+    const uint4* base = reinterpret_cast<const uint4*>(vseq + (int64_t)g8 * kDim);
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb)
+      v.f[kb][nb] = ok ? base[nb * 16 + (lane & 15)] : make_uint4(0u, 0u, 0u, 0u);
+    if (ok && g8 + 8 > t_end) {  // tail group: zero tokens at or past t_end
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) {
+        uint32_t w4[4] = {v.f[kb][nb].x, v.f[kb][nb].y, v.f[kb][nb].z, v.f[kb][nb].w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const uint32_t lo = (g8 + 2 * i < t_end) ? 0x0000FFFFu : 0u;
+          const uint32_t hi = (g8 + 2 * i + 1 < t_end) ? 0xFFFF0000u : 0u;
+          w4[i] &= lo | hi;
+        }
+        v.f[kb][nb] = make_uint4(w4[0], w4[1], w4[2], w4[3]);
+      }
+    }
+  }
+}
+
+// ---- shared memory -------------------------------------------------------------
+template <int MODE, int G, int K>
+struct Smem {
+  static constexpr bool kPacked = MODE == kScorePot && K == 0 && G >= 2;
+  static constexpr int NP = G / 2;
+  static constexpr int kQWords = MODE == kScorePot ? (kPacked ? kDim * (NP > 0 ? NP : 1)
+                                                              : (K + 1) * kDim * G)
+                                 : MODE == kScoreInt8 ? (kDim / 4) * G
+                                                      : (kDim / 2) * G;
+  int32_t q[kQWords];          // PoT packed: [m][pair]; PoT: [b'*64+m][h]; INT8/fp16: [i][h]
+  int32_t qh[G * kDim];        // quantised query per head (prologue staging)
+  float c[G];                  // per-head factor of the log2-domain score
+  float x[kWaves][8][kXRow];   // transposed score tile per wave
+  float wo[kWaves][16][kDim];  // per-wave P.V (rows: heads x {hi, lo})
+  float wl[kWaves][16];
+  int wm[kWaves][8];
+  int last;
 };
 
 template <int MODE, int G, int K, bool DEBUG>
 __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a) {
-  constexpr int NQW = QLayout<MODE, K>::kWords;
-  __shared__ int32_t s_q[NQW][G];
-  __shared__ float s_c[G];
-  __shared__ float s_x[kTile][G];
-  __shared__ float s_red[4][G];
-  __shared__ float s_o[4][G][kDim];
-  __shared__ float s_l[4][G];
-  __shared__ int s_m[G];
-  __shared__ int s_last;
+  using S = Smem<MODE, G, K>;
+  __shared__ S sm;
+  constexpr bool kPacked = S::kPacked;
+  constexpr int NP = S::NP;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
-  const int64_t row0 = ((int64_t)b * a.Hkv + kvh) * a.t_cap;
+  const int64_t seq = (int64_t)b * a.Hkv + kvh;
+  const int64_t row0 = seq * a.t_cap;
+  const uint16_t* vseq = a.v + row0 * kDim;
 
-  // ---- prologue: rotate and quantise this kv head's G query vectors ------
-  for (int h = wave; h < G; h += 4) {
+  // ---- prologue: rotate and quantise this kv head's G query vectors --------
+  for (int h = wave; h < G; h += kWaves) {
     const int64_t bq = (int64_t)b * a.Hq + a.q_of_kv[kvh * G + h];
     float qv = a.q[bq * kDim + lane];
     if constexpr (MODE == kScoreFp16) {
       const uint32_t bits = __half_as_ushort(__float2half_rn(qv));
       const uint32_t other = __shfl_xor(bits, 1, 64);
-      if ((lane & 1) == 0) s_q[lane >> 1][h] = (int32_t)(bits | (other << 16));
-      if (lane == 0) s_c[h] = __fmul_rn(log2e_f32(), 0.125f);
+      if ((lane & 1) == 0) sm.q[(lane >> 1) * G + h] = (int32_t)(bits | (other << 16));
+      if (lane == 0) sm.c[h] = __fmul_rn(log2e_f32(), 0.125f);
     } else {
       if (a.hadamard) qv = (float)(wave_fwht64((double)qv) * 0.125);
       float step;
       const int qi = wave_quantize_int8(qv, &step);
+      sm.qh[h * kDim + lane] = qi;
       if constexpr (MODE == kScorePot) {
-#pragma unroll
-        for (int bb = 0; bb <= K; ++bb) s_q[bb * kDim + lane][h] = qi * (1 << bb);
         if (lane == 0)
-          s_c[h] = __fmul_rn(__fmul_rn(step, log2e_f32()),
-                             __builtin_amdgcn_ldexpf(1.0f, -(a.frac_bits + K + 3)));
+          sm.c[h] = __fmul_rn(__fmul_rn(step, log2e_f32()),
+                              __builtin_amdgcn_ldexpf(1.0f, -(a.frac_bits + K + 3)));
       } else {
         uint32_t word = (uint32_t)(qi & 0xFF) << (8 * (lane & 3));
         word |= __shfl_xor(word, 1, 64);
         word |= __shfl_xor(word, 2, 64);
-        if ((lane & 3) == 0) s_q[lane >> 2][h] = (int32_t)word;
-        if (lane == 0) s_c[h] = __fmul_rn(__fmul_rn(step, log2e_f32()), 0.125f);
+        if ((lane & 3) == 0) sm.q[(lane >> 2) * G + h] = (int32_t)word;
+        if (lane == 0) sm.c[h] = __fmul_rn(__fmul_rn(step, log2e_f32()), 0.125f);
       }
       if constexpr (DEBUG) {
         if (split == 0) {
@@ -95,40 +230,106 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a) {
     }
   }
   __syncthreads();
-
-  const int t_begin = split * a.split_len;
-  const int t_end = min(a.T, t_begin + a.split_len);
-  const int kg = tid >> 3, d8 = tid & 7;
-
-  int m_run[G];
-  float l_acc[G], o_acc[G][8];
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    m_run[h] = INT_MIN;
-    l_acc[h] = 0.0f;
-#pragma unroll
-    for (int dd = 0; dd < 8; ++dd) o_acc[h][dd] = 0.0f;
+  if constexpr (MODE == kScorePot) {
+    if constexpr (kPacked) {
+      // pair p holds heads 2p (low field) and 2p+1 (high field) as one integer
+      for (int i = tid; i < kDim * NP; i += kBlock) {
+        const int m = i / NP, p = i % NP;
+        sm.q[i] = (int32_t)((uint32_t)sm.qh[(2 * p) * kDim + m] +
+                            ((uint32_t)sm.qh[(2 * p + 1) * kDim + m] << 16));
+      }
+    } else {
+      for (int i = tid; i < (K + 1) * kDim * G; i += kBlock) {
+        const int h = i % G, bm = i / G, bb = bm / kDim, m = bm % kDim;
+        sm.q[i] = sm.qh[h * kDim + m] * (1 << bb);
+      }
+    }
+    __syncthreads();
   }
 
-  for (int tile = t_begin; tile < t_end; tile += kTile) {
-    const int t = tile + tid;
+  // ---- per-wave streaming over 64-key tiles ------------------------------------
+  const int t_begin = split * a.split_len;
+  const int t_end = min(a.T, t_begin + a.split_len);
+  const int n_tiles = (t_end - t_begin + kWTile - 1) / kWTile;
+  const int row = lane & 15, grp = lane >> 4, hrow = row & 7, part = row >> 3;
+  const bool hvalid = hrow < G;
+
+  float4v acc[5];
+#pragma unroll
+  for (int nb = 0; nb < 5; ++nb) acc[nb] = float4v{0.0f, 0.0f, 0.0f, 0.0f};
+  int m_run = INT_MIN;
+  half8 ones;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) ones[i] = (_Float16)1.0f;
+
+  KeyRegs<MODE, K> kr[2];
+  ValRegs vr[2];
+  int j = wave;
+  if (j < n_tiles) {
+    const int t0 = t_begin + kWTile * j;
+    load_keys<MODE, K>(a, row0 + t0 + lane, t0 + lane < t_end, kr[0]);
+    load_values(vseq, t0, t_end, lane, vr[0]);
+  }
+
+  auto process = [&](const KeyRegs<MODE, K>& ks, const ValRegs& vs, int t0) {
+    const int t = t0 + lane;
+    const bool kvalid = t < t_end;
     float xs[G];
-    if (t < t_end) {
-      const int64_t row = row0 + t;
-      if constexpr (MODE == kScorePot) {
-        const uint4* cp = reinterpret_cast<const uint4*>(a.codes_se + row * (kDim / 2));
-        const uint4 c0 = cp[0], c1 = cp[1];
-        const uint32_t w[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
-        uint64_t pl[K > 0 ? K : 1];
+    // ---- 1. scores (lane = key) ----
+    if constexpr (MODE == kScorePot) {
+      const uint32_t w[8] = {ks.c0.x, ks.c0.y, ks.c0.z, ks.c0.w,
+                             ks.c1.x, ks.c1.y, ks.c1.z, ks.c1.w};
+      int nneg = 0;
 #pragma unroll
-        for (int bb = 0; bb < K; ++bb)
-          pl[bb] = reinterpret_cast<const uint64_t*>(a.codes_m + row * 8 * K)[bb];
-        int nneg = 0;
+      for (int i = 0; i < 8; ++i) nneg += __popc(w[i] & 0x88888888u);
+      int32_t accv[G];
+      if constexpr (kPacked) {
+        uint32_t accA[NP], accB[NP];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) nneg += __popc(w[i] & 0x88888888u);
-        uint32_t acc[G];
+        for (int p = 0; p < NP; ++p) accA[p] = accB[p] = 0u;
+        const uint4* qp4 = reinterpret_cast<const uint4*>(sm.q);
 #pragma unroll
-        for (int h = 0; h < G; ++h) acc[h] = 0u;
+        for (int i = 0; i < 8; ++i) {
+          const uint32_t e0 = (w[i] & 0x07070707u) + 0x19191919u;
+          const uint32_t e1 = ((w[i] >> 4) & 0x07070707u) + 0x19191919u;
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj) {
+            uint32_t P[NP];
+#pragma unroll
+            for (int p = 0; p < NP; ++p) P[p] = 0x8000u;
+#pragma unroll
+            for (int hf = 0; hf < 2; ++hf) {
+              const int m = 8 * i + 2 * jj + hf;
+              const uint32_t sh = (hf ? e1 : e0) >> (8 * jj);
+              const uint32_t sgn = (uint32_t)((int32_t)(w[i] << (28 - 4 * (2 * jj + hf))) >> 31);
+              uint32_t qq[4];
+              if constexpr (NP == 4) {
+                const uint4 q4 = qp4[m];
+                qq[0] = q4.x; qq[1] = q4.y; qq[2] = q4.z; qq[3] = q4.w;
+              } else {
+#pragma unroll
+                for (int p = 0; p < NP; ++p) qq[p] = (uint32_t)sm.q[m * NP + p];
+              }
+#pragma unroll
+              for (int p = 0; p < NP; ++p)
+                P[p] = xad_u32(__builtin_amdgcn_alignbit(qq[p], 0u, sh), sgn, P[p]);
+            }
+#pragma unroll
+            for (int p = 0; p < NP; ++p) {
+              accA[p] = add_lo16(accA[p], P[p]);
+              accB[p] = add_hi16s(accB[p], P[p]);
+            }
+          }
+        }
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+          accv[2 * p] = (int32_t)(accA[p] - 32u * 0x8000u + (uint32_t)nneg);
+          accv[2 * p + 1] = (int32_t)accB[p];
+        }
+      } else {
+        uint32_t accu[G];
+#pragma unroll
+        for (int h = 0; h < G; ++h) accu[h] = 0u;
 #pragma unroll
         for (int m = 0; m < kDim; ++m) {
           const uint32_t word = w[m >> 3];
@@ -137,213 +338,234 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a) {
           const uint32_t sgn = (uint32_t)((int32_t)(word << (28 - pos)) >> 31);
           uint32_t shb[K > 0 ? K : 1];
 #pragma unroll
-          for (int bb = 0; bb < K; ++bb)
-            shb[bb] = sh & (uint32_t)(-(int32_t)((pl[bb] >> m) & 1u));
+          for (int bb = 0; bb < K; ++bb) {
+            const uint32_t plw = (m < 32) ? ks.pl[bb].x : ks.pl[bb].y;
+            shb[bb] = sh & (uint32_t)((int32_t)(plw << (31 - (m & 31))) >> 31);
+          }
 #pragma unroll
           for (int h = 0; h < G; ++h) {
-            uint32_t term = __builtin_amdgcn_alignbit((uint32_t)s_q[K * kDim + m][h], 0u, sh);
+            uint32_t term = __builtin_amdgcn_alignbit((uint32_t)sm.q[(K * kDim + m) * G + h], 0u, sh);
 #pragma unroll
             for (int bb = 0; bb < K; ++bb)
-              term += __builtin_amdgcn_alignbit((uint32_t)s_q[bb * kDim + m][h], 0u, shb[bb]);
-            acc[h] = (term ^ sgn) + acc[h];
+              term += __builtin_amdgcn_alignbit((uint32_t)sm.q[(bb * kDim + m) * G + h], 0u, shb[bb]);
+            accu[h] = xad_u32(term, sgn, accu[h]);
           }
         }
-        const float s = a.key_scale[row];
 #pragma unroll
-        for (int h = 0; h < G; ++h) {
-          int32_t v = (int32_t)(acc[h] + (uint32_t)nneg);
-          v = a.frac_bits >= kFInt ? (int32_t)((uint32_t)v << (a.frac_bits - kFInt))
-                                   : (v >> (kFInt - a.frac_bits));
-          xs[h] = __fmul_rn(__fmul_rn((float)v, s), s_c[h]);
-          if constexpr (DEBUG) {
-            if (a.dbg_scores)
-              a.dbg_scores[((int64_t)b * a.Hq + a.q_of_kv[kvh * G + h]) * a.T + t] = v;
-          }
+        for (int h = 0; h < G; ++h) accv[h] = (int32_t)(accu[h] + (uint32_t)nneg);
+      }
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        int32_t v = accv[h];
+        v = a.frac_bits >= kFInt ? (int32_t)((uint32_t)v << (a.frac_bits - kFInt))
+                                 : (v >> (kFInt - a.frac_bits));
+        xs[h] = kvalid ? __fmul_rn(__fmul_rn((float)v, ks.s), sm.c[h]) : -INFINITY;
+        if constexpr (DEBUG) {
+          if (a.dbg_scores && kvalid)
+            a.dbg_scores[((int64_t)b * a.Hq + a.q_of_kv[kvh * G + h]) * a.T + t] = v;
         }
-      } else if constexpr (MODE == kScoreInt8) {
-        const int4* kp = reinterpret_cast<const int4*>(a.codes_i8 + row * kDim);
-        int32_t kw[16];
+      }
+    } else if constexpr (MODE == kScoreInt8) {
+      int32_t kw[16];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int4 v4 = kp[i];
-          kw[4 * i] = v4.x;
-          kw[4 * i + 1] = v4.y;
-          kw[4 * i + 2] = v4.z;
-          kw[4 * i + 3] = v4.w;
+      for (int i = 0; i < 4; ++i) {
+        kw[4 * i] = ks.k[i].x;
+        kw[4 * i + 1] = ks.k[i].y;
+        kw[4 * i + 2] = ks.k[i].z;
+        kw[4 * i + 3] = ks.k[i].w;
+      }
+      int32_t accd[G];
+#pragma unroll
+      for (int h = 0; h < G; ++h) accd[h] = 0;
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+#pragma unroll
+        for (int h = 0; h < G; ++h)
+          accd[h] = __builtin_amdgcn_sdot4(sm.q[i * G + h], kw[i], accd[h], false);
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        xs[h] = kvalid ? __fmul_rn(__fmul_rn((float)accd[h], ks.s), sm.c[h]) : -INFINITY;
+        if constexpr (DEBUG) {
+          if (a.dbg_scores && kvalid)
+            a.dbg_scores[((int64_t)b * a.Hq + a.q_of_kv[kvh * G + h]) * a.T + t] = accd[h];
         }
-        int32_t acc[G];
-#pragma unroll
-        for (int h = 0; h < G; ++h) acc[h] = 0;
-#pragma unroll
-        for (int i = 0; i < 16; ++i)
-#pragma unroll
-          for (int h = 0; h < G; ++h) acc[h] = __builtin_amdgcn_sdot4(s_q[i][h], kw[i], acc[h], false);
-        const float s = a.key_scale[row];
-#pragma unroll
-        for (int h = 0; h < G; ++h) {
-          xs[h] = __fmul_rn(__fmul_rn((float)acc[h], s), s_c[h]);
-          if constexpr (DEBUG) {
-            if (a.dbg_scores)
-              a.dbg_scores[((int64_t)b * a.Hq + a.q_of_kv[kvh * G + h]) * a.T + t] = acc[h];
-          }
-        }
-      } else {
-        const uint4* kp = reinterpret_cast<const uint4*>(a.k_f16 + row * kDim);
-        uint32_t kw[32];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const uint4 v4 = kp[i];
-          kw[4 * i] = v4.x;
-          kw[4 * i + 1] = v4.y;
-          kw[4 * i + 2] = v4.z;
-          kw[4 * i + 3] = v4.w;
-        }
-        float dot[G];
-#pragma unroll
-        for (int h = 0; h < G; ++h) dot[h] = 0.0f;
-#pragma unroll
-        for (int i = 0; i < 32; ++i)
-#pragma unroll
-          for (int h = 0; h < G; ++h)
-            dot[h] = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2v, s_q[i][h]),
-                                            __builtin_bit_cast(half2v, kw[i]), dot[h], false);
-#pragma unroll
-        for (int h = 0; h < G; ++h) xs[h] = __fmul_rn(dot[h], s_c[h]);
       }
     } else {
+      uint32_t kw[32];
 #pragma unroll
-      for (int h = 0; h < G; ++h) xs[h] = -INFINITY;
+      for (int i = 0; i < 8; ++i) {
+        kw[4 * i] = ks.k[i].x;
+        kw[4 * i + 1] = ks.k[i].y;
+        kw[4 * i + 2] = ks.k[i].z;
+        kw[4 * i + 3] = ks.k[i].w;
+      }
+      float dot[G];
+#pragma unroll
+      for (int h = 0; h < G; ++h) dot[h] = 0.0f;
+#pragma unroll
+      for (int i = 0; i < 32; ++i)
+#pragma unroll
+        for (int h = 0; h < G; ++h)
+          dot[h] = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2v, sm.q[i * G + h]),
+                                          __builtin_bit_cast(half2v, kw[i]), dot[h], false);
+#pragma unroll
+      for (int h = 0; h < G; ++h) xs[h] = kvalid ? __fmul_rn(dot[h], sm.c[h]) : -INFINITY;
     }
 
-    // tile maximum per head
+    // ---- 2. transpose through wave-private LDS ----
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const float mx = wave_max(xs[h]);
-      if (lane == 0) s_red[wave][h] = mx;
-    }
-    __syncthreads();
-    float scale[G];
+    for (int h = 0; h < G; ++h) sm.x[wave][h][lane] = xs[h];
+    wave_sync_lds();
+    float xv[2][8];
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const float mt = fmaxf(fmaxf(s_red[0][h], s_red[1][h]), fmaxf(s_red[2][h], s_red[3][h]));
-      const int m_new = max(m_run[h], (int)ceilf(mt));
-      scale[h] = m_run[h] == INT_MIN ? 0.0f : __builtin_amdgcn_ldexpf(1.0f, m_run[h] - m_new);
-      m_run[h] = m_new;
-    }
-    // weights of this thread's own key
+    for (int kb = 0; kb < 2; ++kb) {
+      if (hvalid) {
+        const float4* src = reinterpret_cast<const float4*>(&sm.x[wave][hrow][32 * kb + 8 * grp]);
+        const float4 u0 = src[0], u1 = src[1];
+        xv[kb][0] = u0.x; xv[kb][1] = u0.y; xv[kb][2] = u0.z; xv[kb][3] = u0.w;
+        xv[kb][4] = u1.x; xv[kb][5] = u1.y; xv[kb][6] = u1.z; xv[kb][7] = u1.w;
+      } else {
 #pragma unroll
-    for (int h = 0; h < G; ++h)
-      s_x[tid][h] = (t < t_end) ? __builtin_amdgcn_exp2f(xs[h] - (float)m_run[h]) : 0.0f;
-    __syncthreads();
-
-    // A.V: thread (kg, d8) takes keys kg, kg+32, ... and dims 8*d8 .. 8*d8+7
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      l_acc[h] *= scale[h];
-#pragma unroll
-      for (int dd = 0; dd < 8; ++dd) o_acc[h][dd] *= scale[h];
-    }
-#pragma unroll 2
-    for (int i = 0; i < kTile / 32; ++i) {
-      const int tl = kg + 32 * i;
-      if (tile + tl < t_end) {
-        const uint4 vv = *reinterpret_cast<const uint4*>(a.v + (row0 + tile + tl) * kDim + 8 * d8);
-        const uint32_t vw[4] = {vv.x, vv.y, vv.z, vv.w};
-        float vf[8];
-#pragma unroll
-        for (int i2 = 0; i2 < 4; ++i2) {
-          const half2v hv = __builtin_bit_cast(half2v, vw[i2]);
-          vf[2 * i2] = (float)hv.x;
-          vf[2 * i2 + 1] = (float)hv.y;
-        }
-#pragma unroll
-        for (int h = 0; h < G; ++h) {
-          const float p = s_x[tl][h];
-          l_acc[h] += p;
-#pragma unroll
-          for (int dd = 0; dd < 8; ++dd) o_acc[h][dd] = fmaf(p, vf[dd], o_acc[h][dd]);
-        }
+        for (int i = 0; i < 8; ++i) xv[kb][i] = -INFINITY;
       }
     }
-    __syncthreads();
+    wave_sync_lds();  // the tile buffer is rewritten by the next tile
+
+    // ---- 3. integer running maximum per head ----
+    float mx = xv[0][0];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) mx = fmaxf(mx, xv[kb][i]);
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const int mt = hvalid ? (int)ceilf(mx) : INT_MIN;
+    const int m_new = max(m_run, mt);
+    if (__any(m_new != m_run)) {
+      const float f = (m_run == INT_MIN) ? 0.0f : __builtin_amdgcn_ldexpf(1.0f, m_run - m_new);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float fr = __shfl(f, 4 * grp + r, 64);
+#pragma unroll
+        for (int nb = 0; nb < 5; ++nb) acc[nb][r] *= fr;
+      }
+    }
+    m_run = m_new;
+
+    // ---- 4. weights (fp16 high / low parts) and P.V on the matrix cores ----
+    const float bias = hvalid ? kPScale - (float)m_run : 0.0f;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      half8 af;
+#pragma unroll
+      for (int i = 0; i < 8; i += 2) {
+        const float p0 = __builtin_amdgcn_exp2f(xv[kb][i] + bias);
+        const float p1 = __builtin_amdgcn_exp2f(xv[kb][i + 1] + bias);
+        const half2v hi = __builtin_bit_cast(half2v, __builtin_amdgcn_cvt_pkrtz(p0, p1));
+        const half2v lo = __builtin_bit_cast(
+            half2v, __builtin_amdgcn_cvt_pkrtz(p0 - (float)hi.x, p1 - (float)hi.y));
+        const half2v sel = part ? lo : hi;
+        af[i] = sel.x;
+        af[i + 1] = sel.y;
+      }
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb)
+        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+            af, __builtin_bit_cast(half8, vs.f[kb][nb]), acc[nb], 0, 0, 0);
+      acc[4] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af, ones, acc[4], 0, 0, 0);
+    }
+  };
+
+  for (; j < n_tiles; j += 2 * kWaves) {
+    const int j1 = j + kWaves;
+    if (j1 < n_tiles) {
+      const int t1 = t_begin + kWTile * j1;
+      load_keys<MODE, K>(a, row0 + t1 + lane, t1 + lane < t_end, kr[1]);
+      load_values(vseq, t1, t_end, lane, vr[1]);
+    }
+    process(kr[0], vr[0], t_begin + kWTile * j);
+    if (j1 >= n_tiles) break;
+    const int j2 = j1 + kWaves;
+    if (j2 < n_tiles) {
+      const int t2 = t_begin + kWTile * j2;
+      load_keys<MODE, K>(a, row0 + t2 + lane, t2 + lane < t_end, kr[0]);
+      load_values(vseq, t2, t_end, lane, vr[0]);
+    }
+    process(kr[1], vr[1], t_begin + kWTile * j1);
   }
 
-  // ---- reduce this workgroup's partial sums over key groups --------------
+  // ---- merge the four waves ---------------------------------------------------
 #pragma unroll
-  for (int h = 0; h < G; ++h) {
+  for (int r = 0; r < 4; ++r) {
 #pragma unroll
-    for (int dd = 0; dd < 8; ++dd) {
-      float v = o_acc[h][dd];
-      v += __shfl_xor(v, 8, 64);
-      v += __shfl_xor(v, 16, 64);
-      v += __shfl_xor(v, 32, 64);
-      if (lane < 8) s_o[wave][h][8 * lane + dd] = v;
-    }
-    float l = l_acc[h];
-    l += __shfl_xor(l, 8, 64);
-    l += __shfl_xor(l, 16, 64);
-    l += __shfl_xor(l, 32, 64);
-    if (lane == 0) s_l[wave][h] = l;
+    for (int nb = 0; nb < 4; ++nb) sm.wo[wave][4 * grp + r][16 * nb + row] = acc[nb][r];
+    if (row == 0) sm.wl[wave][4 * grp + r] = acc[4][r];
   }
-  if (tid == 0) {
-#pragma unroll
-    for (int h = 0; h < G; ++h) s_m[h] = m_run[h];
-  }
+  if (lane < 8) sm.wm[wave][lane] = m_run;
   __syncthreads();
 
-  const int S = a.n_splits;
+  const int Sn = a.n_splits;
   for (int idx = tid; idx < G * kDim; idx += kBlock) {
     const int h = idx / kDim, d = idx % kDim;
     const int64_t bq = (int64_t)b * a.Hq + a.q_of_kv[kvh * G + h];
-    const float o = (s_o[0][h][d] + s_o[1][h][d]) + (s_o[2][h][d] + s_o[3][h][d]);
-    const float l = (s_l[0][h] + s_l[1][h]) + (s_l[2][h] + s_l[3][h]);
-    if (S == 1) {
+    int M = INT_MIN;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) M = max(M, sm.wm[w][h]);
+    float o = 0.0f, l = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      if (sm.wm[w][h] == INT_MIN) continue;
+      const float f = __builtin_amdgcn_ldexpf(1.0f, sm.wm[w][h] - M);
+      o = fmaf(f, sm.wo[w][h][d] + sm.wo[w][h + 8][d], o);
+      l = fmaf(f, sm.wl[w][h] + sm.wl[w][h + 8], l);
+    }
+    if (Sn == 1) {
       a.out[bq * kDim + d] = o / l;
       if constexpr (DEBUG) {
-        if (d == 0 && a.dbg_m_final) a.dbg_m_final[bq] = s_m[h];
-        if (d == 0 && a.dbg_m_split) a.dbg_m_split[bq] = s_m[h];
+        if (d == 0 && a.dbg_m_final) a.dbg_m_final[bq] = M;
+        if (d == 0 && a.dbg_m_split) a.dbg_m_split[bq] = M;
       }
     } else {
-      const int64_t ps = bq * S + split;
+      const int64_t ps = bq * Sn + split;
       a.part_o[ps * kDim + d] = o;
       if (d == 0) {
         a.part_l[ps] = l;
-        a.part_m[ps] = s_m[h];
+        a.part_m[ps] = M;
         if constexpr (DEBUG) {
-          if (a.dbg_m_split) a.dbg_m_split[ps] = s_m[h];
+          if (a.dbg_m_split) a.dbg_m_split[ps] = M;
         }
       }
     }
   }
-  if (S == 1) return;
+  if (Sn == 1) return;
 
-  // ---- split combine by the last workgroup of this (batch, kv head) -------
+  // ---- split combine by the last workgroup of this (batch, kv head) ------------
   __threadfence();
   __syncthreads();
   if (tid == 0) {
-    const uint32_t old = atomicAdd(&a.counters[(int64_t)b * a.Hkv + kvh], 1u);
-    s_last = (old == (uint32_t)(S - 1));
+    const uint32_t old = atomicAdd(&a.counters[seq], 1u);
+    sm.last = (old == (uint32_t)(Sn - 1));
   }
   __syncthreads();
-  if (!s_last) return;
+  if (!sm.last) return;
   __threadfence();
   for (int idx = tid; idx < G * kDim; idx += kBlock) {
     const int h = idx / kDim, d = idx % kDim;
     const int64_t bq = (int64_t)b * a.Hq + a.q_of_kv[kvh * G + h];
     int M = INT_MIN;
-    for (int s = 0; s < S; ++s) M = max(M, a.part_m[bq * S + s]);
+    for (int s = 0; s < Sn; ++s) M = max(M, a.part_m[bq * Sn + s]);
     float L = 0.0f, O = 0.0f;
-    for (int s = 0; s < S; ++s) {
-      const float f = __builtin_amdgcn_ldexpf(1.0f, a.part_m[bq * S + s] - M);
-      L = fmaf(f, a.part_l[bq * S + s], L);
-      O = fmaf(f, a.part_o[(bq * S + s) * kDim + d], O);
+    for (int s = 0; s < Sn; ++s) {
+      const float f = __builtin_amdgcn_ldexpf(1.0f, a.part_m[bq * Sn + s] - M);
+      L = fmaf(f, a.part_l[bq * Sn + s], L);
+      O = fmaf(f, a.part_o[(bq * Sn + s) * kDim + d], O);
     }
     a.out[bq * kDim + d] = O / L;
     if constexpr (DEBUG) {
       if (d == 0 && a.dbg_m_final) a.dbg_m_final[bq] = M;
     }
   }
-  if (tid == 0) a.counters[(int64_t)b * a.Hkv + kvh] = 0u;
+  if (tid == 0) a.counters[seq] = 0u;
 }
 
 template <int MODE, int G, int K, bool DEBUG>

@@ -124,6 +124,57 @@ __global__ __launch_bounds__(kBlock) void encode_int8_kernel(
   if (lane == 0) key_scale[orow] = step;
 }
 
+// Value-cache store: token t of sequence s, dim d lives at
+// ((s * t_cap + (t/8)*8) * 64 + d * 8 + t % 8) halves. One thread per
+// (sequence, 8-token group, dim) gathers the group's 8 tokens of its dim and
+// writes them as one 16-byte word (or only the tokens inside [t0, t0+n_tok)
+// at the ends of the range).
+__global__ __launch_bounds__(256) void store_values_kernel(
+    const uint16_t* __restrict__ src, int64_t n_seq, int64_t n_tok, int64_t t_cap, int64_t t0,
+    int64_t g_first, int64_t n_groups, uint16_t* __restrict__ dst) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n_seq * n_groups * kDim) return;
+  const int d = (int)(i % kDim);
+  const int64_t sg = i / kDim;
+  const int64_t s = sg / n_groups, g = g_first + sg % n_groups;
+  uint16_t* out = dst + (s * t_cap + g * 8) * kDim + d * 8;
+  uint16_t vals[8];
+  bool full = true;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const int64_t t = g * 8 + k;
+    const bool in = t >= t0 && t < t0 + n_tok;
+    full = full && in;
+    vals[k] = in ? src[(s * n_tok + (t - t0)) * kDim + d] : (uint16_t)0;
+  }
+  if (full) {
+    uint4 w;
+    w.x = vals[0] | ((uint32_t)vals[1] << 16);
+    w.y = vals[2] | ((uint32_t)vals[3] << 16);
+    w.z = vals[4] | ((uint32_t)vals[5] << 16);
+    w.w = vals[6] | ((uint32_t)vals[7] << 16);
+    *reinterpret_cast<uint4*>(out) = w;
+  } else {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int64_t t = g * 8 + k;
+      if (t >= t0 && t < t0 + n_tok) out[k] = vals[k];
+    }
+  }
+}
+
+hipError_t launch_store_values(const uint16_t* src, int64_t n_seq, int64_t n_tok, int64_t t_cap,
+                               int64_t t0, uint16_t* dst, hipStream_t stream) {
+  if (n_seq == 0 || n_tok == 0) return hipSuccess;
+  const int64_t g_first = t0 / 8, g_last = (t0 + n_tok - 1) / 8;
+  const int64_t n_groups = g_last - g_first + 1;
+  const int64_t n = n_seq * n_groups * kDim;
+  const int64_t grid = (n + 255) / 256;
+  hipLaunchKernelGGL(store_values_kernel, dim3((uint32_t)grid), dim3(256), 0, stream, src, n_seq,
+                     n_tok, t_cap, t0, g_first, n_groups, dst);
+  return hipGetLastError();
+}
+
 __global__ void fill_zero_kernel(uint32_t* __restrict__ p, size_t n_words, uint8_t* tail,
                                  size_t tail_bytes) {
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;

@@ -32,6 +32,9 @@ hipError_t launch_encode_int8(const uint16_t* k, int64_t n_rows, int64_t out_str
                               int hadamard, float* key_scale, int8_t* codes,
                               hipStream_t stream);
 
+hipError_t launch_store_values(const uint16_t* src, int64_t n_seq, int64_t n_tok, int64_t t_cap,
+                               int64_t t0, uint16_t* dst, hipStream_t stream);
+
 hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream);
 
 enum ScoreMode : int { kScorePot = 0, kScoreInt8 = 1, kScoreFp16 = 2 };

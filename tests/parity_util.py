@@ -20,6 +20,14 @@ def to_dev(a, dtype=None):
     return t.to(DEV)
 
 
+def store_values(v_bits, B, Hkv, t_cap):
+    """Row-major fp16 values [B, Hkv, t_cap, 64] (host) -> device value cache."""
+    src = to_dev(np.ascontiguousarray(v_bits).reshape(B * Hkv, t_cap, 64)).view(torch.float16)
+    cache = pa.alloc_value_cache(B, Hkv, t_cap, DEV)
+    pa.pot_store_values(src, B * Hkv, t_cap, t_cap, 0, cache)
+    return cache
+
+
 def gpu_encode(k_bits, mant_bits=0, hadamard=False, key_scale=None, frac_bits=7):
     """k_bits: uint16 [rows, 64] host. Returns numpy (codes_se, codes_m, scale)."""
     rows = k_bits.reshape(-1, 64).shape[0]
@@ -49,7 +57,7 @@ def gpu_pot_decode(d, codes_se, codes_m, key_scale, mant_bits=0, frac_bits=7,
     se = to_dev(codes_se)
     cm = to_dev(codes_m) if codes_m is not None else None
     sc = to_dev(key_scale)
-    v = to_dev(d["v_bits"]).view(torch.float16)
+    v = store_values(d["v_bits"], B, Hkv, t_cap)
     out = torch.empty((B, Hq, 64), dtype=torch.float32, device=DEV)
     nws = pa.pot_decode_workspace_bytes_for_splits(B, Hq, Hkv, T, force_splits) \
         if force_splits else pa.pot_decode_workspace_bytes(B, Hq, Hkv, T)

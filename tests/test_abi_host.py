@@ -150,3 +150,18 @@ def test_binding_raises_pot_error():
     with pytest.raises(pa.PotError) as ei:
         pa._check(pa.POT_ERR_WORKSPACE)
     assert ei.value.status == pa.POT_ERR_WORKSPACE
+
+
+def test_store_values_rejects_bad_arguments():
+    S = pa._lib.pot_store_values
+    assert S(FAKE, 2, 5, 12, 0, FAKE, None) == pa.POT_ERR_INVALID_ARG   # t_cap % 8
+    assert S(FAKE, 2, 5, 16, 12, FAKE, None) == pa.POT_ERR_INVALID_ARG  # past t_cap
+    assert S(FAKE, 2, 5, 16, -1, FAKE, None) == pa.POT_ERR_INVALID_ARG
+    assert S(FAKE, -1, 5, 16, 0, FAKE, None) == pa.POT_ERR_INVALID_ARG
+    assert S(None, 2, 5, 16, 0, FAKE, None) == pa.POT_ERR_INVALID_ARG
+    assert S(FAKE + 2, 2, 5, 16, 0, FAKE, None) == pa.POT_ERR_INVALID_ARG
+    assert S(None, 0, 5, 16, 0, None, None) == pa.POT_OK  # nothing to store
+
+
+def test_decode_needs_t_cap_multiple_of_8():
+    assert _decode(t_cap=4100) == pa.POT_ERR_INVALID_ARG

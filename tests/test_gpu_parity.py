@@ -11,7 +11,7 @@ import torch
 import oracle
 import paper_2609_09208_amd as pa
 from parity_util import (DEV, O_TOL, assert_pot_parity, gpu_encode, gpu_pot_decode,
-                         oracle_pot, to_dev)
+                         oracle_pot, store_values, to_dev)
 from workloads import head_map, make_decode_inputs, make_decode_inputs_device
 
 pytestmark = pytest.mark.gpu
@@ -85,6 +85,23 @@ def test_int8_encode(had):
     assert np.array_equal(sc.cpu().numpy().view(np.uint32), osc.view(np.uint32))
 
 
+def test_store_values_layout_and_append():
+    # token t, dim m of sequence q at (q*t_cap + (t//8)*8)*64 + m*8 + t%8
+    rng = np.random.default_rng(6)
+    n_seq, t_cap, T = 3, 48, 37
+    v = rng.standard_normal((n_seq, T, 64)).astype(np.float16)
+    cache = torch.full((n_seq * t_cap * 64,), 7.0, dtype=torch.float16, device=DEV)
+    pa.pot_store_values(to_dev(v), n_seq, T, t_cap, 0, cache)
+    new = rng.standard_normal((n_seq, 1, 64)).astype(np.float16)
+    pa.pot_store_values(to_dev(new), n_seq, 1, t_cap, T, cache)  # append token T
+    torch.cuda.synchronize()
+    got = cache.cpu().numpy().reshape(n_seq, t_cap // 8, 64, 8)
+    logical = got.transpose(0, 1, 3, 2).reshape(n_seq, t_cap, 64)
+    assert np.array_equal(logical[:, :T], v)
+    assert np.array_equal(logical[:, T], new[:, 0])
+    assert (logical[:, T + 1:] == 7.0).all()  # untouched
+
+
 # ---- decode: the paper's configurations ---------------------------------------
 def test_tiny_single_head_pot4():
     # d = 64, T = 256, batch 1, one head; K and q N(0, 1), V fp16 N(0, 1)
@@ -130,10 +147,12 @@ def _sampled_full_size(B, T, mant_bits, hadamard, samples, seed):
     rows = B * Hkv * T
     pa.pot_encode_keys(fmt, d["k"], rows, 1, 0, cache["key_scale"], cache["codes_se"],
                        cache["codes_m"])
+    vcache = pa.alloc_value_cache(B, Hkv, T, DEV)
+    pa.pot_store_values(d["v"], B * Hkv, T, T, 0, vcache)
     out = torch.empty((B, Hq, 64), dtype=torch.float32, device=DEV)
     ws = pa.alloc_workspace(pa.pot_decode_workspace_bytes(B, Hq, Hkv, T), DEV)
     pa.pot_decode_attention(fmt, d["q"], cache["codes_se"], cache["codes_m"],
-                            cache["key_scale"], d["v"], T, d["kv_head_of_q"], B, Hq, Hkv,
+                            cache["key_scale"], vcache, T, d["kv_head_of_q"], B, Hq, Hkv,
                             T, out, ws)
     torch.cuda.synchronize()
     G = Hq // Hkv
@@ -166,7 +185,8 @@ def test_full_size_b8_t32768_hadamard_potm4_sampled():
 
 
 # ---- edge cases ------------------------------------------------------------------
-@pytest.mark.parametrize("T,t_cap", [(1, 1), (5, 9), (255, 255), (257, 300), (1000, 1031)])
+@pytest.mark.parametrize("T,t_cap", [(1, 8), (5, 16), (255, 256), (257, 320), (1000, 1032),
+                                     (4099, 4104)])
 def test_ragged_lengths_and_padding(T, t_cap):
     d = make_decode_inputs(20 + T, B=2, Hq=8, Hkv=2, T=T, t_cap=t_cap)
     assert_pot_parity(d, mant_bits=1)
@@ -227,13 +247,14 @@ def test_split_invariance_and_determinism():
 # ---- comparison kernels ------------------------------------------------------------
 @pytest.mark.parametrize("had", [False, True])
 def test_int8_decode_parity(had):
-    d = make_decode_inputs(50, B=2, Hq=32, Hkv=4, T=2500)
+    B, Hq, Hkv, T = 2, 32, 4, 2500
+    d = make_decode_inputs(50, B=B, Hq=Hq, Hkv=Hkv, T=T)
+    tc = d["t_cap"]
     rows = d["k_bits"].reshape(-1, 64)
     n = rows.shape[0]
     codes = torch.empty((n, 64), dtype=torch.int8, device=DEV)
     sc = torch.empty(n, dtype=torch.float32, device=DEV)
     pa.pot_int8_encode_keys(to_dev(rows).view(torch.float16), n, 1, int(had), sc, codes)
-    B, Hq, Hkv, T = 2, 32, 4, 2500
     out = torch.empty((B, Hq, 64), dtype=torch.float32, device=DEV)
     ws = pa.alloc_workspace(pa.pot_decode_workspace_bytes(B, Hq, Hkv, T), DEV)
     dbg = pa.pot_debug()
@@ -243,11 +264,11 @@ def test_int8_decode_parity(had):
                 m_final=torch.empty((B, Hq), dtype=torch.int32, device=DEV))
     for k_, t_ in taps.items():
         setattr(dbg, k_, t_.data_ptr())
-    pa.pot_int8_decode_attention(to_dev(d["q"]), codes, sc, to_dev(d["v_bits"]).view(torch.float16),
-                                 T, d["kv_head_of_q"], B, Hq, Hkv, T, int(had), out, ws, dbg=dbg)
+    pa.pot_int8_decode_attention(to_dev(d["q"]), codes, sc, store_values(d["v_bits"], B, Hkv, tc),
+                                 tc, d["kv_head_of_q"], B, Hq, Hkv, T, int(had), out, ws, dbg=dbg)
     torch.cuda.synchronize()
     oc, osc = oracle.int8_encode_keys(rows, hadamard=had)
-    r = oracle.int8_decode(d["q"], oc, osc, d["v_bits"], T, d["kv_head_of_q"], B, Hq, Hkv, T,
+    r = oracle.int8_decode(d["q"], oc, osc, d["v_bits"], tc, d["kv_head_of_q"], B, Hq, Hkv, T,
                            hadamard=had)
     assert np.array_equal(taps["qhat"].cpu().numpy(), r["qhat"])
     assert np.array_equal(taps["scores"].cpu().numpy(), r["scores"])
@@ -257,11 +278,12 @@ def test_int8_decode_parity(had):
 
 def test_fp16_decode_parity():
     d = make_decode_inputs(51, B=2, Hq=32, Hkv=4, T=2500, t_cap=2600)
+    assert d["t_cap"] % 8 == 0
     B, Hq, Hkv, T = 2, 32, 4, 2500
     out = torch.empty((B, Hq, 64), dtype=torch.float32, device=DEV)
     ws = pa.alloc_workspace(pa.pot_decode_workspace_bytes(B, Hq, Hkv, T), DEV)
     pa.pot_fp16_decode_attention(to_dev(d["q"]), to_dev(d["k_bits"]).view(torch.float16),
-                                 to_dev(d["v_bits"]).view(torch.float16), 2600,
+                                 store_values(d["v_bits"], B, Hkv, 2600), 2600,
                                  d["kv_head_of_q"], B, Hq, Hkv, T, out, ws)
     torch.cuda.synchronize()
     r = oracle.fp16_decode(d["q"], d["k_bits"], d["v_bits"], 2600, d["kv_head_of_q"], B, Hq,
@@ -269,6 +291,7 @@ def test_fp16_decode_parity():
     err = float(np.abs(out.cpu().numpy() - r).max())
     assert err <= O_TOL, err
     print(f"fp16 O err {err:.3e}")
+    # T = 2500 < t_cap = 2600: the tail group's tokens past T are never used
 
 
 def test_status_errors_do_not_launch():

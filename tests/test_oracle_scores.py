@@ -70,7 +70,7 @@ def test_scores_equal_bruteforce_integer_dot(k, F):
                           d["kv_head_of_q"], 2, 4, 2, 37, mant_bits=k,
                           frac_bits=F)
     kint = key_integers(se, cm if k else np.zeros((len(se), 0), np.uint8), k,
-                        F).reshape(2, 2, 37, 64)
+                        F).reshape(2, 2, d["t_cap"], 64)[:, :, :37]
     for b in range(2):
         for i in range(4):
             h = d["kv_head_of_q"][i]
@@ -85,7 +85,7 @@ def test_scores_track_the_real_dot_product():
     kf = rows.view(np.float16).astype(np.float64)
     for k, tol in [(0, 0.25), (4, 0.03)]:
         se, cm, sc = oracle.encode_keys(rows, mant_bits=k)
-        r = oracle.pot_decode(d["q"], se, cm, sc, d["v_bits"], 400,
+        r = oracle.pot_decode(d["q"], se, cm, sc, d["v_bits"], d["t_cap"],
                               d["kv_head_of_q"], 1, 8, 1, 400, mant_bits=k)
         s_hat = (r["delta"][0][:, None].astype(np.float64) * sc[None, :]
                  * r["scores"][0] * 2.0 ** -(7 + k))
@@ -142,7 +142,7 @@ def test_head_room_F_only_rescales():
     d = make_decode_inputs(8, B=1, Hq=2, Hkv=1, T=50)
     rows = d["k_bits"].reshape(-1, 64)
     se, cm, sc = oracle.encode_keys(rows, mant_bits=2)
-    res = [oracle.pot_decode(d["q"], se, cm, sc, d["v_bits"], 50,
+    res = [oracle.pot_decode(d["q"], se, cm, sc, d["v_bits"], d["t_cap"],
                              d["kv_head_of_q"], 1, 2, 1, 50, mant_bits=2,
                              frac_bits=F) for F in (6, 7, 9)]
     assert np.array_equal(res[0]["scores"] * 2, res[1]["scores"])
@@ -159,9 +159,10 @@ def test_int8_oracle_scores_bruteforce():
     assert np.allclose(sc, np.abs(xf).max(axis=1) / 127, rtol=2e-7)
     err = np.abs(xf - sc[:, None] * codes.astype(np.float32))
     assert (err <= sc[:, None] * 0.5001).all()
-    r = oracle.int8_decode(d["q"], codes, sc, d["v_bits"], 29,
+    tc = d["t_cap"]
+    r = oracle.int8_decode(d["q"], codes, sc, d["v_bits"], tc,
                            d["kv_head_of_q"], 1, 4, 2, 29)
-    c = codes.reshape(2, 29, 64).astype(np.int64)
+    c = codes.reshape(2, tc, 64)[:, :29].astype(np.int64)
     for i in range(4):
         h = d["kv_head_of_q"][i]
         assert np.array_equal(c[h] @ r["qhat"][0, i].astype(np.int64),
@@ -171,11 +172,11 @@ def test_int8_oracle_scores_bruteforce():
 def test_log2_domain_score_follows_the_recorded_fp32_order():
     # reading recorded for this build: x = fl32(fl32(float(acc) * s) * c),
     # c = fl32(fl32(Delta * log2e_f32) * 2^-(F+k+3)); the GPU must match it
-    d = make_decode_inputs(12, B=1, Hq=2, Hkv=1, T=500)
+    d = make_decode_inputs(12, B=1, Hq=2, Hkv=1, T=500, t_cap=500)
     rows = d["k_bits"].reshape(-1, 64)
     for k in (0, 4):
         se, cm, sc = oracle.encode_keys(rows, mant_bits=k)
-        r = oracle.pot_decode(d["q"], se, cm, sc, d["v_bits"], 500,
+        r = oracle.pot_decode(d["q"], se, cm, sc, d["v_bits"], d["t_cap"],
                               d["kv_head_of_q"], 1, 2, 1, 500, mant_bits=k)
         log2e = np.float32(np.log2(np.e))
         assert log2e.view(np.uint32) == 0x3FB8AA3B

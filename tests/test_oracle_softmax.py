@@ -52,7 +52,7 @@ def test_integer_max_properties():
 
 @pytest.mark.parametrize("k,had", [(0, False), (1, False), (4, True)])
 def test_output_is_textbook_softmax_of_dequantised_scores(k, had):
-    d = make_decode_inputs(55, B=1, Hq=8, Hkv=2, T=333)
+    d = make_decode_inputs(55, B=1, Hq=8, Hkv=2, T=333, t_cap=333)
     r, sc = _pot(d, k=k, had=had)
     v = d["v_bits"].view(np.float16).astype(np.float64)
     for i in range(8):
@@ -86,8 +86,8 @@ def test_hadamard_preserves_unquantised_scores():
 
 
 def test_fp16_oracle_matches_numpy_softmax():
-    d = make_decode_inputs(77, B=2, Hq=4, Hkv=2, T=65)
-    out = oracle.fp16_decode(d["q"], d["k_bits"], d["v_bits"], 65,
+    d = make_decode_inputs(77, B=2, Hq=4, Hkv=2, T=65, t_cap=65)
+    out = oracle.fp16_decode(d["q"], d["k_bits"], d["v_bits"], d["t_cap"],
                              d["kv_head_of_q"], 2, 4, 2, 65)
     k = d["k_bits"].view(np.float16).astype(np.float64)
     v = d["v_bits"].view(np.float16).astype(np.float64)

@@ -37,11 +37,12 @@ def make_decode_inputs(seed: int, B: int, Hq: int, Hkv: int, T: int,
     Draw order: channel scale c [Hkv, 64] ~ U[0.5, 4] (if channel_scale),
     z [B, Hkv, T, 64] ~ N(0, 1), v [B, Hkv, T, 64] ~ N(0, 1),
     q [B, Hq, 64] ~ N(0, 1). K = fp16(z * c), V = fp16(v).
-    Rows T..t_cap-1 of each sequence hold POISON values.
+    Rows T..t_cap-1 of each sequence hold POISON values; t_cap defaults to T
+    rounded up to a multiple of 8 (the value cache's token groups).
 
     Returns q (fp32), k_bits / v_bits (uint16 fp16 bit patterns,
     [B, Hkv, t_cap, 64]), kv_head_of_q (int32 [Hq]) and the shape fields."""
-    t_cap = T if t_cap is None else int(t_cap)
+    t_cap = max(8, -(-T // 8) * 8) if t_cap is None else int(t_cap)
     assert t_cap >= T >= 0
     rng = np.random.default_rng(seed)
     if channel_scale:
