@@ -105,6 +105,9 @@ def main() -> int:
     ap.add_argument("--mant-bits", type=int, default=0)
     ap.add_argument("--cpu-budget", type=float, default=10.0)
     ap.add_argument("--no-compare", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
+                    help="only run device-to-device copies of BYTES bytes (calibrates "
+                         "the FETCH_SIZE / WRITE_SIZE counters against a known size)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
@@ -120,6 +123,15 @@ def main() -> int:
 
     dev = "cuda:0"
     torch.cuda.set_device(0)
+    if args.copy_probe:
+        n = args.copy_probe
+        src = torch.ones(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": n, "copies": 3}), flush=True)
+        return 0
     B, T, L, k = args.batch, args.seq, args.layers, args.mant_bits
     G = HQ // HKV
     fmt = pa.make_format(mant_bits=k, frac_bits=7)

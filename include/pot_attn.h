@@ -159,10 +159,11 @@ pot_status pot_store_values(const uint16_t* v_fp16, int64_t n_seq, int64_t n_tok
                             int64_t t_cap, int64_t t0, uint16_t* v_cache,
                             void* stream);
 
-/* Workspace bytes pot_decode_attention needs for this problem shape (the
- * split partials and the split-completion counters). Host-only. Returns 0 for
- * invalid shapes. The same figure serves pot_int8_decode_attention and
- * pot_fp16_decode_attention. */
+/* Workspace bytes pot_decode_attention needs for this problem shape: the
+ * prepared query operands of each (batch, kv head) and the key-split partials
+ * (M_s, l_s, o_s) for the largest split count the planner can choose.
+ * Host-only. Returns 0 for invalid shapes. The same figure serves
+ * pot_int8_decode_attention and pot_fp16_decode_attention. */
 size_t pot_decode_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv,
                                   int32_t T);
 
@@ -172,9 +173,8 @@ size_t pot_decode_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv,
 size_t pot_decode_workspace_bytes_for_splits(int32_t B, int32_t Hq, int32_t Hkv,
                                              int32_t T, int32_t n_splits);
 
-/* Zero the completion counters of a freshly allocated workspace (a fill
- * kernel on `stream`). Needed once per workspace allocation: every decode
- * call leaves the counters at zero again when it completes. */
+/* Zero a workspace (a fill kernel on `stream`). Optional: the decode calls
+ * need no particular initial workspace contents. */
 pot_status pot_workspace_init(void* workspace, size_t ws_bytes, void* stream);
 
 /* Single-token decode attention with PoT keys (Sec. II-B, II-E, II-F).
@@ -186,17 +186,19 @@ pot_status pot_workspace_init(void* workspace, size_t ws_bytes, void* stream);
  *               G in {1, 2, 4, 8}.
  *  T            keys attended, 1 <= T <= t_cap.
  *  out          [B][Hq][d] fp32: O = softmax(S^ / sqrt(d)) V.
- *  workspace    >= pot_decode_workspace_bytes(B, Hq, Hkv, T) bytes, counters
- *               zeroed once by pot_workspace_init. Calls that share a
- *               workspace must not overlap in time.
+ *  workspace    >= pot_decode_workspace_bytes(B, Hq, Hkv, T) bytes, 256-byte
+ *               aligned. Calls that share a workspace must not overlap in
+ *               time.
  * Steps: q is rotated (if hadamard) and quantised to int8 with step
  * Delta = amax/127; each score is the exact int32 sum of sign-flipped left
  * shifts of q^ (eq. sac); x = acc * s * Delta * log2(e) * 2^-(F+k) / 8 in a
  * fixed fp32 order; the running maximum is the integer M = ceil(max x)
  * (eq. logsm) so rescales are exact powers of two; weights 2^(x-M) multiply
  * the fp16 values with fp32 accumulation (matrix cores, weights split into
- * fp16 high and low parts); key splits are merged with exact 2^(M_s - M)
- * factors.
+ * fp16 high and low parts); key splits (chosen to fill the GPU's resident
+ * workgroup slots in one round) are merged with exact 2^(M_s - M) factors.
+ * Launches: a query-preparation kernel, the split decode kernel and, with
+ * more than one split, a combine kernel, all on `stream`.
  */
 pot_status pot_decode_attention(const pot_format* fmt, const float* q,
                                 const uint8_t* codes_se,

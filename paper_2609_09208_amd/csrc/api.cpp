@@ -6,6 +6,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cstdarg>
 #include <cstdio>
 #include <string>
@@ -45,7 +46,6 @@ bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) %
 
 constexpr int kE = 6;
 constexpr int kMaxF = 12;
-constexpr int kTargetGroups = 1024;  // 4 workgroups per CU on a 256-CU MI355X
 
 pot_status check_format(const pot_format* f) {
   if (!f) return fail(POT_ERR_INVALID_ARG, "fmt is NULL");
@@ -67,16 +67,12 @@ struct Plan {
   int n_splits, split_len;
 };
 
-Plan plan_splits(int B, int Hkv, int T, int force) {
+// Key splits: enough workgroups to fill the GPU's resident slots in a single
+// dispatch round (slots = CUs x resident workgroups per CU); one split when
+// the (batch, kv head) pairs alone fill it. Splits are whole 256-key tiles.
+Plan plan_from_count(int T, int S) {
   const int tiles = (T + kTile - 1) / kTile;
-  int S;
-  if (force > 0) {
-    S = std::min(force, tiles);
-  } else {
-    const long units = (long)B * Hkv;
-    S = (int)std::min<long>((kTargetGroups + units - 1) / units, tiles);
-    S = std::max(S, 1);
-  }
+  S = std::max(1, std::min(S, tiles));
   const int tiles_per_split = (tiles + S - 1) / S;
   Plan p;
   p.split_len = tiles_per_split * kTile;
@@ -84,16 +80,50 @@ Plan plan_splits(int B, int Hkv, int T, int force) {
   return p;
 }
 
+int split_count_for_slots(long units, long slots) {
+  return units >= slots ? 1 : (int)(slots / units);
+}
+
+// Upper bound used to size workspaces without a device query: 256 CUs x 8
+// resident workgroups (the decode kernel reaches at most 3 per CU).
+constexpr long kMaxSlots = 256L * 8;
+
+Plan plan_bound(int B, int Hkv, int T) {
+  return plan_from_count(T, split_count_for_slots((long)B * Hkv, kMaxSlots));
+}
+
+std::atomic<int> g_cus[64];
+std::atomic<int> g_occ[3][9][5];
+
+long device_slots(int mode, int G, int mant_bits) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
+  int cus = g_cus[dev].load(std::memory_order_relaxed);
+  if (cus <= 0) {
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus <= 0)
+      cus = 256;
+    g_cus[dev].store(cus, std::memory_order_relaxed);
+  }
+  int occ = g_occ[mode][G][mant_bits].load(std::memory_order_relaxed);
+  if (occ <= 0) {
+    occ = decode_occupancy(mode, G, mant_bits);
+    if (occ <= 0) occ = 2;
+    g_occ[mode][G][mant_bits].store(occ, std::memory_order_relaxed);
+  }
+  return (long)cus * occ;
+}
+
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 struct WsLayout {
-  size_t counters, part_m, part_l, part_o, total;
+  size_t qbuf, part_m, part_l, part_o, total;
 };
 
 WsLayout ws_layout(long B, long Hq, long Hkv, long S) {
   WsLayout w;
-  w.counters = 0;
-  w.part_m = align_up((size_t)(B * Hkv) * 4, 256);
+  w.qbuf = 0;
+  w.part_m = align_up((size_t)(B * Hkv) * query_words((int)(Hq / Hkv)) * 4, 256);
   w.part_l = w.part_m + align_up((size_t)(B * Hq * S) * 4, 256);
   w.part_o = w.part_l + align_up((size_t)(B * Hq * S) * 4, 256);
   w.total = w.part_o + align_up((size_t)(B * Hq * S) * 64 * 4, 256);
@@ -145,13 +175,21 @@ pot_status decode_common(int mode, int mant_bits, DecodeArgs& a, const int32_t* 
   if (st != POT_OK) return st;
   const int force = dbg ? dbg->force_splits : 0;
   if (force < 0) return fail(POT_ERR_INVALID_ARG, "force_splits %d < 0", force);
-  const Plan p = plan_splits(B, Hkv, T, force);
+  Plan p;
+  if (force > 0) {
+    p = plan_from_count(T, force);
+  } else {
+    const int mbits = mode == kScorePot ? mant_bits : 0;
+    const int S = split_count_for_slots((long)B * Hkv, device_slots(mode, G, mbits));
+    p = plan_from_count(T, std::min(S, plan_bound(B, Hkv, T).n_splits));
+  }
   const WsLayout w = ws_layout(B, Hq, Hkv, p.n_splits);
   if (ws_bytes < w.total)
     return fail(POT_ERR_WORKSPACE, "workspace %zu bytes < %zu needed for %d splits", ws_bytes,
                 w.total, p.n_splits);
   uint8_t* ws = static_cast<uint8_t*>(workspace);
-  a.counters = reinterpret_cast<uint32_t*>(ws + w.counters);
+  a.qbuf = reinterpret_cast<int32_t*>(ws + w.qbuf);
+  a.qstride = query_words(G);
   a.part_m = reinterpret_cast<int32_t*>(ws + w.part_m);
   a.part_l = reinterpret_cast<float*>(ws + w.part_l);
   a.part_o = reinterpret_cast<float*>(ws + w.part_o);
@@ -249,14 +287,13 @@ pot_status pot_store_values(const uint16_t* v_fp16, int64_t n_seq, int64_t n_tok
 
 size_t pot_decode_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv, int32_t T) {
   if (!shape_ok(B, Hq, Hkv, T)) return 0;
-  const Plan p = plan_splits(B, Hkv, T, 0);
-  return ws_layout(B, Hq, Hkv, p.n_splits).total;
+  return ws_layout(B, Hq, Hkv, plan_bound(B, Hkv, T).n_splits).total;
 }
 
 size_t pot_decode_workspace_bytes_for_splits(int32_t B, int32_t Hq, int32_t Hkv, int32_t T,
                                              int32_t n_splits) {
   if (!shape_ok(B, Hq, Hkv, T) || n_splits < 0) return 0;
-  const Plan p = plan_splits(B, Hkv, T, n_splits);
+  const Plan p = n_splits > 0 ? plan_from_count(T, n_splits) : plan_bound(B, Hkv, T);
   return ws_layout(B, Hq, Hkv, p.n_splits).total;
 }
 

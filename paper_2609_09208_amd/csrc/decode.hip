@@ -32,11 +32,15 @@
 //     v_mfma_f32_16x16x32_f16, fp32 accumulation; a fifth column block of
 //     ones yields the row sums l. The value cache is stored token-interleaved
 //     ([t/8][d][t%8]) so a lane's 16-byte load is exactly its B fragment.
-// The last workgroup of a (batch, kv-head) to finish (completion counter)
-// merges the key splits with exact 2^(M_s - M) weights.
+// With one split the workgroup writes O directly; otherwise it writes its
+// (M_s, l_s, o_s) and a small combine kernel merges the splits with exact
+// 2^(M_s - M) weights. (A last-workgroup merge inside this kernel would need
+// an agent-scope release/acquire per workgroup, which on a multi-XCD part
+// writes back and invalidates the XCD's L2 each time and serialises.)
 #include <hip/hip_fp16.h>
 
 #include <climits>
+#include <type_traits>
 
 #include "pot_device.hpp"
 #include "pot_launch.hpp"
@@ -106,78 +110,143 @@ struct ValRegs {
   uint4 f[2][4];  // [K-block of 32 keys][16-dim block]
 };
 
+// Loads are unconditional (addresses clamped into the valid range) so that
+// the compiler can count outstanding loads statically and keep the prefetch
+// of the next tile in flight while the current one is processed; keys past
+// the range are masked when the tile is consumed.
 template <int MODE, int K>
-__device__ __forceinline__ void load_keys(const DecodeArgs& a, int64_t row, bool valid,
-                                          KeyRegs<MODE, K>& r) {
+__device__ __forceinline__ void load_keys(const DecodeArgs& a, int64_t row, KeyRegs<MODE, K>& r) {
   if constexpr (MODE == kScorePot) {
-    if (valid) {
-      const uint4* cp = reinterpret_cast<const uint4*>(a.codes_se + row * (kDim / 2));
-      r.c0 = cp[0];
-      r.c1 = cp[1];
+    const uint4* cp = reinterpret_cast<const uint4*>(a.codes_se + row * (kDim / 2));
+    r.c0 = cp[0];
+    r.c1 = cp[1];
 #pragma unroll
-      for (int bb = 0; bb < K; ++bb)
-        r.pl[bb] = reinterpret_cast<const uint2*>(a.codes_m + row * 8 * K)[bb];
-      r.s = a.key_scale[row];
-    } else {
-      r.c0 = r.c1 = make_uint4(0x77777777u, 0x77777777u, 0x77777777u, 0x77777777u);
-#pragma unroll
-      for (int bb = 0; bb < K; ++bb) r.pl[bb] = make_uint2(0u, 0u);
-      r.s = 0.0f;
-    }
+    for (int bb = 0; bb < K; ++bb)
+      r.pl[bb] = reinterpret_cast<const uint2*>(a.codes_m + row * 8 * K)[bb];
+    r.s = a.key_scale[row];
   } else if constexpr (MODE == kScoreInt8) {
     const int4* kp = reinterpret_cast<const int4*>(a.codes_i8 + row * kDim);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) r.k[i] = valid ? kp[i] : make_int4(0, 0, 0, 0);
-    r.s = valid ? a.key_scale[row] : 0.0f;
+    for (int i = 0; i < 4; ++i) r.k[i] = kp[i];
+    r.s = a.key_scale[row];
   } else {
     const uint4* kp = reinterpret_cast<const uint4*>(a.k_f16 + row * kDim);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) r.k[i] = valid ? kp[i] : make_uint4(0u, 0u, 0u, 0u);
+    for (int i = 0; i < 8; ++i) r.k[i] = kp[i];
   }
 }
 
 // B fragments of one 64-key tile: lane l takes keys t0 + 32*kb + 8*(l/16) ..+7
 // of dim 16*nb + l%16, one 16-byte load each from the token-interleaved cache.
-__device__ __forceinline__ void load_values(const uint16_t* vseq, int t0, int t_end, int lane,
+// Groups past the range read the range's last group instead.
+__device__ __forceinline__ void load_values(const uint16_t* vseq, int t0, int g_last, int lane,
                                             ValRegs& v) {
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) {
-    const int g8 = t0 + 32 * kb + 8 * (lane >> 4);
-    const bool ok = g8 < t_end;
+    const int g8 = min(t0 + 32 * kb + 8 * (lane >> 4), g_last);
     const uint4* base = reinterpret_cast<const uint4*>(vseq + (int64_t)g8 * kDim);
 #pragma unroll
-    for (int nb = 0; nb < 4; ++nb)
-      v.f[kb][nb] = ok ? base[nb * 16 + (lane & 15)] : make_uint4(0u, 0u, 0u, 0u);
-    if (ok && g8 + 8 > t_end) {  // tail group: zero tokens at or past t_end
+    for (int nb = 0; nb < 4; ++nb) v.f[kb][nb] = base[nb * 16 + (lane & 15)];
+  }
+}
+
+// Zero the value fragments of tokens at or past t_end (tail tile only), so
+// that whatever the cache holds there cannot reach the sums (p is 0 there).
+__device__ __forceinline__ void mask_values(int t0, int t_end, int lane, ValRegs& v) {
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb) {
-        uint32_t w4[4] = {v.f[kb][nb].x, v.f[kb][nb].y, v.f[kb][nb].z, v.f[kb][nb].w};
+  for (int kb = 0; kb < 2; ++kb) {
+    const int g8 = t0 + 32 * kb + 8 * (lane >> 4);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const uint32_t lo = (g8 + 2 * i < t_end) ? 0x0000FFFFu : 0u;
-          const uint32_t hi = (g8 + 2 * i + 1 < t_end) ? 0xFFFF0000u : 0u;
-          w4[i] &= lo | hi;
-        }
-        v.f[kb][nb] = make_uint4(w4[0], w4[1], w4[2], w4[3]);
+    for (int nb = 0; nb < 4; ++nb) {
+      uint32_t w4[4] = {v.f[kb][nb].x, v.f[kb][nb].y, v.f[kb][nb].z, v.f[kb][nb].w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t lo = (g8 + 2 * i < t_end) ? 0x0000FFFFu : 0u;
+        const uint32_t hi = (g8 + 2 * i + 1 < t_end) ? 0xFFFF0000u : 0u;
+        w4[i] &= lo | hi;
+      }
+      v.f[kb][nb] = make_uint4(w4[0], w4[1], w4[2], w4[3]);
+    }
+  }
+}
+
+// ---- prepared query operands (workspace, one block per kv head) -------------
+// PoT-4 with G >= 2: [m][pair] words q_{2p} + 2^16 q_{2p+1}; other PoT forms:
+// [(b' * 64 + m) * G + h] = q << b'; INT8: [i * G + h] four int8 per word;
+// fp16: [i * G + h] two fp16 per word. The G per-head score factors follow.
+template <int MODE, int G, int K>
+struct QLayout {
+  static constexpr bool kPacked = MODE == kScorePot && K == 0 && G >= 2;
+  static constexpr int NP = G / 2;
+  static constexpr int kWords = MODE == kScorePot ? (kPacked ? kDim * NP : (K + 1) * kDim * G)
+                                : MODE == kScoreInt8 ? (kDim / 4) * G
+                                                     : (kDim / 2) * G;
+};
+
+// Rotates (optionally) and quantises the G query vectors of one (batch, kv
+// head) and writes the operand words the decode kernel reads through the
+// scalar cache. Grid (Hkv, B), 4 waves; wave w handles heads w, w + 4.
+template <int MODE, int G, int K, bool DEBUG>
+__global__ __launch_bounds__(kBlock) void prep_queries_kernel(const DecodeArgs a) {
+  using QL = QLayout<MODE, G, K>;
+  __shared__ int32_t qh[G * kDim];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int kvh = blockIdx.x, b = blockIdx.y;
+  const int64_t seq = (int64_t)b * a.Hkv + kvh;
+  int32_t* qb = a.qbuf + seq * a.qstride;
+  float* cb = reinterpret_cast<float*>(qb + QL::kWords);
+  for (int h = wave; h < G; h += kWaves) {
+    const int64_t bq = (int64_t)b * a.Hq + a.q_of_kv[kvh * G + h];
+    float qv = a.q[bq * kDim + lane];
+    if constexpr (MODE == kScoreFp16) {
+      const uint32_t bits = __half_as_ushort(__float2half_rn(qv));
+      const uint32_t other = __shfl_xor(bits, 1, 64);
+      if ((lane & 1) == 0) qb[(lane >> 1) * G + h] = (int32_t)(bits | (other << 16));
+      if (lane == 0) cb[h] = __fmul_rn(log2e_f32(), 0.125f);
+    } else {
+      if (a.hadamard) qv = (float)(wave_fwht64((double)qv) * 0.125);
+      float step;
+      const int qi = wave_quantize_int8(qv, &step);
+      qh[h * kDim + lane] = qi;
+      if constexpr (MODE == kScorePot) {
+        if (lane == 0)
+          cb[h] = __fmul_rn(__fmul_rn(step, log2e_f32()),
+                            __builtin_amdgcn_ldexpf(1.0f, -(a.frac_bits + K + 3)));
+      } else {
+        uint32_t word = (uint32_t)(qi & 0xFF) << (8 * (lane & 3));
+        word |= __shfl_xor(word, 1, 64);
+        word |= __shfl_xor(word, 2, 64);
+        if ((lane & 3) == 0) qb[(lane >> 2) * G + h] = (int32_t)word;
+        if (lane == 0) cb[h] = __fmul_rn(__fmul_rn(step, log2e_f32()), 0.125f);
+      }
+      if constexpr (DEBUG) {
+        if (a.dbg_qhat) a.dbg_qhat[bq * kDim + lane] = (int8_t)qi;
+        if (a.dbg_delta && lane == 0) a.dbg_delta[bq] = step;
+      }
+    }
+  }
+  if constexpr (MODE == kScorePot) {
+    __syncthreads();
+    if constexpr (QL::kPacked) {
+      // pair p holds heads 2p (low field) and 2p+1 (high field) as one integer
+      for (int i = tid; i < kDim * QL::NP; i += kBlock) {
+        const int m = i / QL::NP, p = i % QL::NP;
+        qb[i] = (int32_t)((uint32_t)qh[(2 * p) * kDim + m] +
+                          ((uint32_t)qh[(2 * p + 1) * kDim + m] << 16));
+      }
+    } else {
+      for (int i = tid; i < (K + 1) * kDim * G; i += kBlock) {
+        const int h = i % G, bm = i / G, bb = bm / kDim, m = bm % kDim;
+        qb[i] = qh[h * kDim + m] * (1 << bb);
       }
     }
   }
 }
 
-// ---- shared memory -------------------------------------------------------------
-template <int MODE, int G, int K>
-struct Smem {
-  static constexpr bool kPacked = MODE == kScorePot && K == 0 && G >= 2;
-  static constexpr int NP = G / 2;
-  static constexpr int kQWords = MODE == kScorePot ? (kPacked ? kDim * (NP > 0 ? NP : 1)
-                                                              : (K + 1) * kDim * G)
-                                 : MODE == kScoreInt8 ? (kDim / 4) * G
-                                                      : (kDim / 2) * G;
-  int32_t q[kQWords];          // PoT packed: [m][pair]; PoT: [b'*64+m][h]; INT8/fp16: [i][h]
-  int32_t qh[G * kDim];        // quantised query per head (prologue staging)
-  float c[G];                  // per-head factor of the log2-domain score
-  float x[kWaves][8][kXRow];   // transposed score tile per wave
-  float wo[kWaves][16][kDim];  // per-wave P.V (rows: heads x {hi, lo})
+// ---- shared memory of the decode kernel -------------------------------------
+struct alignas(16) DecodeSmem {
+  alignas(16) float x[kWaves][8][kXRow];  // transposed score tile per wave
+  float wo[kWaves][16][kDim];             // per-wave P.V (rows: heads x {hi, lo})
   float wl[kWaves][16];
   int wm[kWaves][8];
   int last;
@@ -185,67 +254,19 @@ struct Smem {
 
 template <int MODE, int G, int K, bool DEBUG>
 __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a) {
-  using S = Smem<MODE, G, K>;
-  __shared__ S sm;
-  constexpr bool kPacked = S::kPacked;
-  constexpr int NP = S::NP;
+  using QL = QLayout<MODE, G, K>;
+  __shared__ DecodeSmem sm;
+  constexpr bool kPacked = QL::kPacked;
+  constexpr int NP = QL::NP;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int64_t seq = (int64_t)b * a.Hkv + kvh;
   const int64_t row0 = seq * a.t_cap;
   const uint16_t* vseq = a.v + row0 * kDim;
-
-  // ---- prologue: rotate and quantise this kv head's G query vectors --------
-  for (int h = wave; h < G; h += kWaves) {
-    const int64_t bq = (int64_t)b * a.Hq + a.q_of_kv[kvh * G + h];
-    float qv = a.q[bq * kDim + lane];
-    if constexpr (MODE == kScoreFp16) {
-      const uint32_t bits = __half_as_ushort(__float2half_rn(qv));
-      const uint32_t other = __shfl_xor(bits, 1, 64);
-      if ((lane & 1) == 0) sm.q[(lane >> 1) * G + h] = (int32_t)(bits | (other << 16));
-      if (lane == 0) sm.c[h] = __fmul_rn(log2e_f32(), 0.125f);
-    } else {
-      if (a.hadamard) qv = (float)(wave_fwht64((double)qv) * 0.125);
-      float step;
-      const int qi = wave_quantize_int8(qv, &step);
-      sm.qh[h * kDim + lane] = qi;
-      if constexpr (MODE == kScorePot) {
-        if (lane == 0)
-          sm.c[h] = __fmul_rn(__fmul_rn(step, log2e_f32()),
-                              __builtin_amdgcn_ldexpf(1.0f, -(a.frac_bits + K + 3)));
-      } else {
-        uint32_t word = (uint32_t)(qi & 0xFF) << (8 * (lane & 3));
-        word |= __shfl_xor(word, 1, 64);
-        word |= __shfl_xor(word, 2, 64);
-        if ((lane & 3) == 0) sm.q[(lane >> 2) * G + h] = (int32_t)word;
-        if (lane == 0) sm.c[h] = __fmul_rn(__fmul_rn(step, log2e_f32()), 0.125f);
-      }
-      if constexpr (DEBUG) {
-        if (split == 0) {
-          if (a.dbg_qhat) a.dbg_qhat[bq * kDim + lane] = (int8_t)qi;
-          if (a.dbg_delta && lane == 0) a.dbg_delta[bq] = step;
-        }
-      }
-    }
-  }
-  __syncthreads();
-  if constexpr (MODE == kScorePot) {
-    if constexpr (kPacked) {
-      // pair p holds heads 2p (low field) and 2p+1 (high field) as one integer
-      for (int i = tid; i < kDim * NP; i += kBlock) {
-        const int m = i / NP, p = i % NP;
-        sm.q[i] = (int32_t)((uint32_t)sm.qh[(2 * p) * kDim + m] +
-                            ((uint32_t)sm.qh[(2 * p + 1) * kDim + m] << 16));
-      }
-    } else {
-      for (int i = tid; i < (K + 1) * kDim * G; i += kBlock) {
-        const int h = i % G, bm = i / G, bb = bm / kDim, m = bm % kDim;
-        sm.q[i] = sm.qh[h * kDim + m] * (1 << bb);
-      }
-    }
-    __syncthreads();
-  }
+  // query operands and score factors: uniform, read-only here -> scalar loads
+  const int32_t* __restrict__ qb = a.qbuf + seq * a.qstride;
+  const float* __restrict__ cb = reinterpret_cast<const float*>(qb + QL::kWords);
 
   // ---- per-wave streaming over 64-key tiles ------------------------------------
   const int t_begin = split * a.split_len;
@@ -263,15 +284,23 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a) {
   for (int i = 0; i < 8; ++i) ones[i] = (_Float16)1.0f;
 
   KeyRegs<MODE, K> kr[2];
-  ValRegs vr[2];
+  const int g_last = (t_end - 1) & ~7;  // first token of the range's last 8-token group
+  // key codes of tile jt; keys past the range load the range's last key
+  auto load_keys_tile = [&](int jt, KeyRegs<MODE, K>& kk) {
+    const int t0 = t_begin + kWTile * jt;
+    load_keys<MODE, K>(a, row0 + min(t0 + lane, t_end - 1), kk);
+  };
   int j = wave;
-  if (j < n_tiles) {
-    const int t0 = t_begin + kWTile * j;
-    load_keys<MODE, K>(a, row0 + t0 + lane, t0 + lane < t_end, kr[0]);
-    load_values(vseq, t0, t_end, lane, vr[0]);
-  }
+  const int j_last = n_tiles - 1;
+  if (j < n_tiles) load_keys_tile(j, kr[0]);
 
-  auto process = [&](const KeyRegs<MODE, K>& ks, const ValRegs& vs, int t0) {
+  // One tile: issue its value loads and the key loads of this wave's next
+  // tile, then score (the value loads land meanwhile), then A.V.
+  auto process = [&](const KeyRegs<MODE, K>& ks, KeyRegs<MODE, K>& knext, int jt) {
+    const int t0 = t_begin + kWTile * jt;
+    ValRegs vs;
+    load_values(vseq, t0, g_last, lane, vs);
+    load_keys_tile(min(jt + kWaves, j_last), knext);
     const int t = t0 + lane;
     const bool kvalid = t < t_end;
     float xs[G];
@@ -287,7 +316,6 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a) {
         uint32_t accA[NP], accB[NP];
 #pragma unroll
         for (int p = 0; p < NP; ++p) accA[p] = accB[p] = 0u;
-        const uint4* qp4 = reinterpret_cast<const uint4*>(sm.q);
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
           const uint32_t e0 = (w[i] & 0x07070707u) + 0x19191919u;
@@ -302,14 +330,9 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a) {
               const int m = 8 * i + 2 * jj + hf;
               const uint32_t sh = (hf ? e1 : e0) >> (8 * jj);
               const uint32_t sgn = (uint32_t)((int32_t)(w[i] << (28 - 4 * (2 * jj + hf))) >> 31);
-              uint32_t qq[4];
-              if constexpr (NP == 4) {
-                const uint4 q4 = qp4[m];
-                qq[0] = q4.x; qq[1] = q4.y; qq[2] = q4.z; qq[3] = q4.w;
-              } else {
+              uint32_t qq[NP];
 #pragma unroll
-                for (int p = 0; p < NP; ++p) qq[p] = (uint32_t)sm.q[m * NP + p];
-              }
+              for (int p = 0; p < NP; ++p) qq[p] = (uint32_t)qb[m * NP + p];
 #pragma unroll
               for (int p = 0; p < NP; ++p)
                 P[p] = xad_u32(__builtin_amdgcn_alignbit(qq[p], 0u, sh), sgn, P[p]);
@@ -344,10 +367,10 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a) {
           }
 #pragma unroll
           for (int h = 0; h < G; ++h) {
-            uint32_t term = __builtin_amdgcn_alignbit((uint32_t)sm.q[(K * kDim + m) * G + h], 0u, sh);
+            uint32_t term = __builtin_amdgcn_alignbit((uint32_t)qb[(K * kDim + m) * G + h], 0u, sh);
 #pragma unroll
             for (int bb = 0; bb < K; ++bb)
-              term += __builtin_amdgcn_alignbit((uint32_t)sm.q[(bb * kDim + m) * G + h], 0u, shb[bb]);
+              term += __builtin_amdgcn_alignbit((uint32_t)qb[(bb * kDim + m) * G + h], 0u, shb[bb]);
             accu[h] = xad_u32(term, sgn, accu[h]);
           }
         }
@@ -359,7 +382,7 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a) {
         int32_t v = accv[h];
         v = a.frac_bits >= kFInt ? (int32_t)((uint32_t)v << (a.frac_bits - kFInt))
                                  : (v >> (kFInt - a.frac_bits));
-        xs[h] = kvalid ? __fmul_rn(__fmul_rn((float)v, ks.s), sm.c[h]) : -INFINITY;
+        xs[h] = kvalid ? __fmul_rn(__fmul_rn((float)v, ks.s), cb[h]) : -INFINITY;
         if constexpr (DEBUG) {
           if (a.dbg_scores && kvalid)
             a.dbg_scores[((int64_t)b * a.Hq + a.q_of_kv[kvh * G + h]) * a.T + t] = v;
@@ -381,10 +404,10 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a) {
       for (int i = 0; i < 16; ++i)
 #pragma unroll
         for (int h = 0; h < G; ++h)
-          accd[h] = __builtin_amdgcn_sdot4(sm.q[i * G + h], kw[i], accd[h], false);
+          accd[h] = __builtin_amdgcn_sdot4(qb[i * G + h], kw[i], accd[h], false);
 #pragma unroll
       for (int h = 0; h < G; ++h) {
-        xs[h] = kvalid ? __fmul_rn(__fmul_rn((float)accd[h], ks.s), sm.c[h]) : -INFINITY;
+        xs[h] = kvalid ? __fmul_rn(__fmul_rn((float)accd[h], ks.s), cb[h]) : -INFINITY;
         if constexpr (DEBUG) {
           if (a.dbg_scores && kvalid)
             a.dbg_scores[((int64_t)b * a.Hq + a.q_of_kv[kvh * G + h]) * a.T + t] = accd[h];
@@ -406,10 +429,10 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a) {
       for (int i = 0; i < 32; ++i)
 #pragma unroll
         for (int h = 0; h < G; ++h)
-          dot[h] = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2v, sm.q[i * G + h]),
+          dot[h] = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2v, qb[i * G + h]),
                                           __builtin_bit_cast(half2v, kw[i]), dot[h], false);
 #pragma unroll
-      for (int h = 0; h < G; ++h) xs[h] = kvalid ? __fmul_rn(dot[h], sm.c[h]) : -INFINITY;
+      for (int h = 0; h < G; ++h) xs[h] = kvalid ? __fmul_rn(dot[h], cb[h]) : -INFINITY;
     }
 
     // ---- 2. transpose through wave-private LDS ----
@@ -419,15 +442,13 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a) {
     float xv[2][8];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
-      if (hvalid) {
-        const float4* src = reinterpret_cast<const float4*>(&sm.x[wave][hrow][32 * kb + 8 * grp]);
-        const float4 u0 = src[0], u1 = src[1];
-        xv[kb][0] = u0.x; xv[kb][1] = u0.y; xv[kb][2] = u0.z; xv[kb][3] = u0.w;
-        xv[kb][4] = u1.x; xv[kb][5] = u1.y; xv[kb][6] = u1.z; xv[kb][7] = u1.w;
-      } else {
+      // rows of heads >= G are never written: read row 0 and discard
+      const float4* src =
+          reinterpret_cast<const float4*>(&sm.x[wave][hvalid ? hrow : 0][32 * kb + 8 * grp]);
+      const float4 u0 = src[0], u1 = src[1];
+      const float r8[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
 #pragma unroll
-        for (int i = 0; i < 8; ++i) xv[kb][i] = -INFINITY;
-      }
+      for (int i = 0; i < 8; ++i) xv[kb][i] = hvalid ? r8[i] : -INFINITY;
     }
     wave_sync_lds();  // the tile buffer is rewritten by the next tile
 
@@ -453,6 +474,7 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a) {
     m_run = m_new;
 
     // ---- 4. weights (fp16 high / low parts) and P.V on the matrix cores ----
+    if (t0 + kWTile > t_end) mask_values(t0, t_end, lane, vs);  // wave-uniform
     const float bias = hvalid ? kPScale - (float)m_run : 0.0f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
@@ -476,22 +498,15 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a) {
     }
   };
 
-  for (; j < n_tiles; j += 2 * kWaves) {
-    const int j1 = j + kWaves;
-    if (j1 < n_tiles) {
-      const int t1 = t_begin + kWTile * j1;
-      load_keys<MODE, K>(a, row0 + t1 + lane, t1 + lane < t_end, kr[1]);
-      load_values(vseq, t1, t_end, lane, vr[1]);
+  if (j < n_tiles) {
+    for (;;) {
+      process(kr[0], kr[1], j);
+      j += kWaves;
+      if (j >= n_tiles) break;
+      process(kr[1], kr[0], j);
+      j += kWaves;
+      if (j >= n_tiles) break;
     }
-    process(kr[0], vr[0], t_begin + kWTile * j);
-    if (j1 >= n_tiles) break;
-    const int j2 = j1 + kWaves;
-    if (j2 < n_tiles) {
-      const int t2 = t_begin + kWTile * j2;
-      load_keys<MODE, K>(a, row0 + t2 + lane, t2 + lane < t_end, kr[0]);
-      load_values(vseq, t2, t_end, lane, vr[0]);
-    }
-    process(kr[1], vr[1], t_begin + kWTile * j1);
   }
 
   // ---- merge the four waves ---------------------------------------------------
@@ -537,42 +552,78 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a) {
       }
     }
   }
-  if (Sn == 1) return;
+}
 
-  // ---- split combine by the last workgroup of this (batch, kv head) ------------
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) {
-    const uint32_t old = atomicAdd(&a.counters[seq], 1u);
-    sm.last = (old == (uint32_t)(Sn - 1));
+// Merges the key splits of one (batch, query head): M = max_s M_s and
+// O = sum_s 2^(M_s - M) o_s / sum_s 2^(M_s - M) l_s with exact power-of-two
+// weights (Sec. II-E). Grid B * Hq, one thread per output dimension.
+template <bool DEBUG>
+__global__ __launch_bounds__(64) void combine_kernel(const DecodeArgs a) {
+  const int64_t bq = blockIdx.x;
+  const int d = threadIdx.x;
+  const int Sn = a.n_splits;
+  const int32_t* __restrict__ pm = a.part_m + bq * Sn;
+  const float* __restrict__ pl = a.part_l + bq * Sn;
+  const float* __restrict__ po = a.part_o + bq * Sn * kDim;
+  int M = INT_MIN;
+  for (int s = 0; s < Sn; ++s) M = max(M, pm[s]);
+  float L = 0.0f, O = 0.0f;
+  for (int s = 0; s < Sn; ++s) {
+    const float f = __builtin_amdgcn_ldexpf(1.0f, pm[s] - M);
+    L = fmaf(f, pl[s], L);
+    O = fmaf(f, po[s * kDim + d], O);
   }
-  __syncthreads();
-  if (!sm.last) return;
-  __threadfence();
-  for (int idx = tid; idx < G * kDim; idx += kBlock) {
-    const int h = idx / kDim, d = idx % kDim;
-    const int64_t bq = (int64_t)b * a.Hq + a.q_of_kv[kvh * G + h];
-    int M = INT_MIN;
-    for (int s = 0; s < Sn; ++s) M = max(M, a.part_m[bq * Sn + s]);
-    float L = 0.0f, O = 0.0f;
-    for (int s = 0; s < Sn; ++s) {
-      const float f = __builtin_amdgcn_ldexpf(1.0f, a.part_m[bq * Sn + s] - M);
-      L = fmaf(f, a.part_l[bq * Sn + s], L);
-      O = fmaf(f, a.part_o[(bq * Sn + s) * kDim + d], O);
-    }
-    a.out[bq * kDim + d] = O / L;
-    if constexpr (DEBUG) {
-      if (d == 0 && a.dbg_m_final) a.dbg_m_final[bq] = M;
-    }
+  a.out[bq * kDim + d] = O / L;
+  if constexpr (DEBUG) {
+    if (d == 0 && a.dbg_m_final) a.dbg_m_final[bq] = M;
   }
-  if (tid == 0) a.counters[seq] = 0u;
 }
 
 template <int MODE, int G, int K, bool DEBUG>
 static hipError_t launch_t(const DecodeArgs& a, hipStream_t stream) {
+  hipLaunchKernelGGL((prep_queries_kernel<MODE, G, K, DEBUG>), dim3((uint32_t)a.Hkv, (uint32_t)a.B),
+                     dim3(kBlock), 0, stream, a);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   const dim3 grid((uint32_t)a.n_splits, (uint32_t)a.Hkv, (uint32_t)a.B);
   hipLaunchKernelGGL((decode_kernel<MODE, G, K, DEBUG>), grid, dim3(kBlock), 0, stream, a);
+  if (a.n_splits == 1) return hipGetLastError();
+  const hipError_t e2 = hipGetLastError();
+  if (e2 != hipSuccess) return e2;
+  hipLaunchKernelGGL((combine_kernel<DEBUG>), dim3((uint32_t)(a.B * a.Hq)), dim3(64), 0, stream,
+                     a);
   return hipGetLastError();
+}
+
+template <int MODE, int G, int K>
+static int occupancy_t() {
+  int n = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+          &n, reinterpret_cast<const void*>(&decode_kernel<MODE, G, K, false>), kBlock, 0) !=
+      hipSuccess)
+    return 0;
+  return n;
+}
+
+int decode_occupancy(int mode, int G, int mant_bits) {
+  auto by_k = [&](auto g_tag) -> int {
+    constexpr int GG = decltype(g_tag)::value;
+    if (mode == kScoreInt8) return occupancy_t<kScoreInt8, GG, 0>();
+    if (mode == kScoreFp16) return occupancy_t<kScoreFp16, GG, 0>();
+    switch (mant_bits) {
+      case 0: return occupancy_t<kScorePot, GG, 0>();
+      case 1: return occupancy_t<kScorePot, GG, 1>();
+      case 2: return occupancy_t<kScorePot, GG, 2>();
+      case 3: return occupancy_t<kScorePot, GG, 3>();
+      default: return occupancy_t<kScorePot, GG, 4>();
+    }
+  };
+  switch (G) {
+    case 1: return by_k(std::integral_constant<int, 1>{});
+    case 2: return by_k(std::integral_constant<int, 2>{});
+    case 4: return by_k(std::integral_constant<int, 4>{});
+    default: return by_k(std::integral_constant<int, 8>{});
+  }
 }
 
 template <int MODE, int G, bool DEBUG>

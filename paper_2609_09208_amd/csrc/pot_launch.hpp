@@ -50,7 +50,8 @@ struct DecodeArgs {
   const uint16_t* v;
   float* out;
   // workspace
-  uint32_t* counters;        // [B*Hkv]
+  int32_t* qbuf;             // [B*Hkv][qstride]: prepared query operands per kv head
+  int32_t qstride;           // 32-bit words per kv head in qbuf
   int32_t* part_m;           // [B*Hq*S]
   float* part_l;             // [B*Hq*S]
   float* part_o;             // [B*Hq*S*64]
@@ -66,6 +67,15 @@ struct DecodeArgs {
   int32_t frac_bits, hadamard;
   int32_t q_of_kv[kMaxHqArg];  // [Hkv][G] query heads served by each kv head
 };
+
+// 32-bit words of prepared query operands per kv head for group size G:
+// room for the largest layout ((k+1) shifted copies x 64 elements x G heads)
+// plus the G per-head score factors.
+constexpr int query_words(int G) { return ((5 * 64 + 1) * G + 63) / 64 * 64; }
+
+// Resident workgroups per CU of the (non-debug) decode kernel for this
+// variant, from the HIP occupancy calculator; 0 if the query fails.
+int decode_occupancy(int mode, int G, int mant_bits);
 
 hipError_t launch_decode(int mode, int G, int mant_bits, bool debug,
                          const DecodeArgs& a, hipStream_t stream);
