@@ -294,13 +294,28 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a) {
   const int j_last = n_tiles - 1;
   if (j < n_tiles) load_keys_tile(j, kr[0]);
 
-  // One tile: issue its value loads and the key loads of this wave's next
-  // tile, then score (the value loads land meanwhile), then A.V.
-  auto process = [&](const KeyRegs<MODE, K>& ks, KeyRegs<MODE, K>& knext, int jt) {
+  // PoT scoring is long enough to cover the latency of value loads issued at
+  // the start of the tile; the short INT8 / fp16 scoring is not, so those
+  // prefetch the values of this wave's next tile as well.
+  constexpr bool kPrefetchV = MODE != kScorePot;
+  ValRegs vr[kPrefetchV ? 2 : 1];
+  if constexpr (kPrefetchV) {
+    if (j < n_tiles) load_values(vseq, t_begin + kWTile * j, g_last, lane, vr[0]);
+  }
+
+  // One tile: issue the loads it still needs and those of this wave's next
+  // tile, then score (the loads land meanwhile), then A.V.
+  auto process = [&](const KeyRegs<MODE, K>& ks, KeyRegs<MODE, K>& knext, ValRegs& vs,
+                     ValRegs& vnext, int jt) {
     const int t0 = t_begin + kWTile * jt;
-    ValRegs vs;
-    load_values(vseq, t0, g_last, lane, vs);
-    load_keys_tile(min(jt + kWaves, j_last), knext);
+    const int jn = min(jt + kWaves, j_last);
+    if constexpr (kPrefetchV) {
+      load_keys_tile(jn, knext);
+      load_values(vseq, t_begin + kWTile * jn, g_last, lane, vnext);
+    } else {
+      load_values(vseq, t0, g_last, lane, vs);
+      load_keys_tile(jn, knext);
+    }
     const int t = t0 + lane;
     const bool kvalid = t < t_end;
     float xs[G];
@@ -377,11 +392,16 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a) {
 #pragma unroll
         for (int h = 0; h < G; ++h) accv[h] = (int32_t)(accu[h] + (uint32_t)nneg);
       }
+      if (a.frac_bits != kFInt) {  // uniform: rescale to head-room F exactly
+#pragma unroll
+        for (int h = 0; h < G; ++h)
+          accv[h] = a.frac_bits > kFInt
+                        ? (int32_t)((uint32_t)accv[h] << (a.frac_bits - kFInt))
+                        : (accv[h] >> (kFInt - a.frac_bits));
+      }
 #pragma unroll
       for (int h = 0; h < G; ++h) {
-        int32_t v = accv[h];
-        v = a.frac_bits >= kFInt ? (int32_t)((uint32_t)v << (a.frac_bits - kFInt))
-                                 : (v >> (kFInt - a.frac_bits));
+        const int32_t v = accv[h];
         xs[h] = kvalid ? __fmul_rn(__fmul_rn((float)v, ks.s), cb[h]) : -INFINITY;
         if constexpr (DEBUG) {
           if (a.dbg_scores && kvalid)
@@ -476,6 +496,9 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a) {
     // ---- 4. weights (fp16 high / low parts) and P.V on the matrix cores ----
     if (t0 + kWTile > t_end) mask_values(t0, t_end, lane, vs);  // wave-uniform
     const float bias = hvalid ? kPScale - (float)m_run : 0.0f;
+    // rows 0-7 take the fp16 high part h = rtz(p), rows 8-15 the low part
+    // rtz(p - h): one fused p + m * h with m = 0 or -1 serves both
+    const float mlo = part ? -1.0f : 0.0f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
       half8 af;
@@ -484,9 +507,9 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a) {
         const float p0 = __builtin_amdgcn_exp2f(xv[kb][i] + bias);
         const float p1 = __builtin_amdgcn_exp2f(xv[kb][i + 1] + bias);
         const half2v hi = __builtin_bit_cast(half2v, __builtin_amdgcn_cvt_pkrtz(p0, p1));
-        const half2v lo = __builtin_bit_cast(
-            half2v, __builtin_amdgcn_cvt_pkrtz(p0 - (float)hi.x, p1 - (float)hi.y));
-        const half2v sel = part ? lo : hi;
+        const half2v sel = __builtin_bit_cast(
+            half2v, __builtin_amdgcn_cvt_pkrtz(__builtin_fmaf(mlo, (float)hi.x, p0),
+                                               __builtin_fmaf(mlo, (float)hi.y, p1)));
         af[i] = sel.x;
         af[i + 1] = sel.y;
       }
@@ -500,10 +523,10 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a) {
 
   if (j < n_tiles) {
     for (;;) {
-      process(kr[0], kr[1], j);
+      process(kr[0], kr[1], vr[0], vr[kPrefetchV ? 1 : 0], j);
       j += kWaves;
       if (j >= n_tiles) break;
-      process(kr[1], kr[0], j);
+      process(kr[1], kr[0], vr[kPrefetchV ? 1 : 0], vr[0], j);
       j += kWaves;
       if (j >= n_tiles) break;
     }
