@@ -10,18 +10,20 @@
 //
 // Per 64-key tile and wave:
 //  1. Scores, one key per lane (Sec. II-B eq. sac). PoT-4: the key's 32 code
-//     bytes arrive as two 16-byte loads. Each exponent e gives a funnel-shift
-//     amount sh = e + 25, so v_alignbit(q, 0, sh) = q << (7 - e) for e <= 6
-//     and 0 for the zero code e = 7 (sh = 32 = 0 mod 32); every shift is a
-//     left shift (eq. exact). Two query heads share one 32-bit register as
-//     q_a + 2^16 q_b, so one alignbit shifts both; v_xad_u32 applies the sign
-//     as (t ^ s) + acc with s in {0, -1}, and the missing +1 per negative
-//     element is added once per key from a popcount of the sign bits. After
-//     every 2 elements the 16-bit fields (each at most 2 * 127 * 2^7 in
-//     magnitude, kept non-negative by a 2^15 bias) are added into two int32
-//     accumulators by SDWA word adds, so the sums stay exact. PoT-Mk and the
-//     single-head case use one int32 accumulator per head with one more
-//     alignbit per mantissa bit.
+//     bytes arrive as two 16-byte loads. Two query heads share one 32-bit
+//     operand Q2 = 2 (q_a + 2^16 q_b), whose bit 0 is clear. Each code byte
+//     holds two exponents; one subtraction per code word turns four of them
+//     into shift bytes s = (6 - e) mod 32, and an SDWA v_lshlrev_b32 reads its
+//     shift straight from one byte: Q2 << (6 - e) = (q_a + 2^16 q_b) << (7 - e)
+//     for e <= 6, and Q2 << 31 = 0 for the zero code e = 7. Every shift is a
+//     left shift (eq. exact). v_xad_u32 applies the sign as (t ^ s) + acc with
+//     s in {0, -1}; the missing +1 per negative element is added once per key
+//     from a popcount of the sign bits. After every 2 elements the 16-bit
+//     fields (each at most 2 * 127 * 2^7 in magnitude, kept non-negative by a
+//     2^15 bias) are added into two int32 accumulators by SDWA word adds, so
+//     the sums stay exact. PoT-Mk and the single-head case use one int32
+//     accumulator per head and v_alignbit(q, 0, e + 25) = q << (7 - e) (0 for
+//     e = 7), one more per mantissa bit.
 //  2. x = fl32(fl32(float(acc) * s) * c), c = fl32(fl32(Delta * log2 e) *
 //     2^-(F+k+3)) in this order; x is staged transposed in wave-private LDS.
 //  3. Integer running maximum M = max(M, ceil(max x)) per head (eq. logsm);
@@ -55,6 +57,7 @@ constexpr int kWaves = kBlock / 64;
 constexpr int kWTile = 64;    // keys per wave tile
 constexpr int kXRow = 68;     // floats per head row of the transposed score tile
 constexpr float kPScale = 12.0f;  // p is formed as 2^(x - M + 12) (fp16-normal range)
+constexpr int kDppRowRor8 = 0x128;  // DPP row_ror:8: lane l reads lane l ^ 8 within its row of 16
 
 // ---- VALU forms the compiler does not pick by itself ------------------------
 __device__ __forceinline__ uint32_t xad_u32(uint32_t a, uint32_t b, uint32_t c) {
@@ -79,6 +82,30 @@ __device__ __forceinline__ uint32_t add_hi16s(uint32_t acc, uint32_t p) {
       : "=v"(r)
       : "v"(p), "v"(acc));
   return r;
+}
+
+// q << (byte BYTE of sh) (shift taken mod 32), with q a wave-uniform operand
+template <int BYTE>
+__device__ __forceinline__ uint32_t shl_by_byte(uint32_t sh, uint32_t q) {
+  uint32_t r;
+  if constexpr (BYTE == 0)
+    asm("v_lshlrev_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_0 "
+        "src1_sel:DWORD" : "=v"(r) : "v"(sh), "s"(q));
+  else if constexpr (BYTE == 1)
+    asm("v_lshlrev_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_1 "
+        "src1_sel:DWORD" : "=v"(r) : "v"(sh), "s"(q));
+  else if constexpr (BYTE == 2)
+    asm("v_lshlrev_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_2 "
+        "src1_sel:DWORD" : "=v"(r) : "v"(sh), "s"(q));
+  else
+    asm("v_lshlrev_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_3 "
+        "src1_sel:DWORD" : "=v"(r) : "v"(sh), "s"(q));
+  return r;
+}
+
+// max(a, b) for scores (never NaN) as v_max_f32 without operand canonicalisation
+__device__ __forceinline__ float max_f32(float a, float b) {
+  return __builtin_amdgcn_fmed3f(a, b, __builtin_inff());
 }
 
 __device__ __forceinline__ void wave_sync_lds() {
@@ -171,7 +198,7 @@ __device__ __forceinline__ void mask_values(int t0, int t_end, int lane, ValRegs
 }
 
 // ---- prepared query operands (workspace, one block per kv head) -------------
-// PoT-4 with G >= 2: [m][pair] words q_{2p} + 2^16 q_{2p+1}; other PoT forms:
+// PoT-4 with G >= 2: [m][pair] words 2 (q_{2p} + 2^16 q_{2p+1}); other PoT forms:
 // [(b' * 64 + m) * G + h] = q << b'; INT8: [i * G + h] four int8 per word;
 // fp16: [i * G + h] two fp16 per word. The G per-head score factors follow.
 template <int MODE, int G, int K>
@@ -228,11 +255,12 @@ __global__ __launch_bounds__(kBlock) void prep_queries_kernel(const DecodeArgs a
   if constexpr (MODE == kScorePot) {
     __syncthreads();
     if constexpr (QL::kPacked) {
-      // pair p holds heads 2p (low field) and 2p+1 (high field) as one integer
+      // pair p holds heads 2p (low field) and 2p+1 (high field) as one
+      // integer, doubled so that a shift by 31 clears it
       for (int i = tid; i < kDim * QL::NP; i += kBlock) {
         const int m = i / QL::NP, p = i % QL::NP;
-        qb[i] = (int32_t)((uint32_t)qh[(2 * p) * kDim + m] +
-                          ((uint32_t)qh[(2 * p + 1) * kDim + m] << 16));
+        qb[i] = (int32_t)(((uint32_t)qh[(2 * p) * kDim + m] +
+                           ((uint32_t)qh[(2 * p + 1) * kDim + m] << 16)) << 1);
       }
     } else {
       for (int i = tid; i < (K + 1) * kDim * G; i += kBlock) {
@@ -253,19 +281,26 @@ struct alignas(16) DecodeSmem {
 };
 
 template <int MODE, int G, int K, bool DEBUG>
-__global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a) {
+// qbuf is passed on its own as a restrict parameter: the prepared query
+// operands are never written here, which lets the compiler read them through
+// the scalar cache even in the debug variants that store score taps.
+__global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
+                                                        const int32_t* __restrict__ qbuf) {
   using QL = QLayout<MODE, G, K>;
   __shared__ DecodeSmem sm;
   constexpr bool kPacked = QL::kPacked;
   constexpr int NP = QL::NP;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  // the wave index is uniform in a wave; saying so keeps the tile loop's
+  // control flow scalar (no per-lane loop exit masks)
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int64_t seq = (int64_t)b * a.Hkv + kvh;
   const int64_t row0 = seq * a.t_cap;
   const uint16_t* vseq = a.v + row0 * kDim;
   // query operands and score factors: uniform, read-only here -> scalar loads
-  const int32_t* __restrict__ qb = a.qbuf + seq * a.qstride;
+  const int32_t* __restrict__ qb = qbuf + seq * a.qstride;
   const float* __restrict__ cb = reinterpret_cast<const float*>(qb + QL::kWords);
 
   // ---- per-wave streaming over 64-key tiles ------------------------------------
@@ -282,6 +317,11 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a) {
   half8 ones;
 #pragma unroll
   for (int i = 0; i < 8; ++i) ones[i] = (_Float16)1.0f;
+  // byte addresses of lanes l ^ 16 and l ^ 32 for ds_bpermute
+  const int bp16 = (lane ^ 16) << 2, bp32 = (lane ^ 32) << 2;
+  // -1 kept opaque so that p - hi stays one fma_mix reading hi as fp16
+  float neg_one = -1.0f;
+  asm("" : "+v"(neg_one));
 
   KeyRegs<MODE, K> kr[2];
   const int g_last = (t_end - 1) & ~7;  // first token of the range's last 8-token group
@@ -331,33 +371,34 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a) {
         uint32_t accA[NP], accB[NP];
 #pragma unroll
         for (int p = 0; p < NP; ++p) accA[p] = accB[p] = 0u;
+        // one 2-element step: byte JJ of the shift words holds the shifts of
+        // elements 8i + 2JJ (s0) and 8i + 2JJ + 1 (s1)
+        auto step = [&](auto jj_tag, int i, uint32_t wi, uint32_t s0, uint32_t s1) {
+          constexpr int JJ = decltype(jj_tag)::value;
+          const int m = 8 * i + 2 * JJ;
+          const uint32_t sg0 = (uint32_t)((int32_t)(wi << (28 - 8 * JJ)) >> 31);
+          const uint32_t sg1 = (uint32_t)((int32_t)(wi << (24 - 8 * JJ)) >> 31);
+          uint32_t P[NP];
+#pragma unroll
+          for (int p = 0; p < NP; ++p)
+            P[p] = xad_u32(shl_by_byte<JJ>(s0, (uint32_t)qb[m * NP + p]), sg0, 0x8000u);
+#pragma unroll
+          for (int p = 0; p < NP; ++p)
+            P[p] = xad_u32(shl_by_byte<JJ>(s1, (uint32_t)qb[(m + 1) * NP + p]), sg1, P[p]);
+#pragma unroll
+          for (int p = 0; p < NP; ++p) {
+            accA[p] = add_lo16(accA[p], P[p]);
+            accB[p] = add_hi16s(accB[p], P[p]);
+          }
+        };
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-          const uint32_t e0 = (w[i] & 0x07070707u) + 0x19191919u;
-          const uint32_t e1 = ((w[i] >> 4) & 0x07070707u) + 0x19191919u;
-#pragma unroll
-          for (int jj = 0; jj < 4; ++jj) {
-            uint32_t P[NP];
-#pragma unroll
-            for (int p = 0; p < NP; ++p) P[p] = 0x8000u;
-#pragma unroll
-            for (int hf = 0; hf < 2; ++hf) {
-              const int m = 8 * i + 2 * jj + hf;
-              const uint32_t sh = (hf ? e1 : e0) >> (8 * jj);
-              const uint32_t sgn = (uint32_t)((int32_t)(w[i] << (28 - 4 * (2 * jj + hf))) >> 31);
-              uint32_t qq[NP];
-#pragma unroll
-              for (int p = 0; p < NP; ++p) qq[p] = (uint32_t)qb[m * NP + p];
-#pragma unroll
-              for (int p = 0; p < NP; ++p)
-                P[p] = xad_u32(__builtin_amdgcn_alignbit(qq[p], 0u, sh), sgn, P[p]);
-            }
-#pragma unroll
-            for (int p = 0; p < NP; ++p) {
-              accA[p] = add_lo16(accA[p], P[p]);
-              accB[p] = add_hi16s(accB[p], P[p]);
-            }
-          }
+          const uint32_t s0 = 0x26262626u - (w[i] & 0x07070707u);
+          const uint32_t s1 = 0x26262626u - ((w[i] >> 4) & 0x07070707u);
+          step(std::integral_constant<int, 0>{}, i, w[i], s0, s1);
+          step(std::integral_constant<int, 1>{}, i, w[i], s0, s1);
+          step(std::integral_constant<int, 2>{}, i, w[i], s0, s1);
+          step(std::integral_constant<int, 3>{}, i, w[i], s0, s1);
         }
 #pragma unroll
         for (int p = 0; p < NP; ++p) {
@@ -402,7 +443,7 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a) {
 #pragma unroll
       for (int h = 0; h < G; ++h) {
         const int32_t v = accv[h];
-        xs[h] = kvalid ? __fmul_rn(__fmul_rn((float)v, ks.s), cb[h]) : -INFINITY;
+        xs[h] = __fmul_rn(__fmul_rn((float)v, ks.s), cb[h]);
         if constexpr (DEBUG) {
           if (a.dbg_scores && kvalid)
             a.dbg_scores[((int64_t)b * a.Hq + a.q_of_kv[kvh * G + h]) * a.T + t] = v;
@@ -427,7 +468,7 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a) {
           accd[h] = __builtin_amdgcn_sdot4(qb[i * G + h], kw[i], accd[h], false);
 #pragma unroll
       for (int h = 0; h < G; ++h) {
-        xs[h] = kvalid ? __fmul_rn(__fmul_rn((float)accd[h], ks.s), cb[h]) : -INFINITY;
+        xs[h] = __fmul_rn(__fmul_rn((float)accd[h], ks.s), cb[h]);
         if constexpr (DEBUG) {
           if (a.dbg_scores && kvalid)
             a.dbg_scores[((int64_t)b * a.Hq + a.q_of_kv[kvh * G + h]) * a.T + t] = accd[h];
@@ -452,84 +493,115 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a) {
           dot[h] = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2v, qb[i * G + h]),
                                           __builtin_bit_cast(half2v, kw[i]), dot[h], false);
 #pragma unroll
-      for (int h = 0; h < G; ++h) xs[h] = kvalid ? __fmul_rn(dot[h], cb[h]) : -INFINITY;
+      for (int h = 0; h < G; ++h) xs[h] = __fmul_rn(dot[h], cb[h]);
     }
 
     // ---- 2. transpose through wave-private LDS ----
+    // Lane (row, grp) takes head row & 7 and keys 32 * part + 8 * grp .. + 7
+    // of the tile (part = row >> 3), so every weight is computed once. Keys
+    // past the range carry the score of the range's last key (clamped loads):
+    // they cannot raise the maximum and are zeroed below in the tail tile.
 #pragma unroll
     for (int h = 0; h < G; ++h) sm.x[wave][h][lane] = xs[h];
     wave_sync_lds();
-    float xv[2][8];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    float xv[8];
+    {
       // rows of heads >= G are never written: read row 0 and discard
       const float4* src =
-          reinterpret_cast<const float4*>(&sm.x[wave][hvalid ? hrow : 0][32 * kb + 8 * grp]);
+          reinterpret_cast<const float4*>(&sm.x[wave][hvalid ? hrow : 0][32 * part + 8 * grp]);
       const float4 u0 = src[0], u1 = src[1];
       const float r8[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
 #pragma unroll
-      for (int i = 0; i < 8; ++i) xv[kb][i] = hvalid ? r8[i] : -INFINITY;
+      for (int i = 0; i < 8; ++i) xv[i] = hvalid ? r8[i] : -INFINITY;
     }
     wave_sync_lds();  // the tile buffer is rewritten by the next tile
+    const bool tail = t0 + kWTile > t_end;  // wave-uniform
+    if (tail) {
+      const int k0 = t0 + 32 * part + 8 * grp;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) xv[i] = (k0 + i < t_end) ? xv[i] : -INFINITY;
+      mask_values(t0, t_end, lane, vs);
+    }
 
     // ---- 3. integer running maximum per head ----
-    float mx = xv[0][0];
+    float mx = xv[0];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int i = 0; i < 8; ++i) mx = fmaxf(mx, xv[kb][i]);
-    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    for (int i = 1; i < 8; ++i) mx = max_f32(mx, xv[i]);
+    mx = max_f32(mx, __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(
+                                                   __builtin_bit_cast(int, mx), kDppRowRor8, 0xF,
+                                                   0xF, true)));  // the other part
+    mx = max_f32(mx, __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(
+                                                   bp16, __builtin_bit_cast(int, mx))));
+    mx = max_f32(mx, __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(
+                                                   bp32, __builtin_bit_cast(int, mx))));
     const int mt = hvalid ? (int)ceilf(mx) : INT_MIN;
     const int m_new = max(m_run, mt);
     if (__any(m_new != m_run)) {
+      // acc <- diag(2^(M_old - M_new)) acc, also on the matrix cores so the
+      // accumulators never pass through VALU registers inside the loop:
+      // D = sum_j A_j B_j with B_j = acc[.][j] (16x16x4 f32 layout: lane l
+      // holds row 4 (l / 16) + j of column l % 16) and A_j[i][k] = f_i for
+      // i = 4k + j, else 0. Each element gets one exact power-of-two product.
       const float f = (m_run == INT_MIN) ? 0.0f : __builtin_amdgcn_ldexpf(1.0f, m_run - m_new);
+      const int arow = lane & 15, acol = lane >> 4;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float fr = __shfl(f, 4 * grp + r, 64);
+      for (int nb = 0; nb < 5; ++nb) {
+        float4v d = float4v{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-        for (int nb = 0; nb < 5; ++nb) acc[nb][r] *= fr;
+        for (int jj = 0; jj < 4; ++jj)
+          d = __builtin_amdgcn_mfma_f32_16x16x4f32(arow == 4 * acol + jj ? f : 0.0f, acc[nb][jj],
+                                                   d, 0, 0, 0);
+        acc[nb] = d;
       }
     }
     m_run = m_new;
 
     // ---- 4. weights (fp16 high / low parts) and P.V on the matrix cores ----
-    if (t0 + kWTile > t_end) mask_values(t0, t_end, lane, vs);  // wave-uniform
+    // Each lane splits its 8 weights into hi = rtz(p) and lo = rtz(p - hi)
+    // and hands lo to its partner lane (row ^ 8). Block kb = 0 then takes
+    // rows 0-7 = hi, 8-15 = lo of the part-0 weights; block kb = 1 takes rows
+    // 0-7 = lo, 8-15 = hi of the part-1 weights. Rows h and h + 8 are summed
+    // at the end, so both blocks see hi + lo of every weight.
     const float bias = hvalid ? kPScale - (float)m_run : 0.0f;
-    // rows 0-7 take the fp16 high part h = rtz(p), rows 8-15 the low part
-    // rtz(p - h): one fused p + m * h with m = 0 or -1 serves both
-    const float mlo = part ? -1.0f : 0.0f;
+    uint32_t hw[4], lw[4];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      half8 af;
-#pragma unroll
-      for (int i = 0; i < 8; i += 2) {
-        const float p0 = __builtin_amdgcn_exp2f(xv[kb][i] + bias);
-        const float p1 = __builtin_amdgcn_exp2f(xv[kb][i + 1] + bias);
-        const half2v hi = __builtin_bit_cast(half2v, __builtin_amdgcn_cvt_pkrtz(p0, p1));
-        const half2v sel = __builtin_bit_cast(
-            half2v, __builtin_amdgcn_cvt_pkrtz(__builtin_fmaf(mlo, (float)hi.x, p0),
-                                               __builtin_fmaf(mlo, (float)hi.y, p1)));
-        af[i] = sel.x;
-        af[i + 1] = sel.y;
-      }
-#pragma unroll
-      for (int nb = 0; nb < 4; ++nb)
-        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-            af, __builtin_bit_cast(half8, vs.f[kb][nb]), acc[nb], 0, 0, 0);
-      acc[4] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af, ones, acc[4], 0, 0, 0);
+    for (int i = 0; i < 4; ++i) {
+      const float p0 = __builtin_amdgcn_exp2f(xv[2 * i] + bias);
+      const float p1 = __builtin_amdgcn_exp2f(xv[2 * i + 1] + bias);
+      const half2v hi = __builtin_bit_cast(half2v, __builtin_amdgcn_cvt_pkrtz(p0, p1));
+      hw[i] = __builtin_bit_cast(uint32_t, hi);
+      lw[i] = __builtin_bit_cast(
+          uint32_t, __builtin_amdgcn_cvt_pkrtz(__builtin_fmaf(neg_one, (float)hi.x, p0),
+                                               __builtin_fmaf(neg_one, (float)hi.y, p1)));
     }
+    uint32_t a0w[4], a1w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t rl = (uint32_t)__builtin_amdgcn_mov_dpp((int)lw[i], kDppRowRor8, 0xF, 0xF, true);
+      a0w[i] = part ? rl : hw[i];
+      a1w[i] = part ? hw[i] : rl;
+    }
+    const half8 af0 = __builtin_bit_cast(half8, make_uint4(a0w[0], a0w[1], a0w[2], a0w[3]));
+    const half8 af1 = __builtin_bit_cast(half8, make_uint4(a1w[0], a1w[1], a1w[2], a1w[3]));
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb)
+      acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+          af0, __builtin_bit_cast(half8, vs.f[0][nb]), acc[nb], 0, 0, 0);
+    acc[4] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af0, ones, acc[4], 0, 0, 0);
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb)
+      acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+          af1, __builtin_bit_cast(half8, vs.f[1][nb]), acc[nb], 0, 0, 0);
+    acc[4] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af1, ones, acc[4], 0, 0, 0);
   };
 
-  if (j < n_tiles) {
-    for (;;) {
-      process(kr[0], kr[1], vr[0], vr[kPrefetchV ? 1 : 0], j);
-      j += kWaves;
-      if (j >= n_tiles) break;
-      process(kr[1], kr[0], vr[kPrefetchV ? 1 : 0], vr[0], j);
-      j += kWaves;
-      if (j >= n_tiles) break;
-    }
+  // one loop body; the prefetched registers move forward at its end so that
+  // every tile uses the same registers (the accumulators stay in place)
+#pragma nounroll
+  for (; j < n_tiles; j += kWaves) {
+    process(kr[0], kr[1], vr[0], vr[kPrefetchV ? 1 : 0], j);
+    kr[0] = kr[1];
+    if constexpr (kPrefetchV) vr[0] = vr[1];
   }
 
   // ---- merge the four waves ---------------------------------------------------
@@ -609,7 +681,8 @@ static hipError_t launch_t(const DecodeArgs& a, hipStream_t stream) {
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const dim3 grid((uint32_t)a.n_splits, (uint32_t)a.Hkv, (uint32_t)a.B);
-  hipLaunchKernelGGL((decode_kernel<MODE, G, K, DEBUG>), grid, dim3(kBlock), 0, stream, a);
+  hipLaunchKernelGGL((decode_kernel<MODE, G, K, DEBUG>), grid, dim3(kBlock), 0, stream, a,
+                     static_cast<const int32_t*>(a.qbuf));
   if (a.n_splits == 1) return hipGetLastError();
   const hipError_t e2 = hipGetLastError();
   if (e2 != hipSuccess) return e2;
