@@ -108,6 +108,67 @@ __device__ __forceinline__ float max_f32(float a, float b) {
   return __builtin_amdgcn_fmed3f(a, b, __builtin_inff());
 }
 
+// One 2-element step of the packed PoT-4 score for four head pairs (G = 8),
+// as one block so that no wait states are padded between its instructions
+// (all of them are full-dword VALU ops without forwarding hazards):
+//   P_p = ((Q_{m,p} << s0) ^ g0) + 2^15;  P_p += (Q_{m+1,p} << s1) ^ g1;
+//   A_p += P_p & 0xffff;  B_p += sext(P_p >> 16)
+// with the shifts taken from byte JJ of s0 / s1.
+#define POT_STEP8_ASM(JJ)                                                                      \
+  "v_lshlrev_b32_sdwa %[p0], %[s0], %[a0] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_" #JJ \
+  " src1_sel:DWORD\n"                                                                          \
+  "v_lshlrev_b32_sdwa %[p1], %[s0], %[a1] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_" #JJ \
+  " src1_sel:DWORD\n"                                                                          \
+  "v_lshlrev_b32_sdwa %[p2], %[s0], %[a2] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_" #JJ \
+  " src1_sel:DWORD\n"                                                                          \
+  "v_lshlrev_b32_sdwa %[p3], %[s0], %[a3] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_" #JJ \
+  " src1_sel:DWORD\n"                                                                          \
+  "v_xad_u32 %[p0], %[p0], %[g0], %[bias]\n"                                                  \
+  "v_xad_u32 %[p1], %[p1], %[g0], %[bias]\n"                                                  \
+  "v_xad_u32 %[p2], %[p2], %[g0], %[bias]\n"                                                  \
+  "v_xad_u32 %[p3], %[p3], %[g0], %[bias]\n"                                                  \
+  "v_lshlrev_b32_sdwa %[t], %[s1], %[b0] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_" #JJ \
+  " src1_sel:DWORD\n"                                                                          \
+  "v_xad_u32 %[p0], %[t], %[g1], %[p0]\n"                                                     \
+  "v_lshlrev_b32_sdwa %[t], %[s1], %[b1] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_" #JJ \
+  " src1_sel:DWORD\n"                                                                          \
+  "v_xad_u32 %[p1], %[t], %[g1], %[p1]\n"                                                     \
+  "v_lshlrev_b32_sdwa %[t], %[s1], %[b2] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_" #JJ \
+  " src1_sel:DWORD\n"                                                                          \
+  "v_xad_u32 %[p2], %[t], %[g1], %[p2]\n"                                                     \
+  "v_lshlrev_b32_sdwa %[t], %[s1], %[b3] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_" #JJ \
+  " src1_sel:DWORD\n"                                                                          \
+  "v_xad_u32 %[p3], %[t], %[g1], %[p3]\n"                                                     \
+  "v_add_u32_sdwa %[A0], %[p0], %[A0] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 src1_sel:DWORD\n" \
+  "v_add_u32_sdwa %[B0], sext(%[p0]), %[B0] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_1 src1_sel:DWORD\n" \
+  "v_add_u32_sdwa %[A1], %[p1], %[A1] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 src1_sel:DWORD\n" \
+  "v_add_u32_sdwa %[B1], sext(%[p1]), %[B1] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_1 src1_sel:DWORD\n" \
+  "v_add_u32_sdwa %[A2], %[p2], %[A2] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 src1_sel:DWORD\n" \
+  "v_add_u32_sdwa %[B2], sext(%[p2]), %[B2] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_1 src1_sel:DWORD\n" \
+  "v_add_u32_sdwa %[A3], %[p3], %[A3] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 src1_sel:DWORD\n" \
+  "v_add_u32_sdwa %[B3], sext(%[p3]), %[B3] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_1 src1_sel:DWORD"
+
+template <int JJ>
+__device__ __forceinline__ void pot_step8(uint32_t s0, uint32_t s1, uint32_t g0, uint32_t g1,
+                                          const int32_t* __restrict__ qm, uint32_t (&A)[4],
+                                          uint32_t (&B)[4]) {
+  uint32_t p0, p1, p2, p3, t;
+#define POT_STEP8_OPERANDS                                                                   \
+  : [p0] "=&v"(p0), [p1] "=&v"(p1), [p2] "=&v"(p2), [p3] "=&v"(p3), [t] "=&v"(t),          \
+    [A0] "+v"(A[0]), [A1] "+v"(A[1]),                                                        \
+    [A2] "+v"(A[2]), [A3] "+v"(A[3]), [B0] "+v"(B[0]), [B1] "+v"(B[1]), [B2] "+v"(B[2]),    \
+    [B3] "+v"(B[3])                                                                          \
+  : [s0] "v"(s0), [s1] "v"(s1), [g0] "v"(g0), [g1] "v"(g1), [bias] "s"(0x8000u),             \
+    [a0] "s"(qm[0]), [a1] "s"(qm[1]), [a2] "s"(qm[2]), [a3] "s"(qm[3]), [b0] "s"(qm[4]),     \
+    [b1] "s"(qm[5]), [b2] "s"(qm[6]), [b3] "s"(qm[7])
+  if constexpr (JJ == 0) asm(POT_STEP8_ASM(0) POT_STEP8_OPERANDS);
+  else if constexpr (JJ == 1) asm(POT_STEP8_ASM(1) POT_STEP8_OPERANDS);
+  else if constexpr (JJ == 2) asm(POT_STEP8_ASM(2) POT_STEP8_OPERANDS);
+  else asm(POT_STEP8_ASM(3) POT_STEP8_OPERANDS);
+#undef POT_STEP8_OPERANDS
+}
+#undef POT_STEP8_ASM
+
 __device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
@@ -343,10 +404,13 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
     if (j < n_tiles) load_values(vseq, t_begin + kWTile * j, g_last, lane, vr[0]);
   }
 
-  // One tile: issue the loads it still needs and those of this wave's next
-  // tile, then score (the loads land meanwhile), then A.V.
-  auto process = [&](const KeyRegs<MODE, K>& ks, KeyRegs<MODE, K>& knext, ValRegs& vs,
-                     ValRegs& vnext, int jt) {
+  // Stage 1 of a tile: issue the loads it still needs and those of this
+  // wave's next tile, score (the loads land meanwhile), transpose and find
+  // the tile's integer maximum per head (returned in m_new).
+  float xv[8];
+  int m_new = m_run;
+  auto stage1 = [&](const KeyRegs<MODE, K>& ks, KeyRegs<MODE, K>& knext, ValRegs& vs,
+                    ValRegs& vnext, int jt) {
     const int t0 = t_begin + kWTile * jt;
     const int jn = min(jt + kWaves, j_last);
     if constexpr (kPrefetchV) {
@@ -378,6 +442,10 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
           const int m = 8 * i + 2 * JJ;
           const uint32_t sg0 = (uint32_t)((int32_t)(wi << (28 - 8 * JJ)) >> 31);
           const uint32_t sg1 = (uint32_t)((int32_t)(wi << (24 - 8 * JJ)) >> 31);
+          if constexpr (NP == 4) {
+            pot_step8<JJ>(s0, s1, sg0, sg1, qb + m * NP, accA, accB);
+            return;
+          }
           uint32_t P[NP];
 #pragma unroll
           for (int p = 0; p < NP; ++p)
@@ -504,7 +572,6 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
 #pragma unroll
     for (int h = 0; h < G; ++h) sm.x[wave][h][lane] = xs[h];
     wave_sync_lds();
-    float xv[8];
     {
       // rows of heads >= G are never written: read row 0 and discard
       const float4* src =
@@ -535,27 +602,31 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
     mx = max_f32(mx, __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(
                                                    bp32, __builtin_bit_cast(int, mx))));
     const int mt = hvalid ? (int)ceilf(mx) : INT_MIN;
-    const int m_new = max(m_run, mt);
-    if (__any(m_new != m_run)) {
-      // acc <- diag(2^(M_old - M_new)) acc, also on the matrix cores so the
-      // accumulators never pass through VALU registers inside the loop:
-      // D = sum_j A_j B_j with B_j = acc[.][j] (16x16x4 f32 layout: lane l
-      // holds row 4 (l / 16) + j of column l % 16) and A_j[i][k] = f_i for
-      // i = 4k + j, else 0. Each element gets one exact power-of-two product.
-      const float f = (m_run == INT_MIN) ? 0.0f : __builtin_amdgcn_ldexpf(1.0f, m_run - m_new);
-      const int arow = lane & 15, acol = lane >> 4;
+    m_new = max(m_run, mt);
+  };
+
+  // acc <- diag(2^(M_old - M_new)) acc on the matrix cores: D = sum_j A_j B_j
+  // with B_j = acc[.][j] (16x16x4 f32 layout: lane l holds row 4 (l / 16) + j
+  // of column l % 16) and A_j[i][k] = f_i for i = 4k + j, else 0. Each
+  // element gets one exact power-of-two product. It runs outside the hot
+  // loop below, so the accumulators stay in the matrix-core registers there.
+  auto rescale = [&]() {
+    const float f = (m_run == INT_MIN) ? 0.0f : __builtin_amdgcn_ldexpf(1.0f, m_run - m_new);
+    const int arow = lane & 15, acol = lane >> 4;
 #pragma unroll
-      for (int nb = 0; nb < 5; ++nb) {
-        float4v d = float4v{0.0f, 0.0f, 0.0f, 0.0f};
+    for (int nb = 0; nb < 5; ++nb) {
+      float4v d = float4v{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-        for (int jj = 0; jj < 4; ++jj)
-          d = __builtin_amdgcn_mfma_f32_16x16x4f32(arow == 4 * acol + jj ? f : 0.0f, acc[nb][jj],
-                                                   d, 0, 0, 0);
-        acc[nb] = d;
-      }
+      for (int jj = 0; jj < 4; ++jj)
+        d = __builtin_amdgcn_mfma_f32_16x16x4f32(arow == 4 * acol + jj ? f : 0.0f, acc[nb][jj], d,
+                                                 0, 0, 0);
+      acc[nb] = d;
     }
     m_run = m_new;
+  };
 
+  // Stage 2 of a tile: weights from the scores and P.V on the matrix cores.
+  auto stage2 = [&](const ValRegs& vs) {
     // ---- 4. weights (fp16 high / low parts) and P.V on the matrix cores ----
     // Each lane splits its 8 weights into hi = rtz(p) and lo = rtz(p - hi)
     // and hands lo to its partner lane (row ^ 8). Block kb = 0 then takes
@@ -595,13 +666,29 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
     acc[4] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af1, ones, acc[4], 0, 0, 0);
   };
 
-  // one loop body; the prefetched registers move forward at its end so that
-  // every tile uses the same registers (the accumulators stay in place)
-#pragma nounroll
-  for (; j < n_tiles; j += kWaves) {
-    process(kr[0], kr[1], vr[0], vr[kPrefetchV ? 1 : 0], j);
+  // The hot loop runs the tiles that do not raise any head's maximum; a tile
+  // that does leaves it, is rescaled and finished in the outer loop (a few
+  // times per wave). The prefetched registers move forward after each tile so
+  // that every tile uses the same registers.
+  auto advance = [&]() {
     kr[0] = kr[1];
     if constexpr (kPrefetchV) vr[0] = vr[1];
+    j += kWaves;
+  };
+#pragma nounroll
+  while (j < n_tiles) {
+#pragma nounroll
+    for (;;) {
+      stage1(kr[0], kr[1], vr[0], vr[kPrefetchV ? 1 : 0], j);
+      if (__any(m_new != m_run)) break;
+      stage2(vr[0]);
+      advance();
+      if (j >= n_tiles) break;
+    }
+    if (j >= n_tiles) break;
+    rescale();
+    stage2(vr[0]);
+    advance();
   }
 
   // ---- merge the four waves ---------------------------------------------------
