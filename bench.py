@@ -1,17 +1,29 @@
-"""Benchmark: TinyLlama-1.1B-shaped decode step with PoT-4 key caches.
+"""Benchmark: TinyLlama-1.1B-shaped decode steps over PoT key caches.
 
-One step = 22 layers, each: append the new token's key and value to that
-layer's cache (pot_encode_keys and pot_store_values, one row per (batch, kv
-head)) and run single-token decode attention over T keys
-(pot_decode_attention). 32 query heads, 4 kv
-heads, d = 64, fp16 values, synthetic seeded inputs resident in HBM before the
-timed region. Every layer has its own cache, so consecutive calls never hit
-the previous layer's data in the 256 MB last-level cache.
+Default (the headline JSON line): one step = 22 layers at B = 64, T = 32768,
+PoT-4 keys, fp16 values. Each layer:
+1. appends the new token's key and value to that layer's cache
+   (pot_encode_keys and pot_store_values, one row per (batch, kv head));
+2. runs single-token decode attention over T keys (pot_decode_attention).
 
-Prints one JSON line: keys scored per second (B * Hq * T * layers per step),
-the roofline of the decode kernel (algorithmic bytes per launch / mean launch
-time from HIP events on the launch stream), speed-up over the in-repo fp16
-and INT8 kernels, and the CPU oracle timed on host cores on a bounded sample.
+32 query heads, 4 kv heads, d = 64. Inputs are synthetic, seeded, and resident
+in HBM before the timed region. Every layer has its own cache, so consecutive
+calls never hit the previous layer's data in the 256 MB last-level cache.
+
+The line reports:
+- keys scored per second (B * Hq * T * layers per step);
+- the roofline of the decode call: algorithmic bytes per launch over the mean
+  launch time from HIP events on the launch stream, with median and best;
+- speed-up over the in-repo fp16 and INT8 kernels on the same shape;
+- the CPU oracle timed on host cores on a bounded sample, with one thread and
+  with all threads.
+
+--sweep prints one JSON line per point instead:
+- the 22-layer step for B in {1, 16, 64} x T in {1k, 4k, 16k, 32k}, PoT-4 and
+  PoT-M4;
+- the single-layer configurations (B = 1, T = 4096 PoT-4; B = 1, T = 32768
+  PoT-M1; B = 8, T = 32768 Hadamard + PoT-M4 with the fp16 and INT8
+  comparators on the same seeds).
 """
 from __future__ import annotations
 
@@ -25,9 +37,12 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HQ, HKV, D = 32, 4, 64
+G = HQ // HKV
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E peak
+LLC_BYTES = 256 << 20  # last-level (MALL) cache
 PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "decode_pot4_b64_t32768_traffic.txt")
-KERNEL_SRC = os.path.join(ROOT, "paper_2609_09208_amd", "csrc", "decode.hip")
+CSRC = os.path.join(ROOT, "paper_2609_09208_amd", "csrc")
+METRIC = "decode-attention keys scored/s and achieved HBM GB/s at T=32k (PoT-4)"
 
 
 def row_bytes(mant_bits: int) -> int:
@@ -35,15 +50,15 @@ def row_bytes(mant_bits: int) -> int:
     return 32 + 8 * mant_bits + 4 + 2 * D
 
 
-def algorithmic_bytes(B: int, T: int, mant_bits: int) -> int:
-    return B * HKV * T * row_bytes(mant_bits) + B * HQ * D * 4 * 2  # + q in, O out
+def algorithmic_bytes(B: int, T: int, per_row: int) -> int:
+    return B * HKV * T * per_row + B * HQ * D * 4 * 2  # + q in, O out
 
 
 def source_digest() -> str:
     import hashlib
     h = hashlib.sha256()
-    for name in sorted(os.listdir(os.path.dirname(KERNEL_SRC))):
-        with open(os.path.join(os.path.dirname(KERNEL_SRC), name), "rb") as f:
+    for name in sorted(os.listdir(CSRC)):
+        with open(os.path.join(CSRC, name), "rb") as f:
             h.update(name.encode() + f.read())
     return h.hexdigest()[:16]
 
@@ -55,7 +70,7 @@ def read_traffic():
         return None
     vals = {}
     for line in open(PROFILE_TRAFFIC):
-        if ":" in line:
+        if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             vals[k.strip()] = v.strip()
     if vals.get("source_digest") != source_digest():
@@ -66,32 +81,216 @@ def read_traffic():
         return None
 
 
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(T: int, budget_s: float) -> dict:
-    """The oracle (plain C, one thread) on (batch, kv-head) slices of the same
-    workload: append-encode one key row, then decode attention of the G = 8
-    query heads over T PoT-4 keys. Slices repeat until budget_s is spent."""
+    """The oracle (plain C) on (batch, kv-head) slices of the same workload:
+    append-encode one key row, then decode attention of the G = 8 query heads
+    over T PoT-4 keys. Half the budget runs one thread, half runs one slice per
+    thread on every available host thread (the oracle holds no shared state and
+    its ctypes calls release the interpreter lock)."""
+    from concurrent.futures import ThreadPoolExecutor
+
     import numpy as np
 
     import oracle
     from workloads import make_decode_inputs
 
-    G = HQ // HKV
     d = make_decode_inputs(1234, B=1, Hq=G, Hkv=1, T=T)
     rows = d["k_bits"].reshape(-1, D)
     se, cm, sc = oracle.encode_keys(rows)
-    n = 0
-    t0 = time.perf_counter()
-    while True:
+    zeros = np.zeros(G, np.int32)
+
+    def one_slice(_=None):
         oracle.encode_keys(rows[-1:])
-        oracle.pot_decode(d["q"], se, cm, sc, d["v_bits"], T, np.zeros(G, np.int32),
-                          1, G, 1, T)
-        n += 1
-        el = time.perf_counter() - t0
-        if el >= budget_s:
-            break
-    return {"value": n * G * T / el, "unit": "keys/s", "cores": 1, "kind": "oracle",
-            "sample": f"{n} (batch, kv-head) slices of T={T}: 1 appended key + "
-                      f"{G} query heads over {T} PoT-4 keys, {el:.1f} s, 1 thread"}
+        oracle.pot_decode(d["q"], se, cm, sc, d["v_bits"], T, zeros, 1, G, 1, T)
+
+    def run(threads: int, budget: float):
+        n, t0 = 0, time.perf_counter()
+        with ThreadPoolExecutor(max_workers=threads) as ex:
+            while True:
+                list(ex.map(one_slice, range(threads)))
+                n += threads
+                el = time.perf_counter() - t0
+                if el >= budget:
+                    return n, el
+
+    n1, e1 = run(1, budget_s / 2)
+    threads = max(1, min(16, os.cpu_count() or 1))
+    nt, et = run(threads, budget_s / 2)
+    return {"value": nt * G * T / et, "unit": "keys/s", "cores": threads, "kind": "oracle",
+            "value_1thread": n1 * G * T / e1,
+            "sample": f"(batch, kv-head) slices of T={T}: 1 appended key + {G} query heads over "
+                      f"{T} PoT-4 keys; {n1} slices in {e1:.1f} s on 1 thread, {nt} slices in "
+                      f"{et:.1f} s on {threads} threads; host CPU {cpu_model()}, "
+                      f"{os.cpu_count()} logical CPUs"}
+
+
+class Layers:
+    """Per-layer PoT caches (codes, scales, interleaved V) plus the appended
+    token of each layer, all resident on the device. With distinct=False the
+    layers hold copies of one drawn K/V (separate buffers, fresh queries)."""
+
+    def __init__(self, pa, B, T, L, mant_bits, hadamard, dev, distinct=True, keep_k16=0):
+        import numpy as np
+        import torch
+
+        from workloads import make_decode_inputs_device
+        self.pa, self.B, self.T, self.L, self.k = pa, B, T, L, mant_bits
+        self.fmt = pa.make_format(mant_bits=mant_bits, frac_bits=7, hadamard=hadamard)
+        self.layers = []
+        shared = None
+        for layer in range(L):
+            if distinct or shared is None:
+                d = make_decode_inputs_device(1000 + layer, B, HQ, HKV, T, dev)
+                if not distinct:
+                    shared = d
+            else:
+                d = dict(shared, q=torch.randn((B, HQ, D), device=dev))
+            cache = pa.alloc_pot_cache(B, HKV, T, mant_bits, dev)
+            pa.pot_encode_keys(self.fmt, d["k"], B * HKV * T, 1, 0, cache["key_scale"],
+                               cache["codes_se"], cache["codes_m"])
+            v = pa.alloc_value_cache(B, HKV, T, dev)
+            pa.pot_store_values(d["v"], B * HKV, T, T, 0, v)
+            rec = dict(q=d["q"], v=v, new_k=d["k"][:, :, T - 1].contiguous(),
+                       new_v=d["v"][:, :, T - 1].contiguous(), **cache)
+            if layer < keep_k16:
+                rec["k16"] = d["k"] if distinct else d["k"].clone()
+            self.layers.append(rec)
+            del d
+        del shared
+        self.heads = np.arange(HQ, dtype=np.int32) // G
+        self.out = torch.empty((B, HQ, D), dtype=torch.float32, device=dev)
+        self.ws = pa.alloc_workspace(pa.pot_decode_workspace_bytes(B, HQ, HKV, T), dev)
+
+    def decode(self, c):
+        self.pa.pot_decode_attention(self.fmt, c["q"], c["codes_se"], c["codes_m"],
+                                     c["key_scale"], c["v"], self.T, self.heads, self.B, HQ,
+                                     HKV, self.T, self.out, self.ws)
+
+    def step(self, events=None):
+        pa, T, B, k = self.pa, self.T, self.B, self.k
+        pos = T - 1
+        for i, c in enumerate(self.layers):
+            pa.pot_encode_keys(self.fmt, c["new_k"], B * HKV, T, 0,
+                               c["key_scale"].view(-1)[pos:],
+                               c["codes_se"].view(-1, 32)[pos:],
+                               c["codes_m"].view(-1, 8 * k)[pos:] if k else None)
+            pa.pot_store_values(c["new_v"], B * HKV, 1, T, pos, c["v"])
+            if events is not None:
+                events[i][0].record()
+            self.decode(c)
+            if events is not None:
+                events[i][1].record()
+
+
+def time_steps(lay, steps, warmup):
+    """Wall time of `steps` steps and the per-launch decode times (us) from
+    HIP events recorded on the launch stream."""
+    import numpy as np
+    import torch
+    for _ in range(warmup):
+        lay.step()
+    torch.cuda.synchronize()
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(lay.L)] for _ in range(steps)]
+    t0 = time.perf_counter()
+    for s in range(steps):
+        lay.step(ev[s])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    us = np.array([a.elapsed_time(b) for row in ev for (a, b) in row]) * 1e3
+    return elapsed, us
+
+
+def timed_calls(fn, n_layers, reps=10, warm=2):
+    """Mean microseconds per call of fn(layer) over reps passes of n_layers."""
+    import torch
+    for _ in range(warm):
+        for i in range(n_layers):
+            fn(i)
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(reps):
+        for i in range(n_layers):
+            fn(i)
+    e.record()
+    torch.cuda.synchronize()
+    return s.elapsed_time(e) / (reps * n_layers) * 1e3
+
+
+def comparators(pa, lay, dev):
+    """fp16 and INT8 kernels and the PoT kernel on the same caches, rotating
+    over the layers kept with their fp16 keys."""
+    import torch
+    cl = [c for c in lay.layers if "k16" in c]
+    B, T = lay.B, lay.T
+    n8 = B * HKV * T
+    i8 = [dict(codes=torch.empty((n8, D), dtype=torch.int8, device=dev),
+               sc=torch.empty(n8, dtype=torch.float32, device=dev)) for _ in cl]
+    had = int(lay.fmt.hadamard)
+    for c, x in zip(cl, i8):
+        pa.pot_int8_encode_keys(c["k16"], n8, 1, had, x["sc"], x["codes"])
+    out, ws, heads = lay.out, lay.ws, lay.heads
+    pot_us = timed_calls(lambda i: lay.decode(cl[i]), len(cl))
+    f16_us = timed_calls(lambda i: pa.pot_fp16_decode_attention(
+        cl[i]["q"], cl[i]["k16"], cl[i]["v"], T, heads, B, HQ, HKV, T, out, ws), len(cl))
+    i8_us = timed_calls(lambda i: pa.pot_int8_decode_attention(
+        cl[i]["q"], i8[i]["codes"], i8[i]["sc"], cl[i]["v"], T, heads, B, HQ, HKV, T, had,
+        out, ws), len(cl))
+
+    def frac(per_row, us):
+        return algorithmic_bytes(B, T, per_row) / (us * 1e-6) / 1e9 / HBM_PEAK_GBS
+
+    return {"pot_us_per_layer": pot_us, "fp16_us_per_layer": f16_us, "int8_us_per_layer": i8_us,
+            "speedup_vs_fp16": f16_us / pot_us, "speedup_vs_int8": i8_us / pot_us,
+            "pot_hbm_frac": frac(row_bytes(lay.k), pot_us), "fp16_hbm_frac": frac(256, f16_us),
+            "int8_hbm_frac": frac(196, i8_us), "layers_rotated": len(cl)}
+
+
+def fmt_name(k: int, had: bool) -> str:
+    return ("Hadamard + " if had else "") + ("PoT-4" if k == 0 else f"PoT-M{k}")
+
+
+def sweep(pa, dev, steps, warmup):
+    import numpy as np
+    import torch
+    pts = []
+    for B in (1, 16, 64):
+        for T in (1024, 4096, 16384, 32768):
+            for k in (0, 4):
+                pts.append(dict(B=B, T=T, k=k, had=False, L=22, compare=False))
+    pts += [dict(B=1, T=4096, k=0, had=False, L=4, compare=True),
+            dict(B=1, T=32768, k=1, had=False, L=4, compare=True),
+            dict(B=8, T=32768, k=4, had=True, L=4, compare=True),
+            dict(B=8, T=32768, k=0, had=False, L=4, compare=True)]
+    for p in pts:
+        lay = Layers(pa, p["B"], p["T"], p["L"], p["k"], p["had"], dev, distinct=False,
+                     keep_k16=4 if p["compare"] else 0)
+        elapsed, us = time_steps(lay, steps, warmup)
+        alg = algorithmic_bytes(p["B"], p["T"], row_bytes(p["k"]))
+        foot = p["L"] * alg
+        rec = {"B": p["B"], "T": p["T"], "format": fmt_name(p["k"], p["had"]), "layers": p["L"],
+               "keys_per_s_step": p["B"] * HQ * p["T"] * p["L"] * steps / elapsed,
+               "ms_per_step": elapsed / steps * 1e3,
+               "decode_us_mean": float(us.mean()), "decode_us_median": float(np.median(us)),
+               "decode_us_best": float(us.min()),
+               "hbm_frac_mean": alg / (us.mean() * 1e-6) / 1e9 / HBM_PEAK_GBS,
+               "step_footprint_bytes": foot, "cache_resident": foot < LLC_BYTES}
+        if p["compare"]:
+            rec["comparators"] = comparators(pa, lay, dev)
+        print(json.dumps(rec), flush=True)
+        del lay
+        torch.cuda.empty_cache()
 
 
 def main() -> int:
@@ -105,6 +304,8 @@ def main() -> int:
     ap.add_argument("--mant-bits", type=int, default=0)
     ap.add_argument("--cpu-budget", type=float, default=10.0)
     ap.add_argument("--no-compare", action="store_true")
+    ap.add_argument("--sweep", action="store_true",
+                    help="one JSON line per workload point instead of the headline line")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run device-to-device copies of BYTES bytes (calibrates "
                          "the FETCH_SIZE / WRITE_SIZE counters against a known size)")
@@ -119,7 +320,6 @@ def main() -> int:
     import torch
 
     import paper_2609_09208_amd as pa
-    from workloads import make_decode_inputs_device
 
     dev = "cuda:0"
     torch.cuda.set_device(0)
@@ -132,121 +332,41 @@ def main() -> int:
         torch.cuda.synchronize()
         print(json.dumps({"copy_probe_bytes": n, "copies": 3}), flush=True)
         return 0
+    if args.sweep:
+        sweep(pa, dev, max(2, min(args.steps, 5)), max(1, min(args.warmup, 2)))
+        return 0
+
     B, T, L, k = args.batch, args.seq, args.layers, args.mant_bits
-    G = HQ // HKV
-    fmt = pa.make_format(mant_bits=k, frac_bits=7)
-    layers = []
-    for layer in range(L):
-        d = make_decode_inputs_device(1000 + layer, B, HQ, HKV, T, dev)
-        cache = pa.alloc_pot_cache(B, HKV, T, k, dev)
-        pa.pot_encode_keys(fmt, d["k"], B * HKV * T, 1, 0, cache["key_scale"],
-                           cache["codes_se"], cache["codes_m"])
-        vcache = pa.alloc_value_cache(B, HKV, T, dev)
-        pa.pot_store_values(d["v"], B * HKV, T, T, 0, vcache)
-        new_k = d["k"][:, :, T - 1].contiguous()  # the appended token's key
-        new_v = d["v"][:, :, T - 1].contiguous()  # and value
-        keep_k16 = d["k"] if (not args.no_compare and layer < 4) else None
-        layers.append(dict(q=d["q"], v=vcache, new_k=new_k, new_v=new_v, k16=keep_k16,
-                           **cache))
-        del d
-    heads = np.arange(HQ, dtype=np.int32) // G
-    out = torch.empty((B, HQ, D), dtype=torch.float32, device=dev)
-    ws = pa.alloc_workspace(pa.pot_decode_workspace_bytes(B, HQ, HKV, T), dev)
+    lay = Layers(pa, B, T, L, k, False, dev, distinct=True,
+                 keep_k16=0 if args.no_compare else 4)
     torch.cuda.synchronize()
-
-    def step(events=None):
-        for i, c in enumerate(layers):
-            pos = T - 1
-            pa.pot_encode_keys(fmt, c["new_k"], B * HKV, T, 0, c["key_scale"].view(-1)[pos:],
-                               c["codes_se"].view(-1, 32)[pos:],
-                               c["codes_m"].view(-1, 8 * k)[pos:] if k else None)
-            pa.pot_store_values(c["new_v"], B * HKV, 1, T, pos, c["v"])
-            if events is not None:
-                events[i][0].record()
-            pa.pot_decode_attention(fmt, c["q"], c["codes_se"], c["codes_m"], c["key_scale"],
-                                    c["v"], T, heads, B, HQ, HKV, T, out, ws)
-            if events is not None:
-                events[i][1].record()
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(L)] for _ in range(args.steps)]
-    t0 = time.perf_counter()
-    for s in range(args.steps):
-        step(ev[s])
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    kern_ms = [a.elapsed_time(b) for row in ev for (a, b) in row]
-    kern_s = float(np.mean(kern_ms)) / 1e3
-    ms_step = elapsed / args.steps * 1e3
-    keys_per_step = B * HQ * T * L
-    value = keys_per_step * args.steps / elapsed
-    alg = algorithmic_bytes(B, T, k)
+    elapsed, us = time_steps(lay, args.steps, args.warmup)
+    kern_s = float(us.mean()) * 1e-6
+    alg = algorithmic_bytes(B, T, row_bytes(k))
     achieved = alg / kern_s / 1e9
-    traffic = read_traffic()
 
     result = {
-        "metric": "decode-attention keys scored/s and achieved HBM GB/s at T=32k (PoT-4)",
-        "value": value, "unit": "keys/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "int32+fp32",
-        "data": "synthetic",
+        "metric": METRIC,
+        "value": B * HQ * T * L * args.steps / elapsed, "unit": "keys/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": elapsed / args.steps * 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "int32+fp32", "data": "synthetic",
         "config": {"workload": f"TinyLlama-1.1B-shaped {L}-layer decode step, "
-                               f"PoT-{'4' if k == 0 else 'M%d' % k} keys (append + attend), "
+                               f"{fmt_name(k, False)} keys (append + attend), "
                                f"fp16 V, B={B}, T={T}, Hq={HQ}, Hkv={HKV}, d={D}",
                    "B": B, "T": T, "layers": L, "Hq": HQ, "Hkv": HKV, "head_dim": D,
                    "mant_bits": k, "frac_bits": 7, "parallelism": "none (1 GPU)"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": traffic,
-                     "kernel": "potattn::decode_kernel<PoT,G=8>",
+                     "traffic": read_traffic() if (B, T, k) == (64, 32768, 0) else None,
+                     "kernel": "potattn::decode_kernel<PoT,G=8> (+ query prep and combine)",
                      "alg_bytes_per_launch": alg, "launch_us": kern_s * 1e6,
+                     "launch_us_median": float(np.median(us)), "launch_us_best": float(us.min()),
+                     "launches_timed": int(us.size),
                      "keys_scored_per_s_kernel": B * HQ * T / kern_s},
     }
-
     if not args.no_compare:
-        # in-repo comparators on the same shape, rotating over 4 layer caches
-        comp = {}
-        cl = layers[:4]
-        n8 = B * HKV * T
-        i8 = [dict(codes=torch.empty((n8, D), dtype=torch.int8, device=dev),
-                   sc=torch.empty(n8, dtype=torch.float32, device=dev)) for _ in cl]
-        for c, x in zip(cl, i8):
-            pa.pot_int8_encode_keys(c["k16"], n8, 1, 0, x["sc"], x["codes"])
-
-        def timed(fn, reps=10):
-            for _ in range(2):
-                for c_i in range(len(cl)):
-                    fn(c_i)
-            torch.cuda.synchronize()
-            s_ev, e_ev = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            s_ev.record()
-            for _ in range(reps):
-                for c_i in range(len(cl)):
-                    fn(c_i)
-            e_ev.record()
-            torch.cuda.synchronize()
-            return s_ev.elapsed_time(e_ev) / (reps * len(cl)) * 1e3  # us
-
-        pot_us = timed(lambda i: pa.pot_decode_attention(
-            fmt, cl[i]["q"], cl[i]["codes_se"], cl[i]["codes_m"], cl[i]["key_scale"],
-            cl[i]["v"], T, heads, B, HQ, HKV, T, out, ws))
-        f16_us = timed(lambda i: pa.pot_fp16_decode_attention(
-            cl[i]["q"], cl[i]["k16"], cl[i]["v"], T, heads, B, HQ, HKV, T, out, ws))
-        i8_us = timed(lambda i: pa.pot_int8_decode_attention(
-            cl[i]["q"], i8[i]["codes"], i8[i]["sc"], cl[i]["v"], T, heads, B, HQ, HKV, T, 0,
-            out, ws))
-        comp = {"pot_us_per_layer": pot_us, "fp16_us_per_layer": f16_us,
-                "int8_us_per_layer": i8_us, "speedup_vs_fp16": f16_us / pot_us,
-                "speedup_vs_int8": i8_us / pot_us,
-                "fp16_hbm_frac": (B * HKV * T * 256 + B * HQ * D * 8) / (f16_us * 1e-6) / 1e9
-                / HBM_PEAK_GBS,
-                "int8_hbm_frac": (B * HKV * T * 196 + B * HQ * D * 8) / (i8_us * 1e-6) / 1e9
-                / HBM_PEAK_GBS}
-        result["comparators"] = comp
-
+        result["comparators"] = comparators(pa, lay, dev)
     if args.cpu_budget > 0:
         result["cpu_baseline"] = cpu_baseline(T, args.cpu_budget)
     print(json.dumps(result), flush=True)
