@@ -378,8 +378,6 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
   half8 ones;
 #pragma unroll
   for (int i = 0; i < 8; ++i) ones[i] = (_Float16)1.0f;
-  // byte addresses of lanes l ^ 16 and l ^ 32 for ds_bpermute
-  const int bp16 = (lane ^ 16) << 2, bp32 = (lane ^ 32) << 2;
   // -1 kept opaque so that p - hi stays one fma_mix reading hi as fp16
   float neg_one = -1.0f;
   asm("" : "+v"(neg_one));
@@ -597,11 +595,16 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
     mx = max_f32(mx, __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(
                                                    __builtin_bit_cast(int, mx), kDppRowRor8, 0xF,
                                                    0xF, true)));  // the other part
-    mx = max_f32(mx, __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(
-                                                   bp16, __builtin_bit_cast(int, mx))));
-    mx = max_f32(mx, __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(
-                                                   bp32, __builtin_bit_cast(int, mx))));
-    const int mt = hvalid ? (int)ceilf(mx) : INT_MIN;
+    // ceil is monotonic, so M = max over lanes of ceil(x): the reduction over
+    // the four rows of 16 lanes runs on int32 (swap odd with even rows, then
+    // the two halves; v_permlane*_swap, no LDS)
+    int mt = hvalid ? (int)ceilf(mx) : INT_MIN;
+    {
+      const auto r16 = __builtin_amdgcn_permlane16_swap((uint32_t)mt, (uint32_t)mt, false, false);
+      mt = max((int)r16[0], (int)r16[1]);
+      const auto r32 = __builtin_amdgcn_permlane32_swap((uint32_t)mt, (uint32_t)mt, false, false);
+      mt = max((int)r32[0], (int)r32[1]);
+    }
     m_new = max(m_run, mt);
   };
 
