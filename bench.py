@@ -247,6 +247,11 @@ def comparators(pa, lay, dev):
     i8_us = timed_calls(lambda i: pa.pot_int8_decode_attention(
         cl[i]["q"], i8[i]["codes"], i8[i]["sc"], cl[i]["v"], T, heads, B, HQ, HKV, T, had,
         out, ws), len(cl))
+    ds4a_us = None
+    if lay.k == 0:  # byte decode + v_dot4 on the same PoT-4 caches (a multiply path)
+        ds4a_us = timed_calls(lambda i: pa.pot_ds4a_decode_attention(
+            lay.fmt, cl[i]["q"], cl[i]["codes_se"], cl[i]["key_scale"], cl[i]["v"], T, heads,
+            B, HQ, HKV, T, out, ws), len(cl))
 
     def frac(per_row, us):
         return algorithmic_bytes(B, T, per_row) / (us * 1e-6) / 1e9 / HBM_PEAK_GBS
@@ -254,7 +259,12 @@ def comparators(pa, lay, dev):
     return {"pot_us_per_layer": pot_us, "fp16_us_per_layer": f16_us, "int8_us_per_layer": i8_us,
             "speedup_vs_fp16": f16_us / pot_us, "speedup_vs_int8": i8_us / pot_us,
             "pot_hbm_frac": frac(row_bytes(lay.k), pot_us), "fp16_hbm_frac": frac(256, f16_us),
-            "int8_hbm_frac": frac(196, i8_us), "layers_rotated": len(cl)}
+            "int8_hbm_frac": frac(196, i8_us), "layers_rotated": len(cl),
+            "ds4a_us_per_layer": ds4a_us,
+            "ds4a_hbm_frac": frac(row_bytes(0), ds4a_us) if ds4a_us else None,
+            "ds4a_speedup_vs_fp16": f16_us / ds4a_us if ds4a_us else None,
+            "ds4a_note": "PoT-4 codes decoded to int8 bytes by v_perm and scored by v_dot4 "
+                         "(software packed shift-dot, a multiply path)"}
 
 
 def fmt_name(k: int, had: bool) -> str:

@@ -93,7 +93,8 @@ typedef struct pot_format {
   int32_t hadamard;
 } pot_format;
 
-/* Optional debug taps of pot_decode_attention / pot_int8_decode_attention.
+/* Optional debug taps of pot_decode_attention, pot_ds4a_decode_attention and
+ * pot_int8_decode_attention.
  * Every pointer may be NULL (tap off). When any tap is non-NULL the call runs
  * an instrumented build of the same kernel source.
  *  qhat     int8  [B][Hq][d]  quantised (rotated) query q^ (eq. pot)
@@ -226,6 +227,24 @@ pot_status pot_int8_decode_attention(
     int32_t B, int32_t Hq, int32_t Hkv, int32_t T, int32_t hadamard,
     float* out, void* workspace, size_t ws_bytes, pot_debug* dbg,
     void* stream);
+
+/* Decode attention over a PoT-4 cache (mant_bits = 0) with the score computed
+ * by a software form of the packed shift-dot operation DS4A (Sec. III,
+ * eq. ds4a): each code nibble is decoded by a byte table (v_perm_b32) to the
+ * int8 value sigma 2^(6-e) (0 for the zero code, which must be stored with
+ * neg = 0 as pot_encode_keys writes it), and v_dot4_i32_i8 accumulates
+ * q^ * sigma 2^(6-e); one left shift by F - 6 gives exactly the int32 score
+ * of pot_decode_attention. This is a multiply path, provided to measure what
+ * a packed shift-dot would buy (eq. proj); pot_decode_attention is the
+ * shift-accumulate path. Arguments, layout, workspace, taps and errors as
+ * pot_decode_attention; fmt->mant_bits other than 0 -> POT_ERR_UNSUPPORTED. */
+pot_status pot_ds4a_decode_attention(const pot_format* fmt, const float* q,
+                                     const uint8_t* codes_se, const float* key_scale,
+                                     const uint16_t* v_cache, int64_t t_cap,
+                                     const int32_t* kv_head_of_q, int32_t B,
+                                     int32_t Hq, int32_t Hkv, int32_t T, float* out,
+                                     void* workspace, size_t ws_bytes,
+                                     pot_debug* dbg, void* stream);
 
 /* Decode attention on an unquantised fp16 cache (the FP16 baseline of
  * Sec. IV): q is rounded to fp16, scores accumulate in fp32.

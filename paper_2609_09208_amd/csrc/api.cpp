@@ -329,6 +329,31 @@ pot_status pot_decode_attention(const pot_format* fmt, const float* q, const uin
                        workspace, ws_bytes, dbg, stream);
 }
 
+pot_status pot_ds4a_decode_attention(const pot_format* fmt, const float* q,
+                                     const uint8_t* codes_se, const float* key_scale,
+                                     const uint16_t* v_cache, int64_t t_cap,
+                                     const int32_t* kv_head_of_q, int32_t B, int32_t Hq,
+                                     int32_t Hkv, int32_t T, float* out, void* workspace,
+                                     size_t ws_bytes, pot_debug* dbg, void* stream) {
+  pot_status st = check_format(fmt);
+  if (st != POT_OK) return st;
+  if (fmt->mant_bits != 0)
+    return fail(POT_ERR_UNSUPPORTED, "the byte-decode path scores PoT-4 codes only (mant_bits 0)");
+  if (!codes_se || !key_scale) return fail(POT_ERR_INVALID_ARG, "codes_se or key_scale is NULL");
+  if (!aligned(codes_se, 16) || !aligned(key_scale, 4))
+    return fail(POT_ERR_INVALID_ARG, "misaligned codes_se / key_scale");
+  DecodeArgs a{};
+  a.q = q;
+  a.codes_se = codes_se;
+  a.key_scale = key_scale;
+  a.v = v_cache;
+  a.out = out;
+  a.frac_bits = fmt->frac_bits;
+  a.hadamard = fmt->hadamard;
+  return decode_common(kScoreDs4a, 0, a, kv_head_of_q, B, Hq, Hkv, T, t_cap, workspace, ws_bytes,
+                       dbg, stream);
+}
+
 pot_status pot_int8_encode_keys(const uint16_t* k_fp16, int64_t n_rows, int64_t out_row_stride,
                                 int32_t hadamard, float* key_scale, int8_t* codes, void* stream) {
   if (n_rows < 0) return fail(POT_ERR_INVALID_ARG, "n_rows %lld < 0", (long long)n_rows);

@@ -185,6 +185,11 @@ struct KeyRegs<kScorePot, K> {
   float s;
 };
 template <int K>
+struct KeyRegs<kScoreDs4a, K> {
+  uint4 c0, c1;
+  float s;
+};
+template <int K>
 struct KeyRegs<kScoreInt8, K> {
   int4 k[4];
   float s;
@@ -211,6 +216,11 @@ __device__ __forceinline__ void load_keys(const DecodeArgs& a, int64_t row, KeyR
 #pragma unroll
     for (int bb = 0; bb < K; ++bb)
       r.pl[bb] = reinterpret_cast<const uint2*>(a.codes_m + row * 8 * K)[bb];
+    r.s = a.key_scale[row];
+  } else if constexpr (MODE == kScoreDs4a) {
+    const uint4* cp = reinterpret_cast<const uint4*>(a.codes_se + row * (kDim / 2));
+    r.c0 = cp[0];
+    r.c1 = cp[1];
     r.s = a.key_scale[row];
   } else if constexpr (MODE == kScoreInt8) {
     const int4* kp = reinterpret_cast<const int4*>(a.codes_i8 + row * kDim);
@@ -261,13 +271,14 @@ __device__ __forceinline__ void mask_values(int t0, int t_end, int lane, ValRegs
 // ---- prepared query operands (workspace, one block per kv head) -------------
 // PoT-4 with G >= 2: [m][pair] words 2 (q_{2p} + 2^16 q_{2p+1}); other PoT forms:
 // [(b' * 64 + m) * G + h] = q << b'; INT8: [i * G + h] four int8 per word;
+// byte decode: [(2c + o) * G + h] four int8 (elements 8c + o + 2t, t = 0..3);
 // fp16: [i * G + h] two fp16 per word. The G per-head score factors follow.
 template <int MODE, int G, int K>
 struct QLayout {
   static constexpr bool kPacked = MODE == kScorePot && K == 0 && G >= 2;
   static constexpr int NP = G / 2;
   static constexpr int kWords = MODE == kScorePot ? (kPacked ? kDim * NP : (K + 1) * kDim * G)
-                                : MODE == kScoreInt8 ? (kDim / 4) * G
+                                : (MODE == kScoreInt8 || MODE == kScoreDs4a) ? (kDim / 4) * G
                                                      : (kDim / 2) * G;
 };
 
@@ -300,6 +311,16 @@ __global__ __launch_bounds__(kBlock) void prep_queries_kernel(const DecodeArgs a
         if (lane == 0)
           cb[h] = __fmul_rn(__fmul_rn(step, log2e_f32()),
                             __builtin_amdgcn_ldexpf(1.0f, -(a.frac_bits + K + 3)));
+      } else if constexpr (MODE == kScoreDs4a) {
+        // the word of code word c and parity o holds elements 8c + o + 2t in
+        // byte t: lanes differing in bits 1 and 2 fill one word
+        uint32_t word = (uint32_t)(qi & 0xFF) << (8 * ((lane >> 1) & 3));
+        word |= __shfl_xor(word, 2, 64);
+        word |= __shfl_xor(word, 4, 64);
+        if ((lane & 6) == 0) qb[(2 * (lane >> 3) + (lane & 1)) * G + h] = (int32_t)word;
+        if (lane == 0)
+          cb[h] = __fmul_rn(__fmul_rn(step, log2e_f32()),
+                            __builtin_amdgcn_ldexpf(1.0f, -(a.frac_bits + 3)));
       } else {
         uint32_t word = (uint32_t)(qi & 0xFF) << (8 * (lane & 3));
         word |= __shfl_xor(word, 1, 64);
@@ -509,6 +530,43 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
 #pragma unroll
       for (int h = 0; h < G; ++h) {
         const int32_t v = accv[h];
+        xs[h] = __fmul_rn(__fmul_rn((float)v, ks.s), cb[h]);
+        if constexpr (DEBUG) {
+          if (a.dbg_scores && kvalid)
+            a.dbg_scores[((int64_t)b * a.Hq + a.q_of_kv[kvh * G + h]) * a.T + t] = v;
+        }
+      }
+    } else if constexpr (MODE == kScoreDs4a) {
+      // Byte decode of the PoT-4 codes (the DS4A operation, eq. ds4a, in
+      // software): a v_perm_b32 table maps each exponent field to 2^(6 - e)
+      // (0 for the zero code), the sign is applied per byte as (m ^ N) + n
+      // with N = 0xff and n = 1 in the bytes of negative elements (no carry
+      // between bytes: m <= 64, and the zero code is never negative), and
+      // v_dot4_i32_i8 accumulates q * sigma 2^(6 - e): the exact score at
+      // head-room 6, which one left shift brings to F. A multiply path.
+      const uint32_t w[8] = {ks.c0.x, ks.c0.y, ks.c0.z, ks.c0.w,
+                             ks.c1.x, ks.c1.y, ks.c1.z, ks.c1.w};
+      int32_t accd[G];
+#pragma unroll
+      for (int h = 0; h < G; ++h) accd[h] = 0;
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        const uint32_t wc = w[c];
+        const uint32_t e0 = wc & 0x07070707u, e1 = (wc >> 4) & 0x07070707u;
+        const uint32_t m0 = __builtin_amdgcn_perm(0x00010204u, 0x08102040u, e0);
+        const uint32_t m1 = __builtin_amdgcn_perm(0x00010204u, 0x08102040u, e1);
+        const uint32_t n0 = (wc >> 3) & 0x01010101u, n1 = (wc >> 7) & 0x01010101u;
+        const uint32_t k0 = xad_u32(m0, (n0 << 8) - n0, n0);
+        const uint32_t k1 = xad_u32(m1, (n1 << 8) - n1, n1);
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+          accd[h] = __builtin_amdgcn_sdot4(qb[(2 * c) * G + h], (int32_t)k0, accd[h], false);
+          accd[h] = __builtin_amdgcn_sdot4(qb[(2 * c + 1) * G + h], (int32_t)k1, accd[h], false);
+        }
+      }
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        const int32_t v = (int32_t)((uint32_t)accd[h] << (a.frac_bits - 6));
         xs[h] = __fmul_rn(__fmul_rn((float)v, ks.s), cb[h]);
         if constexpr (DEBUG) {
           if (a.dbg_scores && kvalid)
@@ -795,6 +853,7 @@ int decode_occupancy(int mode, int G, int mant_bits) {
   auto by_k = [&](auto g_tag) -> int {
     constexpr int GG = decltype(g_tag)::value;
     if (mode == kScoreInt8) return occupancy_t<kScoreInt8, GG, 0>();
+    if (mode == kScoreDs4a) return occupancy_t<kScoreDs4a, GG, 0>();
     if (mode == kScoreFp16) return occupancy_t<kScoreFp16, GG, 0>();
     switch (mant_bits) {
       case 0: return occupancy_t<kScorePot, GG, 0>();
@@ -848,6 +907,9 @@ hipError_t launch_decode(int mode, int G, int mant_bits, bool debug, const Decod
     case kScoreInt8:
       return debug ? launch_g<kScoreInt8, true>(G, 0, a, stream)
                    : launch_g<kScoreInt8, false>(G, 0, a, stream);
+    case kScoreDs4a:
+      return debug ? launch_g<kScoreDs4a, true>(G, 0, a, stream)
+                   : launch_g<kScoreDs4a, false>(G, 0, a, stream);
     case kScoreFp16:
       return launch_g<kScoreFp16, false>(G, 0, a, stream);
     default:

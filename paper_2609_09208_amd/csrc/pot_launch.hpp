@@ -37,7 +37,9 @@ hipError_t launch_store_values(const uint16_t* src, int64_t n_seq, int64_t n_tok
 
 hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream);
 
-enum ScoreMode : int { kScorePot = 0, kScoreInt8 = 1, kScoreFp16 = 2 };
+// kScoreDs4a: PoT-4 codes decoded to int8 bytes and scored by v_dot4 (a
+// multiply path, kept beside the shift path for measurement)
+enum ScoreMode : int { kScorePot = 0, kScoreInt8 = 1, kScoreFp16 = 2, kScoreDs4a = 3 };
 
 // Everything one decode launch needs. Passed by value as the kernel argument.
 struct DecodeArgs {

@@ -48,9 +48,11 @@ def gpu_encode(k_bits, mant_bits=0, hadamard=False, key_scale=None, frac_bits=7)
 
 
 def gpu_pot_decode(d, codes_se, codes_m, key_scale, mant_bits=0, frac_bits=7,
-                   hadamard=False, taps=True, force_splits=0):
+                   hadamard=False, taps=True, force_splits=0, engine="sac"):
     """d: workloads.make_decode_inputs dict; cache arrays are host numpy in the
-    row layout. Returns dict of numpy results (taps when requested)."""
+    row layout. engine "sac" runs pot_decode_attention (shift-accumulate),
+    "ds4a" pot_ds4a_decode_attention (byte decode + v_dot4). Returns dict of
+    numpy results (taps when requested)."""
     B, Hq, Hkv, T, t_cap = d["B"], d["Hq"], d["Hkv"], d["T"], d["t_cap"]
     fmt = pa.make_format(mant_bits, frac_bits, hadamard)
     q = to_dev(d["q"])
@@ -75,8 +77,13 @@ def gpu_pot_decode(d, codes_se, codes_m, key_scale, mant_bits=0, frac_bits=7,
                     m_split=torch.empty((B, Hq, max_s), dtype=torch.int32, device=DEV))
         for k_, t_ in bufs.items():
             setattr(dbg, k_, t_.data_ptr())
-    pa.pot_decode_attention(fmt, q, se, cm, sc, v, t_cap, d["kv_head_of_q"], B,
-                            Hq, Hkv, T, out, ws, dbg=dbg)
+    if engine == "sac":
+        pa.pot_decode_attention(fmt, q, se, cm, sc, v, t_cap, d["kv_head_of_q"], B,
+                                Hq, Hkv, T, out, ws, dbg=dbg)
+    else:
+        assert engine == "ds4a" and cm is None
+        pa.pot_ds4a_decode_attention(fmt, q, se, sc, v, t_cap, d["kv_head_of_q"], B,
+                                     Hq, Hkv, T, out, ws, dbg=dbg)
     torch.cuda.synchronize()
     res["out"] = out.cpu().numpy()
     res["n_splits"], res["split_len"] = dbg.n_splits, dbg.split_len
@@ -102,7 +109,7 @@ def oracle_pot(d, mant_bits=0, frac_bits=7, hadamard=False, split_len=None,
 
 
 def assert_pot_parity(d, mant_bits=0, frac_bits=7, hadamard=False, force_splits=0,
-                      key_scale=None, taps=True):
+                      key_scale=None, taps=True, engine="sac"):
     """Full parity: codes, scales, q^, Delta, scores, M (final and per split)
     bit-exact; O within O_TOL. Returns the max-abs O error."""
     rows = d["k_bits"].reshape(-1, 64)
@@ -114,7 +121,7 @@ def assert_pot_parity(d, mant_bits=0, frac_bits=7, hadamard=False, force_splits=
         assert np.array_equal(g_cm, o_cm), "codes_m differ"
     assert np.array_equal(g_sc.view(np.uint32), o_sc.view(np.uint32)), "key_scale differ"
     g = gpu_pot_decode(d, g_se, g_cm, g_sc, mant_bits, frac_bits, hadamard,
-                       taps=taps, force_splits=force_splits)
+                       taps=taps, force_splits=force_splits, engine=engine)
     _, _, _, o = oracle_pot(d, mant_bits, frac_bits, hadamard,
                             split_len=g["split_len"], key_scale=key_scale)
     if taps:

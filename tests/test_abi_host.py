@@ -169,3 +169,15 @@ def test_store_values_rejects_bad_arguments():
 
 def test_decode_needs_t_cap_multiple_of_8():
     assert _decode(t_cap=4100) == pa.POT_ERR_INVALID_ARG
+
+
+def test_ds4a_rejects_bad_arguments():
+    hm = (np.arange(32, dtype=np.int32) // 8)
+    hp = hm.ctypes.data_as(ctypes.c_void_p)
+    D = pa._lib.pot_ds4a_decode_attention
+    args = lambda fmt, se=FAKE: (ctypes.byref(fmt), FAKE, se, FAKE, FAKE, 4096, hp, 1, 32, 4,
+                                 4096, FAKE, FAKE, 1 << 30, None, None)
+    assert D(*args(pa.make_format(mant_bits=1))) == pa.POT_ERR_UNSUPPORTED
+    assert D(*args(pa.make_format(frac_bits=5))) == pa.POT_ERR_INVALID_ARG
+    assert D(*args(pa.make_format(), se=None)) == pa.POT_ERR_INVALID_ARG
+    assert D(*args(pa.make_format(), se=FAKE + 4)) == pa.POT_ERR_INVALID_ARG
