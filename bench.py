@@ -41,6 +41,7 @@ G = HQ // HKV
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E peak
 LLC_BYTES = 256 << 20  # last-level (MALL) cache
 PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "decode_pot4_b64_t32768_traffic.txt")
+PROFILE_READ_CEILING = os.path.join(ROOT, "profiles", "stream_read_ceiling.md")
 CSRC = os.path.join(ROOT, "paper_2609_09208_amd", "csrc")
 METRIC = "decode-attention keys scored/s and achieved HBM GB/s at T=32k (PoT-4)"
 
@@ -79,6 +80,18 @@ def read_traffic():
         return float(vals["hbm_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
+
+
+def read_ceiling():
+    """Best measured stream-read bandwidth (GB/s) of this device model, from the
+    committed probe summary; None if absent."""
+    try:
+        for line in open(PROFILE_READ_CEILING):
+            if line.startswith("read_ceiling_gbs:"):
+                return float(line.split(":", 1)[1])
+    except (OSError, ValueError):
+        pass
+    return None
 
 
 def cpu_model() -> str:
@@ -373,6 +386,8 @@ def main() -> int:
                      "alg_bytes_per_launch": alg, "launch_us": kern_s * 1e6,
                      "launch_us_median": float(np.median(us)), "launch_us_best": float(us.min()),
                      "launches_timed": int(us.size),
+                     "read_ceiling_gbs": read_ceiling(),
+                     "frac_of_read_ceiling": achieved / read_ceiling() if read_ceiling() else None,
                      "keys_scored_per_s_kernel": B * HQ * T / kern_s},
     }
     if not args.no_compare:

@@ -506,7 +506,10 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
 #pragma unroll
           for (int bb = 0; bb < K; ++bb) {
             const uint32_t plw = (m < 32) ? ks.pl[bb].x : ks.pl[bb].y;
-            shb[bb] = sh & (uint32_t)((int32_t)(plw << (31 - (m & 31))) >> 31);
+            const uint32_t msk = (uint32_t)((int32_t)(plw << (31 - (m & 31))) >> 31);
+            // once per element: left to itself the compiler moves this mask
+            // behind the shift and repeats it for every head
+            asm("v_and_b32 %0, %1, %2" : "=v"(shb[bb]) : "v"(sh), "v"(msk));
           }
 #pragma unroll
           for (int h = 0; h < G; ++h) {
