@@ -150,7 +150,7 @@ __device__ __forceinline__ float max_f32(float a, float b) {
 
 template <int JJ>
 __device__ __forceinline__ void pot_step8(uint32_t s0, uint32_t s1, uint32_t g0, uint32_t g1,
-                                          const int32_t* __restrict__ qm, uint32_t (&A)[4],
+                                          const uint32_t* qm, uint32_t (&A)[4],
                                           uint32_t (&B)[4]) {
   uint32_t p0, p1, p2, p3, t;
 #define POT_STEP8_OPERANDS                                                                   \
@@ -454,6 +454,9 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
         uint32_t accA[NP], accB[NP];
 #pragma unroll
         for (int p = 0; p < NP; ++p) accA[p] = accB[p] = 0u;
+        // G = 8: the 32 operand words of one code word's 8 elements, read as
+        // one group so that a tile waits on the scalar cache 8 times, not 32
+        uint32_t qq[32];
         // one 2-element step: byte JJ of the shift words holds the shifts of
         // elements 8i + 2JJ (s0) and 8i + 2JJ + 1 (s1)
         auto step = [&](auto jj_tag, int i, uint32_t wi, uint32_t s0, uint32_t s1) {
@@ -462,7 +465,7 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
           const uint32_t sg0 = (uint32_t)((int32_t)(wi << (28 - 8 * JJ)) >> 31);
           const uint32_t sg1 = (uint32_t)((int32_t)(wi << (24 - 8 * JJ)) >> 31);
           if constexpr (NP == 4) {
-            pot_step8<JJ>(s0, s1, sg0, sg1, qb + m * NP, accA, accB);
+            pot_step8<JJ>(s0, s1, sg0, sg1, qq + 8 * JJ, accA, accB);
             return;
           }
           uint32_t P[NP];
@@ -482,6 +485,10 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
         for (int i = 0; i < 8; ++i) {
           const uint32_t s0 = 0x26262626u - (w[i] & 0x07070707u);
           const uint32_t s1 = 0x26262626u - ((w[i] >> 4) & 0x07070707u);
+          if constexpr (NP == 4) {
+#pragma unroll
+            for (int k = 0; k < 32; ++k) qq[k] = (uint32_t)qb[32 * i + k];
+          }
           step(std::integral_constant<int, 0>{}, i, w[i], s0, s1);
           step(std::integral_constant<int, 1>{}, i, w[i], s0, s1);
           step(std::integral_constant<int, 2>{}, i, w[i], s0, s1);
