@@ -40,6 +40,7 @@ HQ, HKV, D = 32, 4, 64
 G = HQ // HKV
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E peak
 LLC_BYTES = 256 << 20  # last-level (MALL) cache
+COMPARE_ROUNDS = 3  # interleaved timing rounds per comparator engine
 PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "decode_pot4_b64_t32768_traffic.txt")
 PROFILE_READ_CEILING = os.path.join(ROOT, "profiles", "stream_read_ceiling.md")
 CSRC = os.path.join(ROOT, "paper_2609_09208_amd", "csrc")
@@ -254,17 +255,25 @@ def comparators(pa, lay, dev):
     for c, x in zip(cl, i8):
         pa.pot_int8_encode_keys(c["k16"], n8, 1, had, x["sc"], x["codes"])
     out, ws, heads = lay.out, lay.ws, lay.heads
-    pot_us = timed_calls(lambda i: lay.decode(cl[i]), len(cl))
-    f16_us = timed_calls(lambda i: pa.pot_fp16_decode_attention(
-        cl[i]["q"], cl[i]["k16"], cl[i]["v"], T, heads, B, HQ, HKV, T, out, ws), len(cl))
-    i8_us = timed_calls(lambda i: pa.pot_int8_decode_attention(
-        cl[i]["q"], i8[i]["codes"], i8[i]["sc"], cl[i]["v"], T, heads, B, HQ, HKV, T, had,
-        out, ws), len(cl))
-    ds4a_us = None
+    engines = {
+        "pot": lambda i: lay.decode(cl[i]),
+        "fp16": lambda i: pa.pot_fp16_decode_attention(
+            cl[i]["q"], cl[i]["k16"], cl[i]["v"], T, heads, B, HQ, HKV, T, out, ws),
+        "int8": lambda i: pa.pot_int8_decode_attention(
+            cl[i]["q"], i8[i]["codes"], i8[i]["sc"], cl[i]["v"], T, heads, B, HQ, HKV, T, had,
+            out, ws),
+    }
     if lay.k == 0:  # byte decode + v_dot4 on the same PoT-4 caches (a multiply path)
-        ds4a_us = timed_calls(lambda i: pa.pot_ds4a_decode_attention(
+        engines["ds4a"] = lambda i: pa.pot_ds4a_decode_attention(
             lay.fmt, cl[i]["q"], cl[i]["codes_se"], cl[i]["key_scale"], cl[i]["v"], T, heads,
-            B, HQ, HKV, T, out, ws), len(cl))
+            B, HQ, HKV, T, out, ws)
+    # interleaved rounds, each engine warmed before it is timed; median per engine
+    runs = {name: [] for name in engines}
+    for _ in range(COMPARE_ROUNDS):
+        for name, fn in engines.items():
+            runs[name].append(timed_calls(fn, len(cl), reps=10, warm=4))
+    med = {name: float(sorted(v)[len(v) // 2]) for name, v in runs.items()}
+    pot_us, f16_us, i8_us, ds4a_us = med["pot"], med["fp16"], med["int8"], med.get("ds4a")
 
     def frac(per_row, us):
         return algorithmic_bytes(B, T, per_row) / (us * 1e-6) / 1e9 / HBM_PEAK_GBS
@@ -277,7 +286,9 @@ def comparators(pa, lay, dev):
             "ds4a_hbm_frac": frac(row_bytes(0), ds4a_us) if ds4a_us else None,
             "ds4a_speedup_vs_fp16": f16_us / ds4a_us if ds4a_us else None,
             "ds4a_note": "PoT-4 codes decoded to int8 bytes by v_perm and scored by v_dot4 "
-                         "(software packed shift-dot, a multiply path)"}
+                         "(software packed shift-dot, a multiply path)",
+            "timing": f"median of {COMPARE_ROUNDS} interleaved rounds of 10 passes over the "
+                      f"{len(cl)} layers per engine"}
 
 
 def fmt_name(k: int, had: bool) -> str:
