@@ -1,10 +1,10 @@
 """Benchmark: TinyLlama-1.1B-shaped decode steps over PoT key caches.
 
 Default (the headline JSON line): one step = 22 layers at B = 64, T = 32768,
-PoT-4 keys, fp16 values. Each layer:
-1. appends the new token's key and value to that layer's cache
-   (pot_encode_keys and pot_store_values, one row per (batch, kv head));
-2. runs single-token decode attention over T keys (pot_decode_attention).
+PoT-4 keys, fp16 values. Each layer makes one call,
+pot_append_decode_attention, which appends the new token's key (encoded to
+PoT codes) and values at position T - 1 of every (batch, kv head) sequence of
+that layer's cache and runs single-token decode attention over the T keys.
 
 32 query heads, 4 kv heads, d = 64. Inputs are synthetic, seeded, and resident
 in HBM before the timed region. Every layer has its own cache, so consecutive
@@ -191,17 +191,13 @@ class Layers:
                                      HKV, self.T, self.out, self.ws)
 
     def step(self, events=None):
-        pa, T, B, k = self.pa, self.T, self.B, self.k
-        pos = T - 1
+        pa, T, B = self.pa, self.T, self.B
         for i, c in enumerate(self.layers):
-            pa.pot_encode_keys(self.fmt, c["new_k"], B * HKV, T, 0,
-                               c["key_scale"].view(-1)[pos:],
-                               c["codes_se"].view(-1, 32)[pos:],
-                               c["codes_m"].view(-1, 8 * k)[pos:] if k else None)
-            pa.pot_store_values(c["new_v"], B * HKV, 1, T, pos, c["v"])
             if events is not None:
                 events[i][0].record()
-            self.decode(c)
+            pa.pot_append_decode_attention(self.fmt, c["q"], c["new_k"], c["new_v"],
+                                           c["codes_se"], c["codes_m"], c["key_scale"], c["v"],
+                                           T, self.heads, B, HQ, HKV, T, self.out, self.ws)
             if events is not None:
                 events[i][1].record()
 
@@ -393,7 +389,7 @@ def main() -> int:
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": read_traffic() if (B, T, k) == (64, 32768, 0) else None,
-                     "kernel": "potattn::decode_kernel<PoT,G=8> (+ query prep and combine)",
+                     "kernel": "potattn::decode_kernel<PoT,G=8> (+ query prep with the fused append, and combine)",
                      "alg_bytes_per_launch": alg, "launch_us": kern_s * 1e6,
                      "launch_us_median": float(np.median(us)), "launch_us_best": float(us.min()),
                      "launches_timed": int(us.size),

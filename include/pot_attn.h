@@ -210,6 +210,32 @@ pot_status pot_decode_attention(const pot_format* fmt, const float* q,
                                 void* workspace, size_t ws_bytes,
                                 pot_debug* dbg, void* stream);
 
+/* One decode step on a cache that holds only codes (Sec. II-F, Sec. V-F): the
+ * new token of every (b, kv-head) sequence is appended at position T - 1 and
+ * attention then runs over positions 0 .. T-1, in one call. Equivalent to
+ * pot_encode_keys(fmt, k_new, B*Hkv, t_cap, 0, ...) on the rows at T - 1,
+ * pot_store_values(v_new, B*Hkv, 1, t_cap, T - 1, v_cache) and
+ * pot_decode_attention(...) over T keys, with bit-identical cache contents and
+ * output, but without the two extra launches: the query-preparation kernel
+ * writes the new rows before the decode kernel starts.
+ *  k_new, v_new [B][Hkv][d] fp16, dense, device, 16-byte aligned: the new
+ *               token's key (encoded with the row absmax scale, rotated first
+ *               when fmt->hadamard) and values.
+ *  codes_se, codes_m, key_scale, v_cache: the cache as for
+ *               pot_decode_attention, written at row T - 1 of each sequence
+ *               (nothing else is written).
+ *  Other arguments, the workspace, debug taps (the scores include the new
+ *  key) and errors as pot_decode_attention; NULL or misaligned k_new / v_new
+ *  -> INVALID_ARG. Inputs q, k_new and v_new may not alias the cache. */
+pot_status pot_append_decode_attention(const pot_format* fmt, const float* q,
+                                       const uint16_t* k_new, const uint16_t* v_new,
+                                       uint8_t* codes_se, uint8_t* codes_m,
+                                       float* key_scale, uint16_t* v_cache,
+                                       int64_t t_cap, const int32_t* kv_head_of_q,
+                                       int32_t B, int32_t Hq, int32_t Hkv, int32_t T,
+                                       float* out, void* workspace, size_t ws_bytes,
+                                       pot_debug* dbg, void* stream);
+
 /* ---- comparison paths on the same cache skeleton --------------------- */
 
 /* INT8 uniform key codes (the multiply-accumulate comparator of Sec. III and

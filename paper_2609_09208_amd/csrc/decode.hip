@@ -284,7 +284,8 @@ struct QLayout {
 
 // Rotates (optionally) and quantises the G query vectors of one (batch, kv
 // head) and writes the operand words the decode kernel reads through the
-// scalar cache. Grid (Hkv, B), 4 waves; wave w handles heads w, w + 4.
+// scalar cache. Grid (Hkv, B), 4 waves; wave w handles heads w, w + 4. With a
+// fused append it first writes the sequence's new cache row.
 template <int MODE, int G, int K, bool DEBUG>
 __global__ __launch_bounds__(kBlock) void prep_queries_kernel(const DecodeArgs a) {
   using QL = QLayout<MODE, G, K>;
@@ -294,6 +295,20 @@ __global__ __launch_bounds__(kBlock) void prep_queries_kernel(const DecodeArgs a
   const int64_t seq = (int64_t)b * a.Hkv + kvh;
   int32_t* qb = a.qbuf + seq * a.qstride;
   float* cb = reinterpret_cast<float*>(qb + QL::kWords);
+  if constexpr (MODE == kScorePot) {
+    // fused append of this sequence's new token at row T - 1: wave 0 encodes
+    // the key (row absmax scale), wave 1 stores the values
+    if (a.app_k != nullptr) {
+      const int64_t row = seq * a.t_cap + (a.T - 1);
+      if (wave == 0)
+        encode_key_row_wave(reinterpret_cast<const __half*>(a.app_k) + seq * kDim, a.hadamard, 0,
+                            a.app_key_scale + row, a.app_codes_se + row * (kDim / 2),
+                            a.app_codes_m + row * 8 * K, a.app_tab);
+      else if (wave == 1)
+        store_value_token_wave(a.app_v + seq * kDim, a.app_v_cache + seq * a.t_cap * kDim,
+                               a.T - 1);
+    }
+  }
   for (int h = wave; h < G; h += kWaves) {
     const int64_t bq = (int64_t)b * a.Hq + a.q_of_kv[kvh * G + h];
     float qv = a.q[bq * kDim + lane];

@@ -43,70 +43,15 @@ EncodeTables make_encode_tables(int mant_bits) {
   return t;
 }
 
-// Log-nearest PoT-Mk code of one element. Returns the nibble (neg<<3 | e, or
-// 7 for zero) and the mantissa j.
-__device__ __forceinline__ int classify(float x, float s, const EncodeTables& tab, int* j_out) {
-  *j_out = 0;
-  if (!(s > 0.0f) || x == 0.0f || x != x) return kZeroField;
-  const float u = fabsf(x) / s;  // one correctly rounded division
-  if (!(u > tab.zero_cut)) return kZeroField;
-  const int n = 1 << tab.mant_bits;
-  const uint32_t ub = __float_as_uint(u);
-  const int e2 = (int)((ub >> 23) & 0xFF) - 127;         // u > 2^-7: normal
-  const float m = __uint_as_float((ub & 0x007FFFFFu) | 0x3F800000u);  // [1, 2)
-  int c = 0;
-#pragma unroll
-  for (int i = 0; i < 16; ++i) c += (i < n && m > tab.cut[i]) ? 1 : 0;
-  int e, j;
-  if (e2 >= 0) {  // u >= 1: the top binade, saturating at its largest value
-    e = 0;
-    j = (e2 > 0) ? n - 1 : min(c, n - 1);
-  } else if (c == n) {  // rounds up to the next binade's first value
-    e = -e2 - 1;
-    j = 0;
-  } else {
-    e = -e2;
-    j = c;
-  }
-  if (e > kExpMax) {  // between the zero cut and 2^-E: the smallest magnitude
-    e = kExpMax;
-    j = 0;
-  }
-  *j_out = j;
-  return ((x < 0.0f) ? 8 : 0) | e;
-}
-
 __global__ __launch_bounds__(kBlock) void encode_pot_kernel(
     const __half* __restrict__ k, int64_t n_rows, int64_t out_stride, int scale_mode,
     int hadamard, float* __restrict__ key_scale, uint8_t* __restrict__ codes_se,
     uint8_t* __restrict__ codes_m, EncodeTables tab) {
-  const int lane = lane_id();
   const int64_t row = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
   if (row >= n_rows) return;  // uniform per wave
-  float x = __half2float(k[row * kDim + lane]);
-  if (hadamard) x = (float)(wave_fwht64((double)x) * 0.125);
   const int64_t orow = row * out_stride;
-  float s;
-  if (scale_mode == 0) {
-    s = wave_max(fabsf(x));
-    if (lane == 0) key_scale[orow] = s;
-  } else {
-    s = key_scale[orow];
-  }
-  int j;
-  const int nib = classify(x, s, tab, &j);
-  // sign/exponent nibbles: element m at bit 4*(m%8) of dword m/8
-  uint32_t w = (uint32_t)nib << (4 * (lane & 7));
-  w |= __shfl_xor(w, 1, 64);
-  w |= __shfl_xor(w, 2, 64);
-  w |= __shfl_xor(w, 4, 64);
-  if ((lane & 7) == 0) reinterpret_cast<uint32_t*>(codes_se + orow * (kDim / 2))[lane >> 3] = w;
-  // mantissa bit-planes: bit m of plane b is bit b of j_m
-  for (int b = 0; b < tab.mant_bits; ++b) {
-    const unsigned long long plane = __ballot((j >> b) & 1);
-    if (lane == 0)
-      reinterpret_cast<unsigned long long*>(codes_m + orow * 8 * tab.mant_bits)[b] = plane;
-  }
+  encode_key_row_wave(k + row * kDim, hadamard, scale_mode, key_scale + orow,
+                      codes_se + orow * (kDim / 2), codes_m + orow * 8 * tab.mant_bits, tab);
 }
 
 __global__ __launch_bounds__(kBlock) void encode_int8_kernel(

@@ -4,8 +4,11 @@
 // 64-element head vector maps one element per lane.
 #pragma once
 
+#include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include "pot_launch.hpp"
 
 namespace potattn {
 
@@ -62,6 +65,84 @@ __device__ __forceinline__ int wave_quantize_int8(float x, float* step) {
   r = fminf(fmaxf(r, -127.0f), 127.0f);
   *step = amax / 127.0f;  // correctly rounded division
   return (int)r;
+}
+
+// Log-nearest PoT-Mk code of one element. Returns the nibble (neg<<3 | e, or
+// 7 for zero) and the mantissa j.
+__device__ __forceinline__ int classify(float x, float s, const EncodeTables& tab, int* j_out) {
+  *j_out = 0;
+  if (!(s > 0.0f) || x == 0.0f || x != x) return kZeroField;
+  const float u = fabsf(x) / s;  // one correctly rounded division
+  if (!(u > tab.zero_cut)) return kZeroField;
+  const int n = 1 << tab.mant_bits;
+  const uint32_t ub = __float_as_uint(u);
+  const int e2 = (int)((ub >> 23) & 0xFF) - 127;         // u > 2^-7: normal
+  const float m = __uint_as_float((ub & 0x007FFFFFu) | 0x3F800000u);  // [1, 2)
+  int c = 0;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) c += (i < n && m > tab.cut[i]) ? 1 : 0;
+  int e, j;
+  if (e2 >= 0) {  // u >= 1: the top binade, saturating at its largest value
+    e = 0;
+    j = (e2 > 0) ? n - 1 : min(c, n - 1);
+  } else if (c == n) {  // rounds up to the next binade's first value
+    e = -e2 - 1;
+    j = 0;
+  } else {
+    e = -e2;
+    j = c;
+  }
+  if (e > kExpMax) {  // between the zero cut and 2^-E: the smallest magnitude
+    e = kExpMax;
+    j = 0;
+  }
+  *j_out = j;
+  return ((x < 0.0f) ? 8 : 0) | e;
+}
+
+// Encodes one 64-element fp16 key row with the calling wave, one element per
+// lane (Sec. II-A, II-D): optional exact fp64 Walsh-Hadamard rotation, the row
+// scale (scale_mode 0: s = max|K'| written to *scale; 1: s read from *scale),
+// the log-nearest code of every element, sign/exponent nibbles packed by lane
+// shuffles (element m at bit 4*(m%8) of dword m/8 of se_out) and mantissa
+// bit-planes by ballots (bit m of the 64-bit plane b of m_out is bit b of j_m).
+__device__ __forceinline__ void encode_key_row_wave(const __half* __restrict__ k_row,
+                                                    int hadamard, int scale_mode,
+                                                    float* __restrict__ scale,
+                                                    uint8_t* __restrict__ se_out,
+                                                    uint8_t* __restrict__ m_out,
+                                                    const EncodeTables& tab) {
+  const int lane = lane_id();
+  float x = __half2float(k_row[lane]);
+  if (hadamard) x = (float)(wave_fwht64((double)x) * 0.125);
+  float s;
+  if (scale_mode == 0) {
+    s = wave_max(fabsf(x));
+    if (lane == 0) *scale = s;
+  } else {
+    s = *scale;
+  }
+  int j;
+  const int nib = classify(x, s, tab, &j);
+  uint32_t w = (uint32_t)nib << (4 * (lane & 7));
+  w |= __shfl_xor(w, 1, 64);
+  w |= __shfl_xor(w, 2, 64);
+  w |= __shfl_xor(w, 4, 64);
+  if ((lane & 7) == 0) reinterpret_cast<uint32_t*>(se_out)[lane >> 3] = w;
+  for (int b = 0; b < tab.mant_bits; ++b) {
+    const unsigned long long plane = __ballot((j >> b) & 1);
+    if (lane == 0) reinterpret_cast<unsigned long long*>(m_out)[b] = plane;
+  }
+}
+
+// Value cache layout: token t of a sequence, dim d, lives at
+// ((t/8)*8) * 64 + d * 8 + t % 8 halves from the sequence's base. Stores one
+// token's 64 fp16 values with the calling wave (lane = dim).
+__device__ __forceinline__ void store_value_token_wave(const uint16_t* __restrict__ v_row,
+                                                       uint16_t* __restrict__ v_seq,
+                                                       int64_t t) {
+  const int lane = lane_id();
+  v_seq[(t / 8) * 8 * kDim + lane * 8 + t % 8] = v_row[lane];
 }
 
 }  // namespace potattn

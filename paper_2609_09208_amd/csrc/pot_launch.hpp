@@ -63,6 +63,16 @@ struct DecodeArgs {
   int32_t* dbg_scores;
   int32_t* dbg_m_final;
   int32_t* dbg_m_split;
+  // fused append (PoT only; app_k NULL: none): the new token of every
+  // (batch, kv head) sequence is encoded into cache row T - 1 and its values
+  // stored there by the query-preparation kernel, before the decode kernel runs
+  const uint16_t* app_k;     // fp16 [B*Hkv][64]
+  const uint16_t* app_v;     // fp16 [B*Hkv][64]
+  uint8_t* app_codes_se;     // the cache arrays, written at row T - 1 only
+  uint8_t* app_codes_m;
+  float* app_key_scale;
+  uint16_t* app_v_cache;
+  EncodeTables app_tab;
   int64_t t_cap;
   int32_t B, Hq, Hkv, T;
   int32_t n_splits, split_len;

@@ -1,0 +1,218 @@
+"""GPU parity of the fused append + decode step (pot_append_decode_attention).
+
+One call appends the new token of every (batch, kv head) sequence at position
+T - 1 and attends over positions 0 .. T-1. The bar:
+* the cache rows it writes (codes, mantissa planes, scale, values) and its
+  output equal, bit for bit, those of the three separate calls it replaces
+  (pot_encode_keys on row T - 1, pot_store_values, pot_decode_attention);
+* codes, scales, q^, Delta, int32 scores and integer maxima equal the
+  oracle's, which encodes the whole key block itself, and O is within 2e-3.
+Row T - 1 of the cache holds the encoding of a poison key (and a poison value)
+before the call, so a row the append did not write shows up in every check.
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2609_09208_amd as pa
+from parity_util import DEV, O_TOL, oracle_pot, to_dev
+from workloads import POISON_K, POISON_V, make_decode_inputs, make_decode_inputs_device
+
+pytestmark = pytest.mark.gpu
+
+TAPS = ("qhat", "delta", "scores", "m_final", "m_split")
+
+
+def _cache(k_bits, v_bits, B, Hkv, t_cap, fmt, mant_bits):
+    """Device cache from host fp16 bit patterns [B, Hkv, t_cap, 64]."""
+    rows = B * Hkv * t_cap
+    k = to_dev(np.ascontiguousarray(k_bits).reshape(rows, 64)).view(torch.float16)
+    se = torch.zeros((rows, 32), dtype=torch.uint8, device=DEV)
+    cm = torch.zeros((rows, 8 * mant_bits), dtype=torch.uint8, device=DEV) if mant_bits else None
+    sc = torch.zeros(rows, dtype=torch.float32, device=DEV)
+    pa.pot_encode_keys(fmt, k, rows, 1, 0, sc, se, cm)
+    v = pa.alloc_value_cache(B, Hkv, t_cap, DEV)
+    src = to_dev(np.ascontiguousarray(v_bits).reshape(B * Hkv, t_cap, 64)).view(torch.float16)
+    pa.pot_store_values(src, B * Hkv, t_cap, t_cap, 0, v)
+    return dict(se=se, cm=cm, sc=sc, v=v)
+
+
+def _clone(c):
+    return {k: (t.clone() if t is not None else None) for k, t in c.items()}
+
+
+def _taps(B, Hq, T):
+    max_s = -(-T // 256)
+    bufs = dict(qhat=torch.empty((B, Hq, 64), dtype=torch.int8, device=DEV),
+                delta=torch.empty((B, Hq), dtype=torch.float32, device=DEV),
+                scores=torch.empty((B, Hq, T), dtype=torch.int32, device=DEV),
+                m_final=torch.empty((B, Hq), dtype=torch.int32, device=DEV),
+                m_split=torch.empty((B, Hq, max_s), dtype=torch.int32, device=DEV))
+    dbg = pa.pot_debug()
+    for k, t in bufs.items():
+        setattr(dbg, k, t.data_ptr())
+    return dbg, bufs
+
+
+def _fused_and_separate(q, k_new, v_new, base, heads, B, Hq, Hkv, T, t_cap, fmt, mant_bits,
+                        taps=True):
+    """Runs the fused call on one copy of the cache and the three separate calls
+    on another. Returns (fused cache, fused out, fused taps, separate cache,
+    separate out, separate taps, n_splits, split_len)."""
+    fused, sep = _clone(base), _clone(base)
+    ws_bytes = pa.pot_decode_workspace_bytes(B, Hq, Hkv, T)
+    res = []
+    for path, c in (("fused", fused), ("separate", sep)):
+        out = torch.empty((B, Hq, 64), dtype=torch.float32, device=DEV)
+        ws = pa.alloc_workspace(ws_bytes, DEV)
+        dbg, bufs = _taps(B, Hq, T) if taps else (None, {})
+        if path == "fused":
+            pa.pot_append_decode_attention(fmt, q, k_new, v_new, c["se"], c["cm"], c["sc"],
+                                           c["v"], t_cap, heads, B, Hq, Hkv, T, out, ws,
+                                           dbg=dbg)
+        else:
+            pos = T - 1
+            pa.pot_encode_keys(fmt, k_new, B * Hkv, t_cap, 0, c["sc"][pos:], c["se"][pos:],
+                               c["cm"][pos:] if mant_bits else None)
+            pa.pot_store_values(v_new, B * Hkv, 1, t_cap, pos, c["v"])
+            pa.pot_decode_attention(fmt, q, c["se"], c["cm"], c["sc"], c["v"], t_cap, heads, B,
+                                    Hq, Hkv, T, out, ws, dbg=dbg)
+        torch.cuda.synchronize()
+        res.append((c, out, bufs, dbg))
+    (fc, fo, fb, fd), (sc_, so, sb, _) = res
+    n_splits = fd.n_splits if fd is not None else None
+    split_len = fd.split_len if fd is not None else None
+    return fc, fo, fb, sc_, so, sb, n_splits, split_len
+
+
+def _assert_same(fc, fo, fb, sc_, so, sb):
+    for k in ("se", "cm", "sc", "v"):
+        if fc[k] is not None:
+            assert torch.equal(fc[k].view(torch.uint8), sc_[k].view(torch.uint8)), f"cache {k}"
+    assert torch.equal(fo.view(torch.int32), so.view(torch.int32)), "out differs from 3 calls"
+    for k in fb:
+        assert torch.equal(fb[k], sb[k]), f"tap {k} differs from 3 calls"
+
+
+def _run(seed, B, Hq, Hkv, T, t_cap=None, mant_bits=0, hadamard=False):
+    d = make_decode_inputs(seed, B=B, Hq=Hq, Hkv=Hkv, T=T, t_cap=t_cap)
+    t_cap = d["t_cap"]
+    fmt = pa.make_format(mant_bits, 7, hadamard)
+    k_init, v_init = d["k_bits"].copy(), d["v_bits"].copy()
+    k_init[:, :, T - 1] = np.float16(POISON_K).view(np.uint16)
+    v_init[:, :, T - 1] = np.float16(POISON_V).view(np.uint16)
+    base = _cache(k_init, v_init, B, Hkv, t_cap, fmt, mant_bits)
+    k_new = to_dev(np.ascontiguousarray(d["k_bits"][:, :, T - 1])).view(torch.float16)
+    v_new = to_dev(np.ascontiguousarray(d["v_bits"][:, :, T - 1])).view(torch.float16)
+    q = to_dev(d["q"])
+    fc, fo, fb, sc_, so, sb, n_splits, split_len = _fused_and_separate(
+        q, k_new, v_new, base, d["kv_head_of_q"], B, Hq, Hkv, T, t_cap, fmt, mant_bits)
+    _assert_same(fc, fo, fb, sc_, so, sb)
+    # against the oracle, which encodes the whole (unpoisoned) key block itself
+    o_se, o_cm, o_sc, o = oracle_pot(d, mant_bits, 7, hadamard, split_len=split_len)
+    live = np.zeros((B, Hkv, t_cap), bool)
+    live[:, :, :T] = True
+    live = live.reshape(-1)
+    assert np.array_equal(fc["se"].cpu().numpy()[live], o_se[live]), "codes_se vs oracle"
+    if mant_bits:
+        assert np.array_equal(fc["cm"].cpu().numpy()[live], o_cm[live]), "codes_m vs oracle"
+    assert np.array_equal(fc["sc"].cpu().numpy()[live].view(np.uint32),
+                          o_sc[live].view(np.uint32)), "key_scale vs oracle"
+    for k in TAPS:
+        g = fb[k].cpu().numpy()
+        if k == "m_split":
+            g = g.reshape(-1)[:B * Hq * n_splits].reshape(B, Hq, n_splits)
+        if k == "delta":
+            assert np.array_equal(g.view(np.uint32), o[k].view(np.uint32)), k
+        else:
+            assert np.array_equal(g, o[k]), f"{k} vs oracle"
+    err = float(np.abs(fo.cpu().numpy() - o["out"]).max())
+    assert err <= O_TOL, err
+    return err, n_splits
+
+
+def test_append_tinyllama_layer_t4096():
+    err, s = _run(7, B=1, Hq=32, Hkv=4, T=4096)
+    print(f"append T=4096 splits={s} O err {err:.3e}")
+
+
+@pytest.mark.parametrize("T,t_cap", [(1, 8), (2, 8), (255, 264), (1000, 1024)])
+def test_append_ragged(T, t_cap):
+    _run(100 + T, B=2, Hq=8, Hkv=2, T=T, t_cap=t_cap)
+
+
+@pytest.mark.parametrize("mant_bits,hadamard", [(1, False), (2, True), (4, True)])
+def test_append_mantissa_and_hadamard(mant_bits, hadamard):
+    _run(200 + mant_bits, B=2, Hq=32, Hkv=4, T=300, mant_bits=mant_bits, hadamard=hadamard)
+
+
+@pytest.mark.parametrize("Hq,Hkv", [(4, 4), (8, 4), (16, 4)])
+def test_append_group_sizes(Hq, Hkv):
+    _run(300 + Hq, B=3, Hq=Hq, Hkv=Hkv, T=513)
+
+
+def test_append_three_steps_in_a_row():
+    """Three decode steps T0+1, T0+2, T0+3 on one cache: after each, the cache
+    rows so far and the output match the oracle run on the unpoisoned block."""
+    B, Hq, Hkv, T0, t_cap = 2, 32, 4, 509, 520
+    d = make_decode_inputs(400, B=B, Hq=Hq, Hkv=Hkv, T=T0 + 3, t_cap=t_cap)
+    fmt = pa.make_format(0, 7, False)
+    k_init, v_init = d["k_bits"].copy(), d["v_bits"].copy()
+    k_init[:, :, T0:] = np.float16(POISON_K).view(np.uint16)
+    v_init[:, :, T0:] = np.float16(POISON_V).view(np.uint16)
+    c = _cache(k_init, v_init, B, Hkv, t_cap, fmt, 0)
+    ws = pa.alloc_workspace(pa.pot_decode_workspace_bytes(B, Hq, Hkv, T0 + 3), DEV)
+    out = torch.empty((B, Hq, 64), dtype=torch.float32, device=DEV)
+    for step in range(1, 4):
+        T = T0 + step
+        k_new = to_dev(np.ascontiguousarray(d["k_bits"][:, :, T - 1])).view(torch.float16)
+        v_new = to_dev(np.ascontiguousarray(d["v_bits"][:, :, T - 1])).view(torch.float16)
+        q = to_dev(np.ascontiguousarray(d["q"] * (1.0 + step)).astype(np.float32))
+        dbg, bufs = _taps(B, Hq, T)
+        pa.pot_append_decode_attention(fmt, q, k_new, v_new, c["se"], None, c["sc"], c["v"],
+                                       t_cap, d["kv_head_of_q"], B, Hq, Hkv, T, out, ws,
+                                       dbg=dbg)
+        torch.cuda.synchronize()
+        ds = dict(d, T=T, q=(d["q"] * (1.0 + step)).astype(np.float32))
+        o_se, _, o_sc, o = oracle_pot(ds, 0, 7, False, split_len=dbg.split_len)
+        live = np.zeros((B, Hkv, t_cap), bool)
+        live[:, :, :T] = True
+        live = live.reshape(-1)
+        assert np.array_equal(c["se"].cpu().numpy()[live], o_se[live]), step
+        assert np.array_equal(bufs["scores"].cpu().numpy(), o["scores"]), step
+        assert np.array_equal(bufs["m_final"].cpu().numpy(), o["m_final"]), step
+        err = float(np.abs(out.cpu().numpy() - o["out"]).max())
+        assert err <= O_TOL, (step, err)
+
+
+def test_append_full_size_b64_t32768():
+    """B = 64, T = 32768 (the full-size workload, in the launch configuration
+    the bench times): the fused call and the three separate calls agree bit
+    for bit, and the appended rows equal the oracle's encoding of the keys."""
+    import oracle
+    B, Hq, Hkv, T = 64, 32, 4, 32768
+    d = make_decode_inputs_device(11, B, Hq, Hkv, T, DEV)
+    fmt = pa.make_format(0, 7, False)
+    rows = B * Hkv * T
+    se = torch.zeros((rows, 32), dtype=torch.uint8, device=DEV)
+    sc = torch.zeros(rows, dtype=torch.float32, device=DEV)
+    k_old = d["k"].clone()
+    k_old[:, :, T - 1] = POISON_K
+    pa.pot_encode_keys(fmt, k_old, rows, 1, 0, sc, se, None)
+    del k_old
+    v = pa.alloc_value_cache(B, Hkv, T, DEV)
+    v_old = d["v"].clone()
+    v_old[:, :, T - 1] = POISON_V
+    pa.pot_store_values(v_old, B * Hkv, T, T, 0, v)
+    del v_old
+    base = dict(se=se, cm=None, sc=sc, v=v)
+    k_new = d["k"][:, :, T - 1].contiguous()
+    v_new = d["v"][:, :, T - 1].contiguous()
+    del d["k"], d["v"]
+    fc, fo, fb, sc_, so, sb, _, _ = _fused_and_separate(
+        d["q"], k_new, v_new, base, d["kv_head_of_q"], B, Hq, Hkv, T, T, fmt, 0, taps=False)
+    _assert_same(fc, fo, fb, sc_, so, sb)
+    o_se, _, o_sc = oracle.encode_keys(k_new.cpu().numpy().view(np.uint16).reshape(-1, 64))
+    new_rows = torch.arange(B * Hkv, device=DEV) * T + (T - 1)
+    assert np.array_equal(fc["se"][new_rows].cpu().numpy(), o_se)
+    assert np.array_equal(fc["sc"][new_rows].cpu().numpy().view(np.uint32), o_sc.view(np.uint32))
