@@ -8,7 +8,8 @@ the paper leaves precision open) through ctypes on numpy arrays.
 
 Sections cited: Sec. II-A eq. (pot) key code and INT8 query; Sec. II-B eq. (sac)
 score; Sec. II-C eq. (exact) head-room; Sec. II-D eq. (mant) mantissa family;
-Sec. II-E eq. (logsm) integer-log2 softmax maximum; Sec. I-A / V-A Hadamard.
+Sec. II-E eq. (logsm) integer-log2 softmax maximum, and INT8 values with a
+power-of-two per-token scale; Sec. I-A / V-A Hadamard.
 """
 from __future__ import annotations
 
@@ -58,6 +59,12 @@ def _load():
                                       i32, i32, i32, i32, i32, i32,
                                       P, P, P, P, P, P, P]
     lib.oracle_pot_decode.restype = i32
+    lib.oracle_pot_decode_v8.argtypes = [i32, i32, i32, P, P, P, P, P, P, i64, P,
+                                         i32, i32, i32, i32, i32, i32,
+                                         P, P, P, P, P, P, P]
+    lib.oracle_pot_decode_v8.restype = i32
+    lib.oracle_quantize_values.argtypes = [P, i64, P, P]
+    lib.oracle_quantize_values.restype = i32
     lib.oracle_int8_encode_keys.argtypes = [i32, P, i64, P, P]
     lib.oracle_int8_encode_keys.restype = i32
     lib.oracle_int8_decode.argtypes = [i32, P, P, P, P, i64, P, i32, i32, i32,
@@ -172,6 +179,49 @@ def pot_decode(q, codes_se, codes_m, key_scale, v_fp16_bits, t_cap,
         _ptr(res["m_split"]), _ptr(res["out"]))
     if rc:
         raise ValueError(f"oracle_pot_decode failed: {rc}")
+    return res
+
+
+def quantize_values(v_fp16_bits):
+    """INT8 values with a power-of-two per-token scale (Sec. II-E).
+
+    v_fp16_bits: uint16 [..., 64]. Per row: g = largest integer with
+    max|v| * 2^g <= 127 (0 for a zero row), v^ = round-half-even(v * 2^g).
+    Returns (v^ int8 [rows, 64], g int8 [rows]); the value is v^ * 2^-g."""
+    v = _c(v_fp16_bits, np.uint16).reshape(-1, DIM)
+    rows = v.shape[0]
+    vh = np.empty((rows, DIM), np.int8)
+    g = np.empty(rows, np.int8)
+    rc = _load().oracle_quantize_values(_ptr(v), rows, _ptr(vh), _ptr(g))
+    if rc:
+        raise ValueError(f"oracle_quantize_values failed: {rc}")
+    return vh, g
+
+
+def pot_decode_v8(q, codes_se, codes_m, key_scale, v8, v_exp, t_cap, kv_head_of_q, B, Hq,
+                  Hkv, T, mant_bits=0, frac_bits=7, hadamard=False, split_len=None,
+                  tile=0, want_out=True):
+    """pot_decode with the values given as INT8 codes v8 [rows, 64] and
+    exponents v_exp [rows] (value v8 * 2^-v_exp, Sec. II-E)."""
+    split_len = T if split_len is None else int(split_len)
+    n_split = -(-T // split_len)
+    res = dict(qhat=np.empty((B, Hq, DIM), np.int8),
+               delta=np.empty((B, Hq), np.float32),
+               scores=np.empty((B, Hq, T), np.int32),
+               x=np.empty((B, Hq, T), np.float32),
+               m_final=np.empty((B, Hq), np.int32),
+               m_split=np.empty((B, Hq, n_split), np.int32),
+               out=np.empty((B, Hq, DIM), np.float64) if want_out else None)
+    cm = None if codes_m is None else _c(codes_m, np.uint8)
+    rc = _load().oracle_pot_decode_v8(
+        int(mant_bits), int(frac_bits), int(hadamard), _ptr(_c(q, np.float32)),
+        _ptr(_c(codes_se, np.uint8)), _ptr(cm), _ptr(_c(key_scale, np.float32)),
+        _ptr(_c(v8, np.int8)), _ptr(_c(v_exp, np.int8)), int(t_cap),
+        _ptr(_c(kv_head_of_q, np.int32)), B, Hq, Hkv, T, split_len, int(tile),
+        _ptr(res["qhat"]), _ptr(res["delta"]), _ptr(res["scores"]), _ptr(res["x"]),
+        _ptr(res["m_final"]), _ptr(res["m_split"]), _ptr(res["out"]))
+    if rc:
+        raise ValueError(f"oracle_pot_decode_v8 failed: {rc}")
     return res
 
 

@@ -292,7 +292,20 @@ static int sac_score(const int8_t* qh, const uint8_t* se, const uint8_t* mp,
 /*    tile, exact 2^(M_old - M_new) rescales, splits merged with exact      */
 /*    2^(M_s - M) factors. Used by tests to pin online == two-pass.         */
 
-static void softmax_av(const float* x, const uint16_t* const* vrows, int T,
+/* One cache row of values: fp16 (v16), or INT8 codes v8 with the per-token */
+/* power-of-two scale 2^-g (Sec. II-E), whose value is v8[d] * 2^-g.        */
+typedef struct {
+  const uint16_t* v16;
+  const int8_t* v8;
+  int g;
+} value_row;
+
+static double value_at(const value_row* r, int d) {
+  if (r->v8) return ldexp((double)r->v8[d], -r->g); /* exact */
+  return (double)oracle_half_to_float(r->v16[d]);
+}
+
+static void softmax_av(const float* x, const value_row* vrows, int T,
                        int split_len, int tile, int32_t* m_final,
                        int32_t* m_split, double* out) {
   float xmax = -INFINITY;
@@ -315,7 +328,7 @@ static void softmax_av(const float* x, const uint16_t* const* vrows, int T,
     for (int t = 0; t < T; ++t) {
       double w = exp2((double)x[t] - (double)M);
       l += w;
-      for (int d = 0; d < DIM; ++d) o[d] += w * oracle_half_to_float(vrows[t][d]);
+      for (int d = 0; d < DIM; ++d) o[d] += w * value_at(&vrows[t], d);
     }
     for (int d = 0; d < DIM; ++d) out[d] = o[d] / l;
     return;
@@ -345,7 +358,7 @@ static void softmax_av(const float* x, const uint16_t* const* vrows, int T,
       for (int t = t0; t < t1; ++t) {
         double w = exp2((double)x[t] - (double)Mrun);
         l += w;
-        for (int d = 0; d < DIM; ++d) o[d] += w * oracle_half_to_float(vrows[t][d]);
+        for (int d = 0; d < DIM; ++d) o[d] += w * value_at(&vrows[t], d);
       }
     }
     Ms[s] = Mrun;
@@ -375,19 +388,20 @@ static void softmax_av(const float* x, const uint16_t* const* vrows, int T,
 /* Optional outputs may be NULL. scores/x are [B][Hq][T], m_split is        */
 /* [B][Hq][ceil(T/split_len)], out is [B][Hq][64] in fp64.                  */
 
-int oracle_pot_decode(int mant_bits, int frac_bits, int hadamard,
-                      const float* q, const uint8_t* codes_se,
-                      const uint8_t* codes_m, const float* key_scale,
-                      const uint16_t* v, int64_t t_cap, const int32_t* kv_head_of_q,
-                      int B, int Hq, int Hkv, int T, int split_len, int tile,
-                      int8_t* qhat_out, float* delta_out, int32_t* scores_out,
-                      float* x_out, int32_t* m_final, int32_t* m_split,
-                      double* out) {
+static int pot_decode_impl(int mant_bits, int frac_bits, int hadamard,
+                           const float* q, const uint8_t* codes_se,
+                           const uint8_t* codes_m, const float* key_scale,
+                           const uint16_t* v, const int8_t* v8, const int8_t* v_exp,
+                           int64_t t_cap, const int32_t* kv_head_of_q,
+                           int B, int Hq, int Hkv, int T, int split_len, int tile,
+                           int8_t* qhat_out, float* delta_out, int32_t* scores_out,
+                           float* x_out, int32_t* m_final, int32_t* m_split,
+                           double* out) {
   if (T < 1 || T > t_cap || split_len < 1) return -1;
   int k = mant_bits;
   int n_split = (T + split_len - 1) / split_len;
   float* x = (float*)malloc(sizeof(float) * T);
-  const uint16_t** vrows = (const uint16_t**)malloc(sizeof(void*) * T);
+  value_row* vrows = (value_row*)malloc(sizeof(value_row) * T);
   int rc = 0;
   for (int b = 0; b < B && rc == 0; ++b) {
     for (int i = 0; i < Hq && rc == 0; ++i) {
@@ -408,7 +422,9 @@ int oracle_pot_decode(int mant_bits, int frac_bits, int hadamard,
         if (scores_out) scores_out[bh * T + t] = acc;
         x[t] = ((float)acc * key_scale[row]) * c;
         if (x_out) x_out[bh * T + t] = x[t];
-        vrows[t] = v + row * DIM;
+        vrows[t].v16 = v8 ? NULL : v + row * DIM;
+        vrows[t].v8 = v8 ? v8 + row * DIM : NULL;
+        vrows[t].g = v8 ? v_exp[row] : 0;
       }
       if (rc) break;
       softmax_av(x, vrows, T, split_len, tile, m_final ? m_final + bh : NULL,
@@ -419,6 +435,67 @@ int oracle_pot_decode(int mant_bits, int frac_bits, int hadamard,
   free(x);
   free(vrows);
   return rc;
+}
+
+int oracle_pot_decode(int mant_bits, int frac_bits, int hadamard,
+                      const float* q, const uint8_t* codes_se,
+                      const uint8_t* codes_m, const float* key_scale,
+                      const uint16_t* v, int64_t t_cap, const int32_t* kv_head_of_q,
+                      int B, int Hq, int Hkv, int T, int split_len, int tile,
+                      int8_t* qhat_out, float* delta_out, int32_t* scores_out,
+                      float* x_out, int32_t* m_final, int32_t* m_split,
+                      double* out) {
+  return pot_decode_impl(mant_bits, frac_bits, hadamard, q, codes_se, codes_m, key_scale, v,
+                         NULL, NULL, t_cap, kv_head_of_q, B, Hq, Hkv, T, split_len, tile,
+                         qhat_out, delta_out, scores_out, x_out, m_final, m_split, out);
+}
+
+/* The same with the values as INT8 codes v8 [rows][64] and per-row exponents */
+/* v_exp [rows] (value v8 * 2^-v_exp, Sec. II-E).                            */
+int oracle_pot_decode_v8(int mant_bits, int frac_bits, int hadamard,
+                         const float* q, const uint8_t* codes_se,
+                         const uint8_t* codes_m, const float* key_scale,
+                         const int8_t* v8, const int8_t* v_exp, int64_t t_cap,
+                         const int32_t* kv_head_of_q, int B, int Hq, int Hkv, int T,
+                         int split_len, int tile, int8_t* qhat_out, float* delta_out,
+                         int32_t* scores_out, float* x_out, int32_t* m_final,
+                         int32_t* m_split, double* out) {
+  return pot_decode_impl(mant_bits, frac_bits, hadamard, q, codes_se, codes_m, key_scale, NULL,
+                         v8, v_exp, t_cap, kv_head_of_q, B, Hq, Hkv, T, split_len, tile,
+                         qhat_out, delta_out, scores_out, x_out, m_final, m_split, out);
+}
+
+/* ---------------------------------------------------------------------- */
+/* INT8 values with a power-of-two per-token scale (Sec. II-E): the paper   */
+/* stores V as INT8 codes with a scale 2^-g per token; how g and the codes  */
+/* are rounded is not stated. Reading used here: g is the largest integer   */
+/* with max_d |v_d| * 2^g <= 127 (g = 0 for an all-zero row) and           */
+/* v^_d = round-half-even(v_d * 2^g), so |v^_d| <= 127 and the row maximum  */
+/* lands in [64, 127].                                                      */
+
+int oracle_quantize_values(const uint16_t* v_fp16, int64_t n_rows, int8_t* vhat,
+                           int8_t* v_exp) {
+  for (int64_t r = 0; r < n_rows; ++r) {
+    double v[DIM], amax = 0.0;
+    for (int d = 0; d < DIM; ++d) {
+      v[d] = (double)oracle_half_to_float(v_fp16[r * DIM + d]);
+      if (v[d] != v[d] || isinf(v[d])) return -1;
+      if (fabs(v[d]) > amax) amax = fabs(v[d]);
+    }
+    int g = 0;
+    if (amax > 0.0) {
+      while (ldexp(amax, g) > QMAX) --g;        /* exact: scaling by 2^g */
+      while (ldexp(amax, g + 1) <= QMAX) ++g;
+    }
+    if (g < -128 || g > 127) return -2;
+    v_exp[r] = (int8_t)g;
+    for (int d = 0; d < DIM; ++d) {
+      double c = nearbyint(ldexp(v[d], g)); /* default rounding: half to even */
+      if (c > QMAX || c < -QMAX) return -3;
+      vhat[r * DIM + d] = (int8_t)c;
+    }
+  }
+  return 0;
 }
 
 /* ---------------------------------------------------------------------- */
@@ -449,7 +526,7 @@ int oracle_int8_decode(int hadamard, const float* q, const int8_t* codes,
   if (T < 1 || T > t_cap || split_len < 1) return -1;
   int n_split = (T + split_len - 1) / split_len;
   float* x = (float*)malloc(sizeof(float) * T);
-  const uint16_t** vrows = (const uint16_t**)malloc(sizeof(void*) * T);
+  value_row* vrows = (value_row*)malloc(sizeof(value_row) * T);
   for (int b = 0; b < B; ++b) {
     for (int i = 0; i < Hq; ++i) {
       int h = kv_head_of_q[i];
@@ -466,7 +543,9 @@ int oracle_int8_decode(int hadamard, const float* q, const int8_t* codes,
         for (int m = 0; m < DIM; ++m) acc += (int64_t)qh[m] * codes[row * DIM + m];
         if (scores_out) scores_out[bh * T + t] = (int32_t)acc;
         x[t] = ((float)acc * key_scale[row]) * c;
-        vrows[t] = v + row * DIM;
+        vrows[t].v16 = v + row * DIM;
+        vrows[t].v8 = NULL;
+        vrows[t].g = 0;
       }
       softmax_av(x, vrows, T, split_len, 0, m_final ? m_final + bh : NULL,
                  m_split ? m_split + bh * n_split : NULL,
