@@ -160,6 +160,23 @@ pot_status pot_store_values(const uint16_t* v_fp16, int64_t n_seq, int64_t n_tok
                             int64_t t_cap, int64_t t0, uint16_t* v_cache,
                             void* stream);
 
+/* Store fp16 values as INT8 codes with a power-of-two per-token scale
+ * (Sec. II-E, the value cache the paper pairs with PoT keys: 64 + 1 bytes per
+ * token instead of 128). The paper leaves the rounding open; here, per token
+ * row v (d values): g = the largest integer with max|v| 2^g <= 127 (g = 0 for
+ * an all-zero row) and v^ = round-half-even(v 2^g), so |v^| <= 127 and the
+ * value is v^ 2^-g (exact for every fp16 input range: g lies in [-10, 30]).
+ *  v_fp16   [n_seq][n_tok][d] fp16, dense, device (token-major rows).
+ *  v_u8     value bytes v^ + 128 (offset binary), token-interleaved like the
+ *           fp16 cache: byte ((t/8)*8)*d + dim*8 + t%8 of each sequence's
+ *           t_cap*d bytes; [B*Hkv][t_cap][d] bytes in all.
+ *  v_exp    int8 [B*Hkv][t_cap]: g of each token.
+ * n_seq, n_tok, t_cap, t0 and the errors as pot_store_values (all three
+ * pointers 16-byte aligned). */
+pot_status pot_store_values_int8(const uint16_t* v_fp16, int64_t n_seq, int64_t n_tok,
+                                 int64_t t_cap, int64_t t0, uint8_t* v_u8,
+                                 int8_t* v_exp, void* stream);
+
 /* Workspace bytes pot_decode_attention needs for this problem shape: the
  * prepared query operands of each (batch, kv head) and the key-split partials
  * (M_s, l_s, o_s) for the largest split count the planner can choose.
@@ -235,6 +252,27 @@ pot_status pot_append_decode_attention(const pot_format* fmt, const float* q,
                                        int32_t B, int32_t Hq, int32_t Hkv, int32_t T,
                                        float* out, void* workspace, size_t ws_bytes,
                                        pot_debug* dbg, void* stream);
+
+/* Decode attention with PoT keys and INT8 values (pot_store_values_int8):
+ * O = sum_t p_t v^_t 2^-g_t / sum_t p_t with the weights p of
+ * pot_decode_attention (Sec. II-E). engine 0 scores by shift-accumulate as
+ * pot_decode_attention, engine 1 by the byte-decode path of
+ * pot_ds4a_decode_attention (PoT-4 only, else POT_ERR_UNSUPPORTED); the
+ * int32 scores and integer maxima are the same as with fp16 values. In the
+ * kernel each workgroup takes g_ref = min g over its keys and forms the
+ * weights p 2^(g_ref - g_t) (exact, never above p) for the matrix cores,
+ * with the value bytes read as the fp16 numbers 1152 + v^; the 1152 offset
+ * and 2^-g_ref are applied to the fp32 sums. Arguments, workspace, taps and
+ * errors as pot_decode_attention, with (v_u8, v_exp) in place of v_cache
+ * (NULL or not 16-byte aligned -> INVALID_ARG); engine outside {0, 1} ->
+ * INVALID_ARG. */
+pot_status pot_decode_attention_v8(const pot_format* fmt, int32_t engine, const float* q,
+                                   const uint8_t* codes_se, const uint8_t* codes_m,
+                                   const float* key_scale, const uint8_t* v_u8,
+                                   const int8_t* v_exp, int64_t t_cap,
+                                   const int32_t* kv_head_of_q, int32_t B, int32_t Hq,
+                                   int32_t Hkv, int32_t T, float* out, void* workspace,
+                                   size_t ws_bytes, pot_debug* dbg, void* stream);
 
 /* ---- comparison paths on the same cache skeleton --------------------- */
 

@@ -72,6 +72,9 @@ def _load_library():
         "pot_decode_workspace_bytes_for_splits": (S, [i32, i32, i32, i32, i32]),
         "pot_workspace_init": (i32, [P, S, P]),
         "pot_store_values": (i32, [P, i64, i64, i64, i64, P, P]),
+        "pot_store_values_int8": (i32, [P, i64, i64, i64, i64, P, P, P]),
+        "pot_decode_attention_v8": (i32, [fmt_p, i32, P, P, P, P, P, P, i64, P, i32, i32,
+                                          i32, i32, P, P, S, dbg_p, P]),
         "pot_decode_attention": (i32, [fmt_p, P, P, P, P, P, i64, P, i32, i32,
                                        i32, i32, P, P, S, dbg_p, P]),
         "pot_append_decode_attention": (i32, [fmt_p, P, P, P, P, P, P, P, i64, P, i32, i32,
@@ -155,6 +158,25 @@ def pot_store_values(v_fp16, n_seq: int, n_tok: int, t_cap: int, t0: int, v_cach
                      stream=None) -> None:
     _check(_lib.pot_store_values(_ptr(v_fp16), int(n_seq), int(n_tok), int(t_cap),
                                  int(t0), _ptr(v_cache), _stream(stream)))
+
+
+def pot_store_values_int8(v_fp16, n_seq: int, n_tok: int, t_cap: int, t0: int, v_u8, v_exp,
+                          stream=None) -> None:
+    _check(_lib.pot_store_values_int8(_ptr(v_fp16), int(n_seq), int(n_tok), int(t_cap),
+                                      int(t0), _ptr(v_u8), _ptr(v_exp), _stream(stream)))
+
+
+def pot_decode_attention_v8(fmt: pot_format, engine: int, q, codes_se, codes_m, key_scale,
+                            v_u8, v_exp, t_cap: int, kv_head_of_q, B: int, Hq: int, Hkv: int,
+                            T: int, out, workspace, ws_bytes=None,
+                            dbg: pot_debug | None = None, stream=None) -> None:
+    _, hp = _heads(kv_head_of_q)
+    nbytes = workspace.numel() * workspace.element_size() if ws_bytes is None else ws_bytes
+    _check(_lib.pot_decode_attention_v8(
+        ctypes.byref(fmt), int(engine), _ptr(q), _ptr(codes_se), _ptr(codes_m),
+        _ptr(key_scale), _ptr(v_u8), _ptr(v_exp), int(t_cap), hp, B, Hq, Hkv, T, _ptr(out),
+        _ptr(workspace), nbytes, ctypes.byref(dbg) if dbg is not None else None,
+        _stream(stream)))
 
 
 def pot_encode_keys(fmt: pot_format, k_fp16, n_rows: int, out_row_stride: int,
@@ -252,6 +274,14 @@ def alloc_value_cache(B: int, Hkv: int, t_cap: int, device):
     """Value cache of B*Hkv sequences of t_cap tokens (token-interleaved)."""
     import torch
     return torch.zeros((B, Hkv, t_cap, HEAD_DIM), dtype=torch.float16, device=device)
+
+
+def alloc_value_cache_int8(B: int, Hkv: int, t_cap: int, device):
+    """INT8 value cache: (value bytes uint8 [B,Hkv,t_cap,64] token-interleaved,
+    exponents int8 [B,Hkv,t_cap])."""
+    import torch
+    return (torch.zeros((B, Hkv, t_cap, HEAD_DIM), dtype=torch.uint8, device=device),
+            torch.zeros((B, Hkv, t_cap), dtype=torch.int8, device=device))
 
 
 def alloc_workspace(nbytes: int, device):

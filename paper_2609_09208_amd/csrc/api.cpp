@@ -93,9 +93,10 @@ Plan plan_bound(int B, int Hkv, int T) {
 }
 
 std::atomic<int> g_cus[64];
-std::atomic<int> g_occ[3][9][5];
+// [score mode][INT8 values][G][mant_bits]
+std::atomic<int> g_occ[4][2][9][5];
 
-long device_slots(int mode, int G, int mant_bits) {
+long device_slots(int mode, int G, int mant_bits, bool v8) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
   int cus = g_cus[dev].load(std::memory_order_relaxed);
@@ -105,11 +106,12 @@ long device_slots(int mode, int G, int mant_bits) {
       cus = 256;
     g_cus[dev].store(cus, std::memory_order_relaxed);
   }
-  int occ = g_occ[mode][G][mant_bits].load(std::memory_order_relaxed);
+  std::atomic<int>& slot = g_occ[mode][v8 ? 1 : 0][G][mant_bits];
+  int occ = slot.load(std::memory_order_relaxed);
   if (occ <= 0) {
-    occ = decode_occupancy(mode, G, mant_bits);
+    occ = decode_occupancy(mode, G, mant_bits, v8);
     if (occ <= 0) occ = 2;
-    g_occ[mode][G][mant_bits].store(occ, std::memory_order_relaxed);
+    slot.store(occ, std::memory_order_relaxed);
   }
   return (long)cus * occ;
 }
@@ -158,16 +160,23 @@ pot_status check_heads(const int32_t* map, int Hq, int Hkv, DecodeArgs* a, int* 
 // Shared tail of the three decode entry points.
 pot_status decode_common(int mode, int mant_bits, DecodeArgs& a, const int32_t* map, int B,
                          int Hq, int Hkv, int T, int64_t t_cap, void* workspace,
-                         size_t ws_bytes, pot_debug* dbg, void* stream) {
+                         size_t ws_bytes, pot_debug* dbg, void* stream, bool v8 = false) {
   if (!shape_ok(B, Hq, Hkv, T))
     return fail(POT_ERR_INVALID_ARG, "bad shape B=%d Hq=%d Hkv=%d T=%d", B, Hq, Hkv, T);
   if (t_cap < T) return fail(POT_ERR_INVALID_ARG, "T %d > t_cap %lld", T, (long long)t_cap);
   if (t_cap % 8)
     return fail(POT_ERR_INVALID_ARG, "t_cap %lld is not a multiple of 8 (value-cache groups)",
                 (long long)t_cap);
-  if (!a.q || !a.v || !a.out) return fail(POT_ERR_INVALID_ARG, "q, v or out is NULL");
-  if (!aligned(a.q, 16) || !aligned(a.v, 16) || !aligned(a.out, 16))
-    return fail(POT_ERR_INVALID_ARG, "q, v and out must be 16-byte aligned");
+  if (v8) {
+    if (!a.q || !a.v8 || !a.v_exp || !a.out)
+      return fail(POT_ERR_INVALID_ARG, "q, v_u8, v_exp or out is NULL");
+    if (!aligned(a.q, 16) || !aligned(a.v8, 16) || !aligned(a.v_exp, 16) || !aligned(a.out, 16))
+      return fail(POT_ERR_INVALID_ARG, "q, v_u8, v_exp and out must be 16-byte aligned");
+  } else {
+    if (!a.q || !a.v || !a.out) return fail(POT_ERR_INVALID_ARG, "q, v or out is NULL");
+    if (!aligned(a.q, 16) || !aligned(a.v, 16) || !aligned(a.out, 16))
+      return fail(POT_ERR_INVALID_ARG, "q, v and out must be 16-byte aligned");
+  }
   if (!workspace) return fail(POT_ERR_INVALID_ARG, "workspace is NULL");
   if (!aligned(workspace, 256)) return fail(POT_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
   int G = 0;
@@ -180,7 +189,7 @@ pot_status decode_common(int mode, int mant_bits, DecodeArgs& a, const int32_t* 
     p = plan_from_count(T, force);
   } else {
     const int mbits = mode == kScorePot ? mant_bits : 0;
-    const int S = split_count_for_slots((long)B * Hkv, device_slots(mode, G, mbits));
+    const int S = split_count_for_slots((long)B * Hkv, device_slots(mode, G, mbits, v8));
     p = plan_from_count(T, std::min(S, plan_bound(B, Hkv, T).n_splits));
   }
   const WsLayout w = ws_layout(B, Hq, Hkv, p.n_splits);
@@ -213,8 +222,9 @@ pot_status decode_common(int mode, int mant_bits, DecodeArgs& a, const int32_t* 
     if (debug && mode == kScoreFp16)
       return fail(POT_ERR_UNSUPPORTED, "debug taps are not available on the fp16 path");
   }
-  return hip_status(launch_decode(mode, G, mant_bits, debug, a, static_cast<hipStream_t>(stream)),
-                    "decode launch");
+  return hip_status(
+      launch_decode(mode, G, mant_bits, debug, v8, a, static_cast<hipStream_t>(stream)),
+      "decode launch");
 }
 
 }  // namespace
@@ -282,6 +292,30 @@ pot_status pot_store_values(const uint16_t* v_fp16, int64_t n_seq, int64_t n_tok
     return fail(POT_ERR_INVALID_ARG, "v_fp16 and v_cache must be 16-byte aligned");
   return hip_status(launch_store_values(v_fp16, n_seq, n_tok, t_cap, t0, v_cache,
                                         static_cast<hipStream_t>(stream)),
+                    "store values launch");
+}
+
+pot_status pot_store_values_int8(const uint16_t* v_fp16, int64_t n_seq, int64_t n_tok,
+                                 int64_t t_cap, int64_t t0, uint8_t* v_u8, int8_t* v_exp,
+                                 void* stream) {
+  if (n_seq < 0 || n_tok < 0)
+    return fail(POT_ERR_INVALID_ARG, "n_seq %lld / n_tok %lld < 0", (long long)n_seq,
+                (long long)n_tok);
+  if (t_cap < 8 || t_cap % 8)
+    return fail(POT_ERR_INVALID_ARG, "t_cap %lld is not a positive multiple of 8",
+                (long long)t_cap);
+  if (t0 < 0 || t0 + n_tok > t_cap)
+    return fail(POT_ERR_INVALID_ARG, "tokens [%lld, %lld) outside [0, t_cap = %lld)",
+                (long long)t0, (long long)(t0 + n_tok), (long long)t_cap);
+  if (n_seq == 0 || n_tok == 0) return ok();
+  if (!v_fp16 || !v_u8 || !v_exp)
+    return fail(POT_ERR_INVALID_ARG, "v_fp16, v_u8 or v_exp is NULL");
+  if (!aligned(v_fp16, 16) || !aligned(v_u8, 16) || !aligned(v_exp, 16))
+    return fail(POT_ERR_INVALID_ARG, "v_fp16, v_u8 and v_exp must be 16-byte aligned");
+  if (n_seq > ((int64_t)1 << 31) / n_tok)
+    return fail(POT_ERR_INVALID_ARG, "n_seq * n_tok too large");
+  return hip_status(launch_store_values_i8(v_fp16, n_seq, n_tok, t_cap, t0, v_u8, v_exp,
+                                           static_cast<hipStream_t>(stream)),
                     "store values launch");
 }
 
@@ -364,6 +398,38 @@ pot_status pot_append_decode_attention(const pot_format* fmt, const float* q,
   a.app_tab = make_encode_tables(fmt->mant_bits);
   return decode_common(kScorePot, fmt->mant_bits, a, kv_head_of_q, B, Hq, Hkv, T, t_cap,
                        workspace, ws_bytes, dbg, stream);
+}
+
+pot_status pot_decode_attention_v8(const pot_format* fmt, int32_t engine, const float* q,
+                                   const uint8_t* codes_se, const uint8_t* codes_m,
+                                   const float* key_scale, const uint8_t* v_u8,
+                                   const int8_t* v_exp, int64_t t_cap,
+                                   const int32_t* kv_head_of_q, int32_t B, int32_t Hq,
+                                   int32_t Hkv, int32_t T, float* out, void* workspace,
+                                   size_t ws_bytes, pot_debug* dbg, void* stream) {
+  pot_status st = check_format(fmt);
+  if (st != POT_OK) return st;
+  if (engine != 0 && engine != 1)
+    return fail(POT_ERR_INVALID_ARG, "engine %d (0 shift-accumulate, 1 byte decode)", engine);
+  if (engine == 1 && fmt->mant_bits != 0)
+    return fail(POT_ERR_UNSUPPORTED, "the byte-decode path scores PoT-4 codes only (mant_bits 0)");
+  if (!codes_se || !key_scale) return fail(POT_ERR_INVALID_ARG, "codes_se or key_scale is NULL");
+  if ((fmt->mant_bits > 0) != (codes_m != nullptr))
+    return fail(POT_ERR_INVALID_ARG, "codes_m must be non-NULL exactly when mant_bits > 0");
+  if (!aligned(codes_se, 16) || !aligned(key_scale, 4) || (codes_m && !aligned(codes_m, 8)))
+    return fail(POT_ERR_INVALID_ARG, "misaligned codes_se / key_scale / codes_m");
+  DecodeArgs a{};
+  a.q = q;
+  a.codes_se = codes_se;
+  a.codes_m = codes_m;
+  a.key_scale = key_scale;
+  a.v8 = v_u8;
+  a.v_exp = v_exp;
+  a.out = out;
+  a.frac_bits = fmt->frac_bits;
+  a.hadamard = fmt->hadamard;
+  return decode_common(engine == 0 ? kScorePot : kScoreDs4a, fmt->mant_bits, a, kv_head_of_q, B,
+                       Hq, Hkv, T, t_cap, workspace, ws_bytes, dbg, stream, true);
 }
 
 pot_status pot_ds4a_decode_attention(const pot_format* fmt, const float* q,

@@ -199,8 +199,14 @@ struct KeyRegs<kScoreFp16, K> {
   uint4 k[8];
 };
 
+template <bool V8>
 struct ValRegs {
-  uint4 f[2][4];  // [K-block of 32 keys][16-dim block]
+  uint4 f[2][4];  // [K-block of 32 keys][16-dim block], 8 fp16 values each
+};
+template <>
+struct ValRegs<true> {
+  uint2 f[2][4];  // the same fragments as 8 value bytes (v^ + 128)
+  uint2 g;        // exponents g of the 8 keys whose weights this lane forms
 };
 
 // Loads are unconditional (addresses clamped into the valid range) so that
@@ -235,22 +241,52 @@ __device__ __forceinline__ void load_keys(const DecodeArgs& a, int64_t row, KeyR
 }
 
 // B fragments of one 64-key tile: lane l takes keys t0 + 32*kb + 8*(l/16) ..+7
-// of dim 16*nb + l%16, one 16-byte load each from the token-interleaved cache.
-// Groups past the range read the range's last group instead.
-__device__ __forceinline__ void load_values(const uint16_t* vseq, int t0, int g_last, int lane,
-                                            ValRegs& v) {
+// of dim 16*nb + l%16, one 16-byte (fp16) or 8-byte (INT8) load each from the
+// token-interleaved cache. Groups past the range read the range's last group
+// instead. With INT8 values the lane also loads the exponents of the 8 keys
+// t0 + 32*part + 8*grp ..+7 whose weights it forms in stage 2.
+// vseq: the sequence's first value (fp16 or byte); eseq: its first exponent.
+template <bool V8>
+__device__ __forceinline__ void load_values(const void* vseq, const int8_t* eseq, int t0,
+                                            int g_last, int lane, ValRegs<V8>& v) {
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) {
     const int g8 = min(t0 + 32 * kb + 8 * (lane >> 4), g_last);
-    const uint4* base = reinterpret_cast<const uint4*>(vseq + (int64_t)g8 * kDim);
+    if constexpr (V8) {
+      const uint2* base =
+          reinterpret_cast<const uint2*>(static_cast<const uint8_t*>(vseq) + (int64_t)g8 * kDim);
 #pragma unroll
-    for (int nb = 0; nb < 4; ++nb) v.f[kb][nb] = base[nb * 16 + (lane & 15)];
+      for (int nb = 0; nb < 4; ++nb) v.f[kb][nb] = base[nb * 16 + (lane & 15)];
+    } else {
+      const uint4* base = reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(vseq) +
+                                                         (int64_t)g8 * kDim);
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) v.f[kb][nb] = base[nb * 16 + (lane & 15)];
+    }
+  }
+  if constexpr (V8) {
+    const int part = (lane & 15) >> 3, grp = lane >> 4;
+    v.g = *reinterpret_cast<const uint2*>(eseq + min(t0 + 32 * part + 8 * grp, g_last));
   }
 }
 
+// fp16 B fragment of 8 INT8 values held as v^ + 128: bytes u become the fp16
+// numbers 1024 + u = 1152 + v^ (bit pattern 0x6400 | u, exact), two per
+// v_perm_b32; the 1152 offset is removed after accumulation with the weight
+// sums.
+__device__ __forceinline__ half8 int8_value_fragment(uint2 w) {
+  constexpr uint32_t kHi = 0x64646464u;
+  return __builtin_bit_cast(
+      half8, make_uint4(__builtin_amdgcn_perm(kHi, w.x, 0x04010400u),
+                        __builtin_amdgcn_perm(kHi, w.x, 0x04030402u),
+                        __builtin_amdgcn_perm(kHi, w.y, 0x04010400u),
+                        __builtin_amdgcn_perm(kHi, w.y, 0x04030402u)));
+}
+constexpr float kV8Offset = 1152.0f;
+
 // Zero the value fragments of tokens at or past t_end (tail tile only), so
 // that whatever the cache holds there cannot reach the sums (p is 0 there).
-__device__ __forceinline__ void mask_values(int t0, int t_end, int lane, ValRegs& v) {
+__device__ __forceinline__ void mask_values(int t0, int t_end, int lane, ValRegs<false>& v) {
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) {
     const int g8 = t0 + 32 * kb + 8 * (lane >> 4);
@@ -373,11 +409,13 @@ struct alignas(16) DecodeSmem {
   alignas(16) float x[kWaves][8][kXRow];  // transposed score tile per wave
   float wo[kWaves][16][kDim];             // per-wave P.V (rows: heads x {hi, lo})
   float wl[kWaves][16];
+  float wp[kWaves][64];  // INT8 values: per-lane sums of the unscaled weights
   int wm[kWaves][8];
+  int gm[kWaves];        // INT8 values: per-wave minimum exponent
   int last;
 };
 
-template <int MODE, int G, int K, bool DEBUG>
+template <int MODE, int G, int K, bool DEBUG, bool V8>
 // qbuf is passed on its own as a restrict parameter: the prepared query
 // operands are never written here, which lets the compiler read them through
 // the scalar cache even in the debug variants that store score taps.
@@ -395,7 +433,9 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
   const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int64_t seq = (int64_t)b * a.Hkv + kvh;
   const int64_t row0 = seq * a.t_cap;
-  const uint16_t* vseq = a.v + row0 * kDim;
+  const void* vseq = V8 ? static_cast<const void*>(a.v8 + row0 * kDim)
+                        : static_cast<const void*>(a.v + row0 * kDim);
+  const int8_t* eseq = V8 ? a.v_exp + row0 : nullptr;
   // query operands and score factors: uniform, read-only here -> scalar loads
   const int32_t* __restrict__ qb = qbuf + seq * a.qstride;
   const float* __restrict__ cb = reinterpret_cast<const float*>(qb + QL::kWords);
@@ -406,6 +446,29 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
   const int n_tiles = (t_end - t_begin + kWTile - 1) / kWTile;
   const int row = lane & 15, grp = lane >> 4, hrow = row & 7, part = row >> 3;
   const bool hvalid = hrow < G;
+
+  // INT8 values: the reference exponent g_ref = min g over this workgroup's
+  // keys (Sec. II-E eq. av). Weights are formed as p 2^(g_ref - g_j) <= p, so
+  // they stay in fp16 range for any g, and the sums are scaled by 2^-g_ref at
+  // the end (fp32).
+  int gref = 0;
+  if constexpr (V8) {
+    int gmin = INT_MAX;
+    for (int t = t_begin + 8 * tid; t < t_end; t += 8 * kBlock) {
+      const uint2 w = *reinterpret_cast<const uint2*>(eseq + t);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int gi = (int)(int8_t)(((i < 4) ? w.x : w.y) >> (8 * (i & 3)));
+        gmin = (t + i < t_end) ? min(gmin, gi) : gmin;
+      }
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) gmin = min(gmin, __shfl_xor(gmin, o, 64));
+    if (lane == 0) sm.gm[wave] = gmin;
+    __syncthreads();
+    gref = min(min(sm.gm[0], sm.gm[1]), min(sm.gm[2], sm.gm[3]));
+  }
+  float lsum = 0.0f;  // INT8 values: this lane's sum of the unscaled weights
 
   float4v acc[5];
 #pragma unroll
@@ -433,9 +496,9 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
   // the start of the tile; the short INT8 / fp16 scoring is not, so those
   // prefetch the values of this wave's next tile as well.
   constexpr bool kPrefetchV = MODE != kScorePot;
-  ValRegs vr[kPrefetchV ? 2 : 1];
+  ValRegs<V8> vr[kPrefetchV ? 2 : 1];
   if constexpr (kPrefetchV) {
-    if (j < n_tiles) load_values(vseq, t_begin + kWTile * j, g_last, lane, vr[0]);
+    if (j < n_tiles) load_values<V8>(vseq, eseq, t_begin + kWTile * j, g_last, lane, vr[0]);
   }
 
   // Stage 1 of a tile: issue the loads it still needs and those of this
@@ -443,15 +506,15 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
   // the tile's integer maximum per head (returned in m_new).
   float xv[8];
   int m_new = m_run;
-  auto stage1 = [&](const KeyRegs<MODE, K>& ks, KeyRegs<MODE, K>& knext, ValRegs& vs,
-                    ValRegs& vnext, int jt) {
+  auto stage1 = [&](const KeyRegs<MODE, K>& ks, KeyRegs<MODE, K>& knext, ValRegs<V8>& vs,
+                    ValRegs<V8>& vnext, int jt) {
     const int t0 = t_begin + kWTile * jt;
     const int jn = min(jt + kWaves, j_last);
     if constexpr (kPrefetchV) {
       load_keys_tile(jn, knext);
-      load_values(vseq, t_begin + kWTile * jn, g_last, lane, vnext);
+      load_values<V8>(vseq, eseq, t_begin + kWTile * jn, g_last, lane, vnext);
     } else {
-      load_values(vseq, t0, g_last, lane, vs);
+      load_values<V8>(vseq, eseq, t0, g_last, lane, vs);
       load_keys_tile(jn, knext);
     }
     const int t = t0 + lane;
@@ -668,7 +731,9 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
       const int k0 = t0 + 32 * part + 8 * grp;
 #pragma unroll
       for (int i = 0; i < 8; ++i) xv[i] = (k0 + i < t_end) ? xv[i] : -INFINITY;
-      mask_values(t0, t_end, lane, vs);
+      // weights past the range are 0; fp16 value bytes there could be inf or
+      // NaN and are cleared, INT8 value bytes are always finite numbers
+      if constexpr (!V8) mask_values(t0, t_end, lane, vs);
     }
 
     // ---- 3. integer running maximum per head ----
@@ -708,11 +773,12 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
                                                  0, 0, 0);
       acc[nb] = d;
     }
+    if constexpr (V8) lsum *= f;
     m_run = m_new;
   };
 
   // Stage 2 of a tile: weights from the scores and P.V on the matrix cores.
-  auto stage2 = [&](const ValRegs& vs) {
+  auto stage2 = [&](const ValRegs<V8>& vs) {
     // ---- 4. weights (fp16 high / low parts) and P.V on the matrix cores ----
     // Each lane splits its 8 weights into hi = rtz(p) and lo = rtz(p - hi)
     // and hands lo to its partner lane (row ^ 8). Block kb = 0 then takes
@@ -723,8 +789,16 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
     uint32_t hw[4], lw[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const float p0 = __builtin_amdgcn_exp2f(xv[2 * i] + bias);
-      const float p1 = __builtin_amdgcn_exp2f(xv[2 * i + 1] + bias);
+      float p0 = __builtin_amdgcn_exp2f(xv[2 * i] + bias);
+      float p1 = __builtin_amdgcn_exp2f(xv[2 * i + 1] + bias);
+      if constexpr (V8) {
+        // the softmax sum takes p; A.V takes p 2^(g_ref - g) (exact scaling)
+        lsum += p0;
+        lsum += p1;
+        const uint32_t gw = (i < 2) ? vs.g.x : vs.g.y;
+        p0 = __builtin_amdgcn_ldexpf(p0, gref - (int)(int8_t)(gw >> (16 * (i & 1))));
+        p1 = __builtin_amdgcn_ldexpf(p1, gref - (int)(int8_t)(gw >> (16 * (i & 1) + 8)));
+      }
       const half2v hi = __builtin_bit_cast(half2v, __builtin_amdgcn_cvt_pkrtz(p0, p1));
       hw[i] = __builtin_bit_cast(uint32_t, hi);
       lw[i] = __builtin_bit_cast(
@@ -740,15 +814,17 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
     }
     const half8 af0 = __builtin_bit_cast(half8, make_uint4(a0w[0], a0w[1], a0w[2], a0w[3]));
     const half8 af1 = __builtin_bit_cast(half8, make_uint4(a1w[0], a1w[1], a1w[2], a1w[3]));
+    auto bfrag = [&](int kb, int nb) -> half8 {
+      if constexpr (V8) return int8_value_fragment(vs.f[kb][nb]);
+      else return __builtin_bit_cast(half8, vs.f[kb][nb]);
+    };
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb)
-      acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-          af0, __builtin_bit_cast(half8, vs.f[0][nb]), acc[nb], 0, 0, 0);
+      acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af0, bfrag(0, nb), acc[nb], 0, 0, 0);
     acc[4] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af0, ones, acc[4], 0, 0, 0);
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb)
-      acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-          af1, __builtin_bit_cast(half8, vs.f[1][nb]), acc[nb], 0, 0, 0);
+      acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af1, bfrag(1, nb), acc[nb], 0, 0, 0);
     acc[4] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af1, ones, acc[4], 0, 0, 0);
   };
 
@@ -785,6 +861,7 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
     if (row == 0) sm.wl[wave][4 * grp + r] = acc[4][r];
   }
   if (lane < 8) sm.wm[wave][lane] = m_run;
+  if constexpr (V8) sm.wp[wave][lane] = lsum;
   __syncthreads();
 
   const int Sn = a.n_splits;
@@ -799,9 +876,22 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
     for (int w = 0; w < kWaves; ++w) {
       if (sm.wm[w][h] == INT_MIN) continue;
       const float f = __builtin_amdgcn_ldexpf(1.0f, sm.wm[w][h] - M);
-      o = fmaf(f, sm.wo[w][h][d] + sm.wo[w][h + 8][d], o);
-      l = fmaf(f, sm.wl[w][h] + sm.wl[w][h + 8], l);
+      if constexpr (V8) {
+        // numerator sum w (1152 + v^) minus 1152 sum w; denominator sum p over
+        // the 8 lanes that formed head h's weights
+        const float num = (sm.wo[w][h][d] + sm.wo[w][h + 8][d]) -
+                          kV8Offset * (sm.wl[w][h] + sm.wl[w][h + 8]);
+        float lw = 0.0f;
+#pragma unroll
+        for (int gq = 0; gq < 4; ++gq) lw += sm.wp[w][16 * gq + h] + sm.wp[w][16 * gq + h + 8];
+        o = fmaf(f, num, o);
+        l = fmaf(f, lw, l);
+      } else {
+        o = fmaf(f, sm.wo[w][h][d] + sm.wo[w][h + 8][d], o);
+        l = fmaf(f, sm.wl[w][h] + sm.wl[w][h + 8], l);
+      }
     }
+    if constexpr (V8) o = __builtin_amdgcn_ldexpf(o, -gref);
     if (Sn == 1) {
       a.out[bq * kDim + d] = o / l;
       if constexpr (DEBUG) {
@@ -847,14 +937,17 @@ __global__ __launch_bounds__(64) void combine_kernel(const DecodeArgs a) {
   }
 }
 
-template <int MODE, int G, int K, bool DEBUG>
+template <int MODE, int G, int K, bool DEBUG, bool V8>
 static hipError_t launch_t(const DecodeArgs& a, hipStream_t stream) {
+  if constexpr (V8 && MODE != kScorePot && MODE != kScoreDs4a) {
+    return hipErrorInvalidValue;
+  } else {
   hipLaunchKernelGGL((prep_queries_kernel<MODE, G, K, DEBUG>), dim3((uint32_t)a.Hkv, (uint32_t)a.B),
                      dim3(kBlock), 0, stream, a);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const dim3 grid((uint32_t)a.n_splits, (uint32_t)a.Hkv, (uint32_t)a.B);
-  hipLaunchKernelGGL((decode_kernel<MODE, G, K, DEBUG>), grid, dim3(kBlock), 0, stream, a,
+  hipLaunchKernelGGL((decode_kernel<MODE, G, K, DEBUG, V8>), grid, dim3(kBlock), 0, stream, a,
                      static_cast<const int32_t*>(a.qbuf));
   if (a.n_splits == 1) return hipGetLastError();
   const hipError_t e2 = hipGetLastError();
@@ -862,30 +955,34 @@ static hipError_t launch_t(const DecodeArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL((combine_kernel<DEBUG>), dim3((uint32_t)(a.B * a.Hq)), dim3(64), 0, stream,
                      a);
   return hipGetLastError();
+  }
 }
 
-template <int MODE, int G, int K>
+template <int MODE, int G, int K, bool V8>
 static int occupancy_t() {
   int n = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
-          &n, reinterpret_cast<const void*>(&decode_kernel<MODE, G, K, false>), kBlock, 0) !=
+          &n, reinterpret_cast<const void*>(&decode_kernel<MODE, G, K, false, V8>), kBlock, 0) !=
       hipSuccess)
     return 0;
   return n;
 }
 
-int decode_occupancy(int mode, int G, int mant_bits) {
+template <bool V8>
+static int occupancy_v(int mode, int G, int mant_bits) {
   auto by_k = [&](auto g_tag) -> int {
     constexpr int GG = decltype(g_tag)::value;
-    if (mode == kScoreInt8) return occupancy_t<kScoreInt8, GG, 0>();
-    if (mode == kScoreDs4a) return occupancy_t<kScoreDs4a, GG, 0>();
-    if (mode == kScoreFp16) return occupancy_t<kScoreFp16, GG, 0>();
+    if (mode == kScoreDs4a) return occupancy_t<kScoreDs4a, GG, 0, V8>();
+    if constexpr (!V8) {
+      if (mode == kScoreInt8) return occupancy_t<kScoreInt8, GG, 0, false>();
+      if (mode == kScoreFp16) return occupancy_t<kScoreFp16, GG, 0, false>();
+    }
     switch (mant_bits) {
-      case 0: return occupancy_t<kScorePot, GG, 0>();
-      case 1: return occupancy_t<kScorePot, GG, 1>();
-      case 2: return occupancy_t<kScorePot, GG, 2>();
-      case 3: return occupancy_t<kScorePot, GG, 3>();
-      default: return occupancy_t<kScorePot, GG, 4>();
+      case 0: return occupancy_t<kScorePot, GG, 0, V8>();
+      case 1: return occupancy_t<kScorePot, GG, 1, V8>();
+      case 2: return occupancy_t<kScorePot, GG, 2, V8>();
+      case 3: return occupancy_t<kScorePot, GG, 3, V8>();
+      default: return occupancy_t<kScorePot, GG, 4, V8>();
     }
   };
   switch (G) {
@@ -896,50 +993,64 @@ int decode_occupancy(int mode, int G, int mant_bits) {
   }
 }
 
-template <int MODE, int G, bool DEBUG>
+int decode_occupancy(int mode, int G, int mant_bits, bool v8) {
+  return v8 ? occupancy_v<true>(mode, G, mant_bits) : occupancy_v<false>(mode, G, mant_bits);
+}
+
+template <int MODE, int G, bool DEBUG, bool V8>
 static hipError_t launch_k(int mant_bits, const DecodeArgs& a, hipStream_t stream) {
   if constexpr (MODE != kScorePot) {
-    return launch_t<MODE, G, 0, DEBUG>(a, stream);
+    return launch_t<MODE, G, 0, DEBUG, V8>(a, stream);
   } else {
     switch (mant_bits) {
-      case 0: return launch_t<MODE, G, 0, DEBUG>(a, stream);
-      case 1: return launch_t<MODE, G, 1, DEBUG>(a, stream);
-      case 2: return launch_t<MODE, G, 2, DEBUG>(a, stream);
-      case 3: return launch_t<MODE, G, 3, DEBUG>(a, stream);
-      case 4: return launch_t<MODE, G, 4, DEBUG>(a, stream);
+      case 0: return launch_t<MODE, G, 0, DEBUG, V8>(a, stream);
+      case 1: return launch_t<MODE, G, 1, DEBUG, V8>(a, stream);
+      case 2: return launch_t<MODE, G, 2, DEBUG, V8>(a, stream);
+      case 3: return launch_t<MODE, G, 3, DEBUG, V8>(a, stream);
+      case 4: return launch_t<MODE, G, 4, DEBUG, V8>(a, stream);
       default: return hipErrorInvalidValue;
     }
   }
 }
 
-template <int MODE, bool DEBUG>
+template <int MODE, bool DEBUG, bool V8>
 static hipError_t launch_g(int G, int mant_bits, const DecodeArgs& a, hipStream_t stream) {
   switch (G) {
-    case 1: return launch_k<MODE, 1, DEBUG>(mant_bits, a, stream);
-    case 2: return launch_k<MODE, 2, DEBUG>(mant_bits, a, stream);
-    case 4: return launch_k<MODE, 4, DEBUG>(mant_bits, a, stream);
-    case 8: return launch_k<MODE, 8, DEBUG>(mant_bits, a, stream);
+    case 1: return launch_k<MODE, 1, DEBUG, V8>(mant_bits, a, stream);
+    case 2: return launch_k<MODE, 2, DEBUG, V8>(mant_bits, a, stream);
+    case 4: return launch_k<MODE, 4, DEBUG, V8>(mant_bits, a, stream);
+    case 8: return launch_k<MODE, 8, DEBUG, V8>(mant_bits, a, stream);
     default: return hipErrorInvalidValue;
   }
 }
 
-hipError_t launch_decode(int mode, int G, int mant_bits, bool debug, const DecodeArgs& a,
-                         hipStream_t stream) {
+template <bool V8>
+static hipError_t launch_v(int mode, int G, int mant_bits, bool debug, const DecodeArgs& a,
+                           hipStream_t stream) {
   switch (mode) {
     case kScorePot:
-      return debug ? launch_g<kScorePot, true>(G, mant_bits, a, stream)
-                   : launch_g<kScorePot, false>(G, mant_bits, a, stream);
-    case kScoreInt8:
-      return debug ? launch_g<kScoreInt8, true>(G, 0, a, stream)
-                   : launch_g<kScoreInt8, false>(G, 0, a, stream);
+      return debug ? launch_g<kScorePot, true, V8>(G, mant_bits, a, stream)
+                   : launch_g<kScorePot, false, V8>(G, mant_bits, a, stream);
     case kScoreDs4a:
-      return debug ? launch_g<kScoreDs4a, true>(G, 0, a, stream)
-                   : launch_g<kScoreDs4a, false>(G, 0, a, stream);
+      return debug ? launch_g<kScoreDs4a, true, V8>(G, 0, a, stream)
+                   : launch_g<kScoreDs4a, false, V8>(G, 0, a, stream);
+    case kScoreInt8:
+      if constexpr (V8) return hipErrorInvalidValue;
+      else
+        return debug ? launch_g<kScoreInt8, true, false>(G, 0, a, stream)
+                     : launch_g<kScoreInt8, false, false>(G, 0, a, stream);
     case kScoreFp16:
-      return launch_g<kScoreFp16, false>(G, 0, a, stream);
+      if constexpr (V8) return hipErrorInvalidValue;
+      else return launch_g<kScoreFp16, false, false>(G, 0, a, stream);
     default:
       return hipErrorInvalidValue;
   }
+}
+
+hipError_t launch_decode(int mode, int G, int mant_bits, bool debug, bool v8,
+                         const DecodeArgs& a, hipStream_t stream) {
+  return v8 ? launch_v<true>(mode, G, mant_bits, debug, a, stream)
+            : launch_v<false>(mode, G, mant_bits, debug, a, stream);
 }
 
 }  // namespace potattn

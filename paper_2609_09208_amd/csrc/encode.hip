@@ -120,6 +120,28 @@ hipError_t launch_store_values(const uint16_t* src, int64_t n_seq, int64_t n_tok
   return hipGetLastError();
 }
 
+// One wave per (sequence, token): INT8 quantisation with a power-of-two
+// scale and the byte store (Sec. II-E).
+__global__ __launch_bounds__(kBlock) void store_values_i8_kernel(
+    const uint16_t* __restrict__ src, int64_t n_seq, int64_t n_tok, int64_t t_cap, int64_t t0,
+    uint8_t* __restrict__ v_u8, int8_t* __restrict__ v_exp) {
+  const int64_t r = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
+  if (r >= n_seq * n_tok) return;  // uniform per wave
+  const int64_t s = r / n_tok, t = t0 + r % n_tok;
+  store_value_token_i8_wave(src + r * kDim, v_u8 + s * t_cap * kDim, v_exp + s * t_cap, t);
+}
+
+hipError_t launch_store_values_i8(const uint16_t* src, int64_t n_seq, int64_t n_tok,
+                                  int64_t t_cap, int64_t t0, uint8_t* v_u8, int8_t* v_exp,
+                                  hipStream_t stream) {
+  if (n_seq == 0 || n_tok == 0) return hipSuccess;
+  const int64_t rows = n_seq * n_tok;
+  const int64_t grid = (rows + kBlock / 64 - 1) / (kBlock / 64);
+  hipLaunchKernelGGL(store_values_i8_kernel, dim3((uint32_t)grid), dim3(kBlock), 0, stream, src,
+                     n_seq, n_tok, t_cap, t0, v_u8, v_exp);
+  return hipGetLastError();
+}
+
 __global__ void fill_zero_kernel(uint32_t* __restrict__ p, size_t n_words, uint8_t* tail,
                                  size_t tail_bytes) {
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;

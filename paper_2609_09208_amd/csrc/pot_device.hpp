@@ -145,4 +145,29 @@ __device__ __forceinline__ void store_value_token_wave(const uint16_t* __restric
   v_seq[(t / 8) * 8 * kDim + lane * 8 + t % 8] = v_row[lane];
 }
 
+// INT8 values with a power-of-two per-token scale (Sec. II-E) for one token,
+// quantised and stored by the calling wave (lane = dim): g is the largest
+// integer with max|v| 2^g <= 127 (0 for an all-zero row) and v^ = rne(v 2^g),
+// so |v^| <= 127. The byte cache holds v^ + 128 (offset binary) at the
+// token-interleaved position ((t/8)*8) * 64 + d * 8 + t % 8 of the sequence,
+// and exp_seq[t] = g; the value is v^ 2^-g.
+__device__ __forceinline__ void store_value_token_i8_wave(const uint16_t* __restrict__ v_row,
+                                                          uint8_t* __restrict__ v_seq,
+                                                          int8_t* __restrict__ exp_seq,
+                                                          int64_t t) {
+  const int lane = lane_id();
+  const float v = __half2float(__ushort_as_half(v_row[lane]));
+  const float amax = wave_max(fabsf(v));
+  int g = 0;
+  if (amax > 0.0f) {
+    // amax in [2^e, 2^(e+1)) with e = frexp exponent - 1, so amax 2^(6-e) is
+    // in [64, 128) (exact power-of-two scaling)
+    const int e = __builtin_amdgcn_frexp_expf(amax) - 1;
+    g = (__builtin_amdgcn_ldexpf(amax, 6 - e) <= 127.0f) ? 6 - e : 5 - e;
+  }
+  const int c = (int)rintf(__builtin_amdgcn_ldexpf(v, g));
+  v_seq[(t / 8) * 8 * kDim + lane * 8 + t % 8] = (uint8_t)(c + 128);
+  if (lane == 0) exp_seq[t] = (int8_t)g;
+}
+
 }  // namespace potattn

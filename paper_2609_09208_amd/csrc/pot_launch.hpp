@@ -35,6 +35,12 @@ hipError_t launch_encode_int8(const uint16_t* k, int64_t n_rows, int64_t out_str
 hipError_t launch_store_values(const uint16_t* src, int64_t n_seq, int64_t n_tok, int64_t t_cap,
                                int64_t t0, uint16_t* dst, hipStream_t stream);
 
+// INT8 values with a power-of-two per-token scale: v_u8 holds v^ + 128
+// token-interleaved like the fp16 cache, v_exp one g per cache row.
+hipError_t launch_store_values_i8(const uint16_t* src, int64_t n_seq, int64_t n_tok,
+                                  int64_t t_cap, int64_t t0, uint8_t* v_u8, int8_t* v_exp,
+                                  hipStream_t stream);
+
 hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream);
 
 // kScoreDs4a: PoT-4 codes decoded to int8 bytes and scored by v_dot4 (a
@@ -49,7 +55,9 @@ struct DecodeArgs {
   const int8_t* codes_i8;    // INT8 keys
   const uint16_t* k_f16;     // fp16 keys
   const float* key_scale;
-  const uint16_t* v;
+  const uint16_t* v;         // fp16 value cache, or
+  const uint8_t* v8;         // INT8 value cache (v^ + 128) with
+  const int8_t* v_exp;       // one exponent g per row: value v^ 2^-g
   float* out;
   // workspace
   int32_t* qbuf;             // [B*Hkv][qstride]: prepared query operands per kv head
@@ -87,9 +95,11 @@ constexpr int query_words(int G) { return ((5 * 64 + 1) * G + 63) / 64 * 64; }
 
 // Resident workgroups per CU of the (non-debug) decode kernel for this
 // variant, from the HIP occupancy calculator; 0 if the query fails.
-int decode_occupancy(int mode, int G, int mant_bits);
+int decode_occupancy(int mode, int G, int mant_bits, bool v8);
 
-hipError_t launch_decode(int mode, int G, int mant_bits, bool debug,
+// v8: INT8 value cache (a.v8, a.v_exp) instead of fp16 (a.v); score modes
+// kScorePot and kScoreDs4a only.
+hipError_t launch_decode(int mode, int G, int mant_bits, bool debug, bool v8,
                          const DecodeArgs& a, hipStream_t stream);
 
 }  // namespace potattn

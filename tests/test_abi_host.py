@@ -207,3 +207,30 @@ def test_append_rejects_bad_arguments():
     assert D(*args(T=4097)) == pa.POT_ERR_INVALID_ARG  # beyond t_cap
     assert D(*args(t_cap=4100, T=4097)) == pa.POT_ERR_INVALID_ARG  # t_cap not a multiple of 8
     assert D(*args(ws=16)) == pa.POT_ERR_WORKSPACE
+
+
+def test_int8_values_reject_bad_arguments():
+    S = pa._lib.pot_store_values_int8
+    assert S(FAKE, 1, 1, 12, 0, FAKE, FAKE, None) == pa.POT_ERR_INVALID_ARG   # t_cap % 8
+    assert S(FAKE, 1, 2, 8, 7, FAKE, FAKE, None) == pa.POT_ERR_INVALID_ARG    # past t_cap
+    assert S(FAKE, -1, 1, 8, 0, FAKE, FAKE, None) == pa.POT_ERR_INVALID_ARG
+    assert S(FAKE, 1, 1, 8, 0, FAKE, None, None) == pa.POT_ERR_INVALID_ARG
+    assert S(FAKE, 1, 1, 8, 0, FAKE + 8, FAKE, None) == pa.POT_ERR_INVALID_ARG
+    assert S(None, 0, 1, 8, 0, None, None, None) == pa.POT_OK                 # empty: no-op
+    hm = (np.arange(32, dtype=np.int32) // 8)
+    hp = hm.ctypes.data_as(ctypes.c_void_p)
+    D = pa._lib.pot_decode_attention_v8
+
+    def args(fmt=None, engine=0, vu=FAKE, ve=FAKE, T=4096, ws=1 << 30):
+        fmt = fmt if fmt is not None else pa.make_format()
+        return (ctypes.byref(fmt), engine, FAKE, FAKE, None, FAKE, vu, ve, 4096, hp, 1, 32, 4,
+                T, FAKE, FAKE, ws, None, None)
+    assert D(*args(engine=2)) == pa.POT_ERR_INVALID_ARG
+    assert D(*args(engine=-1)) == pa.POT_ERR_INVALID_ARG
+    assert D(*args(vu=None)) == pa.POT_ERR_INVALID_ARG
+    assert D(*args(ve=None)) == pa.POT_ERR_INVALID_ARG
+    assert D(*args(ve=FAKE + 4)) == pa.POT_ERR_INVALID_ARG
+    assert D(*args(T=0)) == pa.POT_ERR_INVALID_ARG
+    assert D(*args(ws=16)) == pa.POT_ERR_WORKSPACE
+    # byte-decode engine: PoT-4 only
+    assert D(*args(fmt=pa.make_format(mant_bits=1), engine=1)) == pa.POT_ERR_UNSUPPORTED
