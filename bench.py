@@ -52,6 +52,11 @@ def row_bytes(mant_bits: int) -> int:
     return 32 + 8 * mant_bits + 4 + 2 * D
 
 
+def row_bytes_v8(mant_bits: int) -> int:
+    """The same with INT8 values: 64 value bytes + 1 exponent byte."""
+    return 32 + 8 * mant_bits + 4 + D + 1
+
+
 def algorithmic_bytes(B: int, T: int, per_row: int) -> int:
     return B * HKV * T * per_row + B * HQ * D * 4 * 2  # + q in, O out
 
@@ -178,6 +183,7 @@ class Layers:
                        new_v=d["v"][:, :, T - 1].contiguous(), **cache)
             if layer < keep_k16:
                 rec["k16"] = d["k"] if distinct else d["k"].clone()
+                rec["v16"] = d["v"] if distinct else d["v"].clone()
             self.layers.append(rec)
             del d
         del shared
@@ -250,6 +256,12 @@ def comparators(pa, lay, dev):
     had = int(lay.fmt.hadamard)
     for c, x in zip(cl, i8):
         pa.pot_int8_encode_keys(c["k16"], n8, 1, had, x["sc"], x["codes"])
+    # the paper's value cache: INT8 with a power-of-two per-token scale
+    v8 = []
+    for c in cl:
+        vu, ve = pa.alloc_value_cache_int8(B, HKV, T, dev)
+        pa.pot_store_values_int8(c["v16"], B * HKV, T, T, 0, vu, ve)
+        v8.append((vu, ve))
     out, ws, heads = lay.out, lay.ws, lay.heads
     engines = {
         "pot": lambda i: lay.decode(cl[i]),
@@ -259,10 +271,16 @@ def comparators(pa, lay, dev):
             cl[i]["q"], i8[i]["codes"], i8[i]["sc"], cl[i]["v"], T, heads, B, HQ, HKV, T, had,
             out, ws),
     }
+    engines["pot_v8"] = lambda i: pa.pot_decode_attention_v8(
+        lay.fmt, 0, cl[i]["q"], cl[i]["codes_se"], cl[i]["codes_m"], cl[i]["key_scale"],
+        v8[i][0], v8[i][1], T, heads, B, HQ, HKV, T, out, ws)
     if lay.k == 0:  # byte decode + v_dot4 on the same PoT-4 caches (a multiply path)
         engines["ds4a"] = lambda i: pa.pot_ds4a_decode_attention(
             lay.fmt, cl[i]["q"], cl[i]["codes_se"], cl[i]["key_scale"], cl[i]["v"], T, heads,
             B, HQ, HKV, T, out, ws)
+        engines["ds4a_v8"] = lambda i: pa.pot_decode_attention_v8(
+            lay.fmt, 1, cl[i]["q"], cl[i]["codes_se"], None, cl[i]["key_scale"], v8[i][0],
+            v8[i][1], T, heads, B, HQ, HKV, T, out, ws)
     # interleaved rounds, each engine warmed before it is timed; median per engine
     runs = {name: [] for name in engines}
     for _ in range(COMPARE_ROUNDS):
@@ -270,6 +288,7 @@ def comparators(pa, lay, dev):
             runs[name].append(timed_calls(fn, len(cl), reps=10, warm=4))
     med = {name: float(sorted(v)[len(v) // 2]) for name, v in runs.items()}
     pot_us, f16_us, i8_us, ds4a_us = med["pot"], med["fp16"], med["int8"], med.get("ds4a")
+    pv8_us, dv8_us = med["pot_v8"], med.get("ds4a_v8")
 
     def frac(per_row, us):
         return algorithmic_bytes(B, T, per_row) / (us * 1e-6) / 1e9 / HBM_PEAK_GBS
@@ -283,6 +302,15 @@ def comparators(pa, lay, dev):
             "ds4a_speedup_vs_fp16": f16_us / ds4a_us if ds4a_us else None,
             "ds4a_note": "PoT-4 codes decoded to int8 bytes by v_perm and scored by v_dot4 "
                          "(software packed shift-dot, a multiply path)",
+            "int8_values": {
+                "bytes_per_row": row_bytes_v8(lay.k),
+                "pot_us_per_layer": pv8_us,
+                "pot_hbm_frac": frac(row_bytes_v8(lay.k), pv8_us),
+                "pot_speedup_vs_fp16": f16_us / pv8_us,
+                "ds4a_us_per_layer": dv8_us,
+                "ds4a_hbm_frac": frac(row_bytes_v8(0), dv8_us) if dv8_us else None,
+                "ds4a_speedup_vs_fp16": f16_us / dv8_us if dv8_us else None,
+                "note": "INT8 values with a power-of-two per-token scale (pot_store_values_int8)"},
             "timing": f"median of {COMPARE_ROUNDS} interleaved rounds of 10 passes over the "
                       f"{len(cl)} layers per engine"}
 
