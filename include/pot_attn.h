@@ -274,6 +274,22 @@ pot_status pot_decode_attention_v8(const pot_format* fmt, int32_t engine, const 
                                    int32_t Hkv, int32_t T, float* out, void* workspace,
                                    size_t ws_bytes, pot_debug* dbg, void* stream);
 
+/* pot_append_decode_attention on a cache with INT8 values: the new token's
+ * values are quantised as by pot_store_values_int8 and stored with their
+ * exponent at position T - 1, then pot_decode_attention_v8 runs with the
+ * given engine over T keys, in one call (the cache holds only codes: 32 + 4 +
+ * 65 bytes per PoT-4 key). Arguments and errors as the two calls it
+ * combines. */
+pot_status pot_append_decode_attention_v8(const pot_format* fmt, int32_t engine,
+                                          const float* q, const uint16_t* k_new,
+                                          const uint16_t* v_new, uint8_t* codes_se,
+                                          uint8_t* codes_m, float* key_scale,
+                                          uint8_t* v_u8, int8_t* v_exp, int64_t t_cap,
+                                          const int32_t* kv_head_of_q, int32_t B,
+                                          int32_t Hq, int32_t Hkv, int32_t T, float* out,
+                                          void* workspace, size_t ws_bytes,
+                                          pot_debug* dbg, void* stream);
+
 /* ---- comparison paths on the same cache skeleton --------------------- */
 
 /* INT8 uniform key codes (the multiply-accumulate comparator of Sec. III and

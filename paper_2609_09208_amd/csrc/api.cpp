@@ -432,6 +432,50 @@ pot_status pot_decode_attention_v8(const pot_format* fmt, int32_t engine, const 
                        Hq, Hkv, T, t_cap, workspace, ws_bytes, dbg, stream, true);
 }
 
+pot_status pot_append_decode_attention_v8(const pot_format* fmt, int32_t engine,
+                                          const float* q, const uint16_t* k_new,
+                                          const uint16_t* v_new, uint8_t* codes_se,
+                                          uint8_t* codes_m, float* key_scale, uint8_t* v_u8,
+                                          int8_t* v_exp, int64_t t_cap,
+                                          const int32_t* kv_head_of_q, int32_t B, int32_t Hq,
+                                          int32_t Hkv, int32_t T, float* out, void* workspace,
+                                          size_t ws_bytes, pot_debug* dbg, void* stream) {
+  pot_status st = check_format(fmt);
+  if (st != POT_OK) return st;
+  if (engine != 0 && engine != 1)
+    return fail(POT_ERR_INVALID_ARG, "engine %d (0 shift-accumulate, 1 byte decode)", engine);
+  if (engine == 1 && fmt->mant_bits != 0)
+    return fail(POT_ERR_UNSUPPORTED, "the byte-decode path scores PoT-4 codes only (mant_bits 0)");
+  if (!k_new || !v_new) return fail(POT_ERR_INVALID_ARG, "k_new or v_new is NULL");
+  if (!aligned(k_new, 16) || !aligned(v_new, 16))
+    return fail(POT_ERR_INVALID_ARG, "k_new and v_new must be 16-byte aligned");
+  if (!codes_se || !key_scale) return fail(POT_ERR_INVALID_ARG, "codes_se or key_scale is NULL");
+  if ((fmt->mant_bits > 0) != (codes_m != nullptr))
+    return fail(POT_ERR_INVALID_ARG, "codes_m must be non-NULL exactly when mant_bits > 0");
+  if (!aligned(codes_se, 16) || !aligned(key_scale, 4) || (codes_m && !aligned(codes_m, 8)))
+    return fail(POT_ERR_INVALID_ARG, "misaligned codes_se / key_scale / codes_m");
+  DecodeArgs a{};
+  a.q = q;
+  a.codes_se = codes_se;
+  a.codes_m = codes_m;
+  a.key_scale = key_scale;
+  a.v8 = v_u8;
+  a.v_exp = v_exp;
+  a.out = out;
+  a.frac_bits = fmt->frac_bits;
+  a.hadamard = fmt->hadamard;
+  a.app_k = k_new;
+  a.app_v = v_new;
+  a.app_codes_se = codes_se;
+  a.app_codes_m = codes_m;
+  a.app_key_scale = key_scale;
+  a.app_v8 = v_u8;
+  a.app_v_exp = v_exp;
+  a.app_tab = make_encode_tables(fmt->mant_bits);
+  return decode_common(engine == 0 ? kScorePot : kScoreDs4a, fmt->mant_bits, a, kv_head_of_q, B,
+                       Hq, Hkv, T, t_cap, workspace, ws_bytes, dbg, stream, true);
+}
+
 pot_status pot_ds4a_decode_attention(const pot_format* fmt, const float* q,
                                      const uint8_t* codes_se, const float* key_scale,
                                      const uint16_t* v_cache, int64_t t_cap,

@@ -331,15 +331,19 @@ __global__ __launch_bounds__(kBlock) void prep_queries_kernel(const DecodeArgs a
   const int64_t seq = (int64_t)b * a.Hkv + kvh;
   int32_t* qb = a.qbuf + seq * a.qstride;
   float* cb = reinterpret_cast<float*>(qb + QL::kWords);
-  if constexpr (MODE == kScorePot) {
+  if constexpr (MODE == kScorePot || MODE == kScoreDs4a) {
     // fused append of this sequence's new token at row T - 1: wave 0 encodes
-    // the key (row absmax scale), wave 1 stores the values
+    // the key (row absmax scale), wave 1 stores the values (fp16, or INT8
+    // with their exponent)
     if (a.app_k != nullptr) {
       const int64_t row = seq * a.t_cap + (a.T - 1);
       if (wave == 0)
         encode_key_row_wave(reinterpret_cast<const __half*>(a.app_k) + seq * kDim, a.hadamard, 0,
                             a.app_key_scale + row, a.app_codes_se + row * (kDim / 2),
                             a.app_codes_m + row * 8 * K, a.app_tab);
+      else if (wave == 1 && a.app_v8 != nullptr)
+        store_value_token_i8_wave(a.app_v + seq * kDim, a.app_v8 + seq * a.t_cap * kDim,
+                                  a.app_v_exp + seq * a.t_cap, a.T - 1);
       else if (wave == 1)
         store_value_token_wave(a.app_v + seq * kDim, a.app_v_cache + seq * a.t_cap * kDim,
                                a.T - 1);

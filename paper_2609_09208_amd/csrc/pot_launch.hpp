@@ -79,7 +79,9 @@ struct DecodeArgs {
   uint8_t* app_codes_se;     // the cache arrays, written at row T - 1 only
   uint8_t* app_codes_m;
   float* app_key_scale;
-  uint16_t* app_v_cache;
+  uint16_t* app_v_cache;     // fp16 value cache, or
+  uint8_t* app_v8;           // INT8 value cache and
+  int8_t* app_v_exp;         // its exponents
   EncodeTables app_tab;
   int64_t t_cap;
   int32_t B, Hq, Hkv, T;

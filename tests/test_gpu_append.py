@@ -216,3 +216,64 @@ def test_append_full_size_b64_t32768():
     new_rows = torch.arange(B * Hkv, device=DEV) * T + (T - 1)
     assert np.array_equal(fc["se"][new_rows].cpu().numpy(), o_se)
     assert np.array_equal(fc["sc"][new_rows].cpu().numpy().view(np.uint32), o_sc.view(np.uint32))
+
+
+@pytest.mark.parametrize("engine", [0, 1])
+@pytest.mark.parametrize("T,t_cap", [(1, 8), (777, 784), (4096, 4096)])
+def test_append_int8_values(engine, T, t_cap):
+    """The cache with INT8 values (the paper's code-only cache): the fused call
+    matches encode + pot_store_values_int8 + pot_decode_attention_v8 bit for
+    bit, and the oracle on the unpoisoned block."""
+    import oracle
+    B, Hq, Hkv = 2, 32, 4
+    d = make_decode_inputs(600 + T + engine, B=B, Hq=Hq, Hkv=Hkv, T=T, t_cap=t_cap)
+    fmt = pa.make_format(0, 7, False)
+    k_init, v_init = d["k_bits"].copy(), d["v_bits"].copy()
+    k_init[:, :, T - 1] = np.float16(POISON_K).view(np.uint16)
+    v_init[:, :, T - 1] = np.float16(POISON_V).view(np.uint16)
+    base = _cache(k_init, v_init, B, Hkv, t_cap, fmt, 0)
+    vu, ve = pa.alloc_value_cache_int8(B, Hkv, t_cap, DEV)
+    src = to_dev(np.ascontiguousarray(v_init).reshape(B * Hkv, t_cap, 64)).view(torch.float16)
+    pa.pot_store_values_int8(src, B * Hkv, t_cap, t_cap, 0, vu, ve)
+    base = dict(se=base["se"], sc=base["sc"], vu=vu, ve=ve)
+    k_new = to_dev(np.ascontiguousarray(d["k_bits"][:, :, T - 1])).view(torch.float16)
+    v_new = to_dev(np.ascontiguousarray(d["v_bits"][:, :, T - 1])).view(torch.float16)
+    q = to_dev(d["q"])
+    ws_bytes = pa.pot_decode_workspace_bytes(B, Hq, Hkv, T)
+    results = []
+    for path in ("fused", "separate"):
+        c = {k: t.clone() for k, t in base.items()}
+        out = torch.empty((B, Hq, 64), dtype=torch.float32, device=DEV)
+        ws = pa.alloc_workspace(ws_bytes, DEV)
+        dbg, bufs = _taps(B, Hq, T)
+        if path == "fused":
+            pa.pot_append_decode_attention_v8(fmt, engine, q, k_new, v_new, c["se"], None,
+                                              c["sc"], c["vu"], c["ve"], t_cap,
+                                              d["kv_head_of_q"], B, Hq, Hkv, T, out, ws, dbg=dbg)
+        else:
+            pos = T - 1
+            pa.pot_encode_keys(fmt, k_new, B * Hkv, t_cap, 0, c["sc"][pos:], c["se"][pos:], None)
+            pa.pot_store_values_int8(v_new, B * Hkv, 1, t_cap, pos, c["vu"], c["ve"])
+            pa.pot_decode_attention_v8(fmt, engine, q, c["se"], None, c["sc"], c["vu"], c["ve"],
+                                       t_cap, d["kv_head_of_q"], B, Hq, Hkv, T, out, ws, dbg=dbg)
+        torch.cuda.synchronize()
+        results.append((c, out, bufs, dbg))
+    (fc, fo, fb, fd), (sc_, so, sb, _) = results
+    for k in fc:
+        assert torch.equal(fc[k].view(torch.uint8), sc_[k].view(torch.uint8)), f"cache {k}"
+    assert torch.equal(fo.view(torch.int32), so.view(torch.int32)), "out differs from 3 calls"
+    for k in fb:
+        assert torch.equal(fb[k], sb[k]), f"tap {k}"
+    o_se, _, o_sc = oracle.encode_keys(d["k_bits"].reshape(-1, 64))
+    o_vh, o_g = oracle.quantize_values(d["v_bits"].reshape(-1, 64))
+    live = np.zeros((B, Hkv, t_cap), bool)
+    live[:, :, :T] = True
+    live = live.reshape(-1)
+    assert np.array_equal(fc["se"].cpu().numpy()[live], o_se[live])
+    assert np.array_equal(fc["ve"].cpu().numpy().reshape(-1)[live], o_g[live])
+    o = oracle.pot_decode_v8(d["q"], o_se, None, o_sc, o_vh, o_g, t_cap, d["kv_head_of_q"], B,
+                             Hq, Hkv, T, split_len=fd.split_len)
+    assert np.array_equal(fb["scores"].cpu().numpy(), o["scores"])
+    assert np.array_equal(fb["m_final"].cpu().numpy(), o["m_final"])
+    err = float(np.abs(fo.cpu().numpy() - o["out"]).max())
+    assert err <= O_TOL, err
