@@ -208,8 +208,10 @@ pot_status pot_workspace_init(void* workspace, size_t ws_bytes, void* stream);
  *               aligned. Calls that share a workspace must not overlap in
  *               time.
  * Steps: q is rotated (if hadamard) and quantised to int8 with step
- * Delta = amax/127; each score is the exact int32 sum of sign-flipped left
- * shifts of q^ (eq. sac); x = acc * s * Delta * log2(e) * 2^-(F+k) / 8 in a
+ * Delta = amax/127; each score is the exact int32 sum of sign-flipped
+ * shifts of q^ (eq. sac: q^ 2^(F-e), for PoT-4 formed by packed 16-bit shifts
+ * and summed with +-1 weights by v_dot2_i32_i16); x = acc * s * Delta *
+ * log2(e) * 2^-(F+k) / 8 in a
  * fixed fp32 order; the running maximum is the integer M = ceil(max x)
  * (eq. logsm) so rescales are exact powers of two; weights 2^(x-M) multiply
  * the fp16 values with fp32 accumulation (matrix cores, weights split into

@@ -10,20 +10,20 @@
 //
 // Per 64-key tile and wave:
 //  1. Scores, one key per lane (Sec. II-B eq. sac). PoT-4: the key's 32 code
-//     bytes arrive as two 16-byte loads. Two query heads share one 32-bit
-//     operand Q2 = 2 (q_a + 2^16 q_b), whose bit 0 is clear. Each code byte
-//     holds two exponents; one subtraction per code word turns four of them
-//     into shift bytes s = (6 - e) mod 32, and an SDWA v_lshlrev_b32 reads its
-//     shift straight from one byte: Q2 << (6 - e) = (q_a + 2^16 q_b) << (7 - e)
-//     for e <= 6, and Q2 << 31 = 0 for the zero code e = 7. Every shift is a
-//     left shift (eq. exact). v_xad_u32 applies the sign as (t ^ s) + acc with
-//     s in {0, -1}; the missing +1 per negative element is added once per key
-//     from a popcount of the sign bits. After every 2 elements the 16-bit
-//     fields (each at most 2 * 127 * 2^7 in magnitude, kept non-negative by a
-//     2^15 bias) are added into two int32 accumulators by SDWA word adds, so
-//     the sums stay exact. PoT-Mk and the single-head case use one int32
-//     accumulator per head and v_alignbit(q, 0, e + 25) = q << (7 - e) (0 for
-//     e = 7), one more per mantissa bit.
+//     bytes arrive as two 16-byte loads. Each query operand holds two
+//     elements of one head as 16-bit halves, (q + 128) 2^7 (prepared once per
+//     kv head, read through the scalar cache one code word's group at a
+//     time). v_pk_lshrrev_b16 shifts each half by its element's exponent e:
+//     (q + 128) 2^7 >> e = (q + 128) 2^(7 - e), exact since the low 7 bits
+//     are clear, so every product is formed by the shifter with head-room
+//     F_int = 7 >= e (eq. exact); the zero code gets the shift 15, which
+//     clears the operand. v_dot2_i32_i16 with weights sigma = +-1 flips the
+//     signs and adds both halves into the int32 sum (a signed add; no product
+//     q 2^k goes through a multiplier). A ninth column with q = 0 sums the
+//     +128 bias, 128 sigma 2^(7 - e), and is subtracted from every head.
+//     PoT-Mk uses one int32 accumulator per head: v_alignbit(q, 0, e + 25) =
+//     q << (7 - e) (0 for e = 7), one more per mantissa bit, and v_xad_u32
+//     for the sign (ones' complement, +1 per negative element from a popcount).
 //  2. x = fl32(fl32(float(acc) * s) * c), c = fl32(fl32(Delta * log2 e) *
 //     2^-(F+k+3)) in this order; x is staged transposed in wave-private LDS.
 //  3. Integer running maximum M = max(M, ceil(max x)) per head (eq. logsm);
@@ -51,6 +51,8 @@ namespace potattn {
 
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef _Float16 half2v __attribute__((ext_vector_type(2)));
+typedef short s16x2 __attribute__((ext_vector_type(2)));
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
 typedef float float4v __attribute__((ext_vector_type(4)));
 
 constexpr int kWaves = kBlock / 64;
@@ -65,109 +67,11 @@ __device__ __forceinline__ uint32_t xad_u32(uint32_t a, uint32_t b, uint32_t c) 
   asm("v_xad_u32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
   return r;
 }
-// acc + (p & 0xffff)
-__device__ __forceinline__ uint32_t add_lo16(uint32_t acc, uint32_t p) {
-  uint32_t r;
-  asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 "
-      "src1_sel:DWORD"
-      : "=v"(r)
-      : "v"(p), "v"(acc));
-  return r;
-}
-// acc + sign_extend(p >> 16)
-__device__ __forceinline__ uint32_t add_hi16s(uint32_t acc, uint32_t p) {
-  uint32_t r;
-  asm("v_add_u32_sdwa %0, sext(%1), %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_1 "
-      "src1_sel:DWORD"
-      : "=v"(r)
-      : "v"(p), "v"(acc));
-  return r;
-}
-
-// q << (byte BYTE of sh) (shift taken mod 32), with q a wave-uniform operand
-template <int BYTE>
-__device__ __forceinline__ uint32_t shl_by_byte(uint32_t sh, uint32_t q) {
-  uint32_t r;
-  if constexpr (BYTE == 0)
-    asm("v_lshlrev_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_0 "
-        "src1_sel:DWORD" : "=v"(r) : "v"(sh), "s"(q));
-  else if constexpr (BYTE == 1)
-    asm("v_lshlrev_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_1 "
-        "src1_sel:DWORD" : "=v"(r) : "v"(sh), "s"(q));
-  else if constexpr (BYTE == 2)
-    asm("v_lshlrev_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_2 "
-        "src1_sel:DWORD" : "=v"(r) : "v"(sh), "s"(q));
-  else
-    asm("v_lshlrev_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_3 "
-        "src1_sel:DWORD" : "=v"(r) : "v"(sh), "s"(q));
-  return r;
-}
-
 // max(a, b) for scores (never NaN) as v_max_f32 without operand canonicalisation
 __device__ __forceinline__ float max_f32(float a, float b) {
   return __builtin_amdgcn_fmed3f(a, b, __builtin_inff());
 }
 
-// One 2-element step of the packed PoT-4 score for four head pairs (G = 8),
-// as one block so that no wait states are padded between its instructions
-// (all of them are full-dword VALU ops without forwarding hazards):
-//   P_p = ((Q_{m,p} << s0) ^ g0) + 2^15;  P_p += (Q_{m+1,p} << s1) ^ g1;
-//   A_p += P_p & 0xffff;  B_p += sext(P_p >> 16)
-// with the shifts taken from byte JJ of s0 / s1.
-#define POT_STEP8_ASM(JJ)                                                                      \
-  "v_lshlrev_b32_sdwa %[p0], %[s0], %[a0] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_" #JJ \
-  " src1_sel:DWORD\n"                                                                          \
-  "v_lshlrev_b32_sdwa %[p1], %[s0], %[a1] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_" #JJ \
-  " src1_sel:DWORD\n"                                                                          \
-  "v_lshlrev_b32_sdwa %[p2], %[s0], %[a2] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_" #JJ \
-  " src1_sel:DWORD\n"                                                                          \
-  "v_lshlrev_b32_sdwa %[p3], %[s0], %[a3] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_" #JJ \
-  " src1_sel:DWORD\n"                                                                          \
-  "v_xad_u32 %[p0], %[p0], %[g0], %[bias]\n"                                                  \
-  "v_xad_u32 %[p1], %[p1], %[g0], %[bias]\n"                                                  \
-  "v_xad_u32 %[p2], %[p2], %[g0], %[bias]\n"                                                  \
-  "v_xad_u32 %[p3], %[p3], %[g0], %[bias]\n"                                                  \
-  "v_lshlrev_b32_sdwa %[t], %[s1], %[b0] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_" #JJ \
-  " src1_sel:DWORD\n"                                                                          \
-  "v_xad_u32 %[p0], %[t], %[g1], %[p0]\n"                                                     \
-  "v_lshlrev_b32_sdwa %[t], %[s1], %[b1] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_" #JJ \
-  " src1_sel:DWORD\n"                                                                          \
-  "v_xad_u32 %[p1], %[t], %[g1], %[p1]\n"                                                     \
-  "v_lshlrev_b32_sdwa %[t], %[s1], %[b2] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_" #JJ \
-  " src1_sel:DWORD\n"                                                                          \
-  "v_xad_u32 %[p2], %[t], %[g1], %[p2]\n"                                                     \
-  "v_lshlrev_b32_sdwa %[t], %[s1], %[b3] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_" #JJ \
-  " src1_sel:DWORD\n"                                                                          \
-  "v_xad_u32 %[p3], %[t], %[g1], %[p3]\n"                                                     \
-  "v_add_u32_sdwa %[A0], %[p0], %[A0] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 src1_sel:DWORD\n" \
-  "v_add_u32_sdwa %[B0], sext(%[p0]), %[B0] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_1 src1_sel:DWORD\n" \
-  "v_add_u32_sdwa %[A1], %[p1], %[A1] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 src1_sel:DWORD\n" \
-  "v_add_u32_sdwa %[B1], sext(%[p1]), %[B1] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_1 src1_sel:DWORD\n" \
-  "v_add_u32_sdwa %[A2], %[p2], %[A2] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 src1_sel:DWORD\n" \
-  "v_add_u32_sdwa %[B2], sext(%[p2]), %[B2] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_1 src1_sel:DWORD\n" \
-  "v_add_u32_sdwa %[A3], %[p3], %[A3] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 src1_sel:DWORD\n" \
-  "v_add_u32_sdwa %[B3], sext(%[p3]), %[B3] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_1 src1_sel:DWORD"
-
-template <int JJ>
-__device__ __forceinline__ void pot_step8(uint32_t s0, uint32_t s1, uint32_t g0, uint32_t g1,
-                                          const uint32_t* qm, uint32_t (&A)[4],
-                                          uint32_t (&B)[4]) {
-  uint32_t p0, p1, p2, p3, t;
-#define POT_STEP8_OPERANDS                                                                   \
-  : [p0] "=&v"(p0), [p1] "=&v"(p1), [p2] "=&v"(p2), [p3] "=&v"(p3), [t] "=&v"(t),          \
-    [A0] "+v"(A[0]), [A1] "+v"(A[1]),                                                        \
-    [A2] "+v"(A[2]), [A3] "+v"(A[3]), [B0] "+v"(B[0]), [B1] "+v"(B[1]), [B2] "+v"(B[2]),    \
-    [B3] "+v"(B[3])                                                                          \
-  : [s0] "v"(s0), [s1] "v"(s1), [g0] "v"(g0), [g1] "v"(g1), [bias] "s"(0x8000u),             \
-    [a0] "s"(qm[0]), [a1] "s"(qm[1]), [a2] "s"(qm[2]), [a3] "s"(qm[3]), [b0] "s"(qm[4]),     \
-    [b1] "s"(qm[5]), [b2] "s"(qm[6]), [b3] "s"(qm[7])
-  if constexpr (JJ == 0) asm(POT_STEP8_ASM(0) POT_STEP8_OPERANDS);
-  else if constexpr (JJ == 1) asm(POT_STEP8_ASM(1) POT_STEP8_OPERANDS);
-  else if constexpr (JJ == 2) asm(POT_STEP8_ASM(2) POT_STEP8_OPERANDS);
-  else asm(POT_STEP8_ASM(3) POT_STEP8_OPERANDS);
-#undef POT_STEP8_OPERANDS
-}
-#undef POT_STEP8_ASM
 
 __device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -305,15 +209,16 @@ __device__ __forceinline__ void mask_values(int t0, int t_end, int lane, ValRegs
 }
 
 // ---- prepared query operands (workspace, one block per kv head) -------------
-// PoT-4 with G >= 2: [m][pair] words 2 (q_{2p} + 2^16 q_{2p+1}); other PoT forms:
+// PoT-4: [(c * 4 + n) * (G + 1) + col] = (q + 128) 2^7 of elements 8c + n and
+// 8c + n + 4 as 16-bit halves (col = G: q = 0, the bias column); PoT-Mk:
 // [(b' * 64 + m) * G + h] = q << b'; INT8: [i * G + h] four int8 per word;
 // byte decode: [(2c + o) * G + h] four int8 (elements 8c + o + 2t, t = 0..3);
 // fp16: [i * G + h] two fp16 per word. The G per-head score factors follow.
 template <int MODE, int G, int K>
 struct QLayout {
-  static constexpr bool kPacked = MODE == kScorePot && K == 0 && G >= 2;
-  static constexpr int NP = G / 2;
-  static constexpr int kWords = MODE == kScorePot ? (kPacked ? kDim * NP : (K + 1) * kDim * G)
+  static constexpr bool kPk = MODE == kScorePot && K == 0;  // packed 16-bit shift operands
+  static constexpr int kCols = G + 1;                          // G heads + the bias column
+  static constexpr int kWords = MODE == kScorePot ? (kPk ? 32 * kCols : (K + 1) * kDim * G)
                                 : (MODE == kScoreInt8 || MODE == kScoreDs4a) ? (kDim / 4) * G
                                                      : (kDim / 2) * G;
 };
@@ -391,13 +296,17 @@ __global__ __launch_bounds__(kBlock) void prep_queries_kernel(const DecodeArgs a
   }
   if constexpr (MODE == kScorePot) {
     __syncthreads();
-    if constexpr (QL::kPacked) {
-      // pair p holds heads 2p (low field) and 2p+1 (high field) as one
-      // integer, doubled so that a shift by 31 clears it
-      for (int i = tid; i < kDim * QL::NP; i += kBlock) {
-        const int m = i / QL::NP, p = i % QL::NP;
-        qb[i] = (int32_t)(((uint32_t)qh[(2 * p) * kDim + m] +
-                           ((uint32_t)qh[(2 * p + 1) * kDim + m] << 16)) << 1);
+    if constexpr (QL::kPk) {
+      // word ((c * 4 + n) * (G + 1) + col) holds, for elements 8c + n (low
+      // half) and 8c + n + 4 (high half), (q + 128) 2^7 of head col, or
+      // 128 * 2^7 in the bias column col = G: 16-bit operands in [128, 32640]
+      // with 7 clear low bits, so a right shift by e <= 7 is exact
+      for (int i = tid; i < 32 * QL::kCols; i += kBlock) {
+        const int col = i % QL::kCols, cn = i / QL::kCols, n = cn & 3, c = cn >> 2;
+        const int m = 8 * c + n;
+        const uint32_t lo = (uint32_t)((col < G ? qh[col * kDim + m] : 0) + 128) << 7;
+        const uint32_t hi = (uint32_t)((col < G ? qh[col * kDim + m + 4] : 0) + 128) << 7;
+        qb[i] = (int32_t)(lo | (hi << 16));
       }
     } else {
       for (int i = tid; i < (K + 1) * kDim * G; i += kBlock) {
@@ -427,8 +336,8 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
                                                         const int32_t* __restrict__ qbuf) {
   using QL = QLayout<MODE, G, K>;
   __shared__ DecodeSmem sm;
-  constexpr bool kPacked = QL::kPacked;
-  constexpr int NP = QL::NP;
+  constexpr bool kPk = QL::kPk;
+  constexpr int kCols = QL::kCols;
 
   const int tid = threadIdx.x, lane = tid & 63;
   // the wave index is uniform in a wave; saying so keeps the tile loop's
@@ -528,60 +437,56 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
     if constexpr (MODE == kScorePot) {
       const uint32_t w[8] = {ks.c0.x, ks.c0.y, ks.c0.z, ks.c0.w,
                              ks.c1.x, ks.c1.y, ks.c1.z, ks.c1.w};
-      int nneg = 0;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) nneg += __popc(w[i] & 0x88888888u);
       int32_t accv[G];
-      if constexpr (kPacked) {
-        uint32_t accA[NP], accB[NP];
+      if constexpr (kPk) {
+        // Two elements of one head per 16-bit-pair operand (element 8c + n in
+        // the low half, 8c + n + 4 in the high half). v_pk_lshrrev_b16 shifts
+        // each half by its element's exponent: (q + 128) 2^7 >> e =
+        // (q + 128) 2^(7 - e), exact; the zero code (e = 7) is given the
+        // shift 15, which clears the operand. v_dot2_i32_i16 with weights
+        // sigma = +-1 per half then flips the signs and adds both halves into
+        // the int32 sum (a signed add: no product q 2^k goes through a
+        // multiplier). The bias column (q = 0) sums 128 sigma 2^(7 - e), which
+        // is subtracted from every head.
+        int32_t a9[kCols];
 #pragma unroll
-        for (int p = 0; p < NP; ++p) accA[p] = accB[p] = 0u;
-        // G = 8: the 32 operand words of one code word's 8 elements, read as
-        // one group so that a tile waits on the scalar cache 8 times, not 32
-        uint32_t qq[32];
-        // one 2-element step: byte JJ of the shift words holds the shifts of
-        // elements 8i + 2JJ (s0) and 8i + 2JJ + 1 (s1)
-        auto step = [&](auto jj_tag, int i, uint32_t wi, uint32_t s0, uint32_t s1) {
-          constexpr int JJ = decltype(jj_tag)::value;
-          const int m = 8 * i + 2 * JJ;
-          const uint32_t sg0 = (uint32_t)((int32_t)(wi << (28 - 8 * JJ)) >> 31);
-          const uint32_t sg1 = (uint32_t)((int32_t)(wi << (24 - 8 * JJ)) >> 31);
-          if constexpr (NP == 4) {
-            pot_step8<JJ>(s0, s1, sg0, sg1, qq + 8 * JJ, accA, accB);
-            return;
-          }
-          uint32_t P[NP];
-#pragma unroll
-          for (int p = 0; p < NP; ++p)
-            P[p] = xad_u32(shl_by_byte<JJ>(s0, (uint32_t)qb[m * NP + p]), sg0, 0x8000u);
-#pragma unroll
-          for (int p = 0; p < NP; ++p)
-            P[p] = xad_u32(shl_by_byte<JJ>(s1, (uint32_t)qb[(m + 1) * NP + p]), sg1, P[p]);
-#pragma unroll
-          for (int p = 0; p < NP; ++p) {
-            accA[p] = add_lo16(accA[p], P[p]);
-            accB[p] = add_hi16s(accB[p], P[p]);
-          }
-        };
+        for (int c = 0; c < kCols; ++c) a9[c] = 0;
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-          const uint32_t s0 = 0x26262626u - (w[i] & 0x07070707u);
-          const uint32_t s1 = 0x26262626u - ((w[i] >> 4) & 0x07070707u);
-          if constexpr (NP == 4) {
+          const uint32_t wi = w[i];
+          const uint32_t z = wi & (wi >> 1) & (wi >> 2) & 0x11111111u;  // e = 7 per nibble
+          const uint32_t x = (wi & 0x77777777u) | (z << 3);              // e, or 15 for zero
+          // this code word's operands, read as one scalar group per tile (a
+          // zero offset that depends on the tile keeps the compiler from
+          // hoisting all 32 (G + 1) words out of the loop, where they would
+          // not fit in scalar registers and would spill into vector lanes)
+          int toff = 0;
+          asm("" : "+s"(toff) : "s"(jt));
+          uint32_t qq[4 * kCols];
 #pragma unroll
-            for (int k = 0; k < 32; ++k) qq[k] = (uint32_t)qb[32 * i + k];
+          for (int k = 0; k < 4 * kCols; ++k) qq[k] = (uint32_t)qb[toff + 4 * kCols * i + k];
+#pragma unroll
+          for (int n = 0; n < 4; ++n) {
+            const u16x2 sh = __builtin_bit_cast(u16x2, x >> (4 * n)) & (unsigned short)15;
+            const s16x2 sgm = __builtin_bit_cast(s16x2, wi << (12 - 4 * n)) >> (short)15;
+            const s16x2 sg =
+                __builtin_bit_cast(s16x2, __builtin_bit_cast(uint32_t, sgm) | 0x00010001u);
+#pragma unroll
+            for (int c = 0; c < kCols; ++c) {
+              const u16x2 pv = __builtin_bit_cast(u16x2, qq[kCols * n + c]) >> sh;
+              a9[c] = __builtin_amdgcn_sdot2(__builtin_bit_cast(s16x2, pv), sg, a9[c], false);
+            }
           }
-          step(std::integral_constant<int, 0>{}, i, w[i], s0, s1);
-          step(std::integral_constant<int, 1>{}, i, w[i], s0, s1);
-          step(std::integral_constant<int, 2>{}, i, w[i], s0, s1);
-          step(std::integral_constant<int, 3>{}, i, w[i], s0, s1);
         }
 #pragma unroll
-        for (int p = 0; p < NP; ++p) {
-          accv[2 * p] = (int32_t)(accA[p] - 32u * 0x8000u + (uint32_t)nneg);
-          accv[2 * p + 1] = (int32_t)accB[p];
-        }
+        for (int h = 0; h < G; ++h) accv[h] = a9[h] - a9[G];
       } else {
+        // one head per int32 accumulator; v_xad_u32 applies the sign as a
+        // ones' complement and the missing +1 per negative element is added
+        // once per key from a popcount of the sign bits
+        int nneg = 0;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) nneg += __popc(w[i] & 0x88888888u);
         uint32_t accu[G];
 #pragma unroll
         for (int h = 0; h < G; ++h) accu[h] = 0u;
