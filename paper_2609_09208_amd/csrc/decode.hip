@@ -553,8 +553,13 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
         const uint32_t m0 = __builtin_amdgcn_perm(0x00010204u, 0x08102040u, e0);
         const uint32_t m1 = __builtin_amdgcn_perm(0x00010204u, 0x08102040u, e1);
         const uint32_t n0 = (wc >> 3) & 0x01010101u, n1 = (wc >> 7) & 0x01010101u;
-        const uint32_t k0 = xad_u32(m0, (n0 << 8) - n0, n0);
-        const uint32_t k1 = xad_u32(m1, (n1 << 8) - n1, n1);
+        // 0xff in the bytes of negative elements as (n << 8) - n: the shift is
+        // kept opaque, or the compiler forms n * 255 with the quarter-rate
+        // v_mul_lo_u32
+        uint32_t n0s = n0 << 8, n1s = n1 << 8;
+        asm("" : "+v"(n0s), "+v"(n1s));
+        const uint32_t k0 = xad_u32(m0, n0s - n0, n0);
+        const uint32_t k1 = xad_u32(m1, n1s - n1, n1);
 #pragma unroll
         for (int h = 0; h < G; ++h) {
           accd[h] = __builtin_amdgcn_sdot4(qb[(2 * c) * G + h], (int32_t)k0, accd[h], false);
