@@ -63,6 +63,10 @@ def _load():
                                          i32, i32, i32, i32, i32, i32,
                                          P, P, P, P, P, P, P]
     lib.oracle_pot_decode_v8.restype = i32
+    lib.oracle_pot_decode_v8_pow2.argtypes = lib.oracle_pot_decode_v8.argtypes
+    lib.oracle_pot_decode_v8_pow2.restype = i32
+    lib.oracle_attend_x.argtypes = [P, P, P, i32, i32, i32, i32, P, P]
+    lib.oracle_attend_x.restype = i32
     lib.oracle_quantize_values.argtypes = [P, i64, P, P]
     lib.oracle_quantize_values.restype = i32
     lib.oracle_int8_encode_keys.argtypes = [i32, P, i64, P, P]
@@ -200,9 +204,11 @@ def quantize_values(v_fp16_bits):
 
 def pot_decode_v8(q, codes_se, codes_m, key_scale, v8, v_exp, t_cap, kv_head_of_q, B, Hq,
                   Hkv, T, mant_bits=0, frac_bits=7, hadamard=False, split_len=None,
-                  tile=0, want_out=True):
+                  tile=0, want_out=True, pow2=False):
     """pot_decode with the values given as INT8 codes v8 [rows, 64] and
-    exponents v_exp [rows] (value v8 * 2^-v_exp, Sec. II-E)."""
+    exponents v_exp [rows] (value v8 * 2^-v_exp, Sec. II-E). pow2: the
+    power-of-two weights 2^-k of eq. logsm (k = M - ceil(x - 1/2)) instead of
+    the softmax weights."""
     split_len = T if split_len is None else int(split_len)
     n_split = -(-T // split_len)
     res = dict(qhat=np.empty((B, Hq, DIM), np.int8),
@@ -213,7 +219,8 @@ def pot_decode_v8(q, codes_se, codes_m, key_scale, v8, v_exp, t_cap, kv_head_of_
                m_split=np.empty((B, Hq, n_split), np.int32),
                out=np.empty((B, Hq, DIM), np.float64) if want_out else None)
     cm = None if codes_m is None else _c(codes_m, np.uint8)
-    rc = _load().oracle_pot_decode_v8(
+    fn = _load().oracle_pot_decode_v8_pow2 if pow2 else _load().oracle_pot_decode_v8
+    rc = fn(
         int(mant_bits), int(frac_bits), int(hadamard), _ptr(_c(q, np.float32)),
         _ptr(_c(codes_se, np.uint8)), _ptr(cm), _ptr(_c(key_scale, np.float32)),
         _ptr(_c(v8, np.int8)), _ptr(_c(v_exp, np.int8)), int(t_cap),
@@ -223,6 +230,22 @@ def pot_decode_v8(q, codes_se, codes_m, key_scale, v8, v_exp, t_cap, kv_head_of_
     if rc:
         raise ValueError(f"oracle_pot_decode_v8 failed: {rc}")
     return res
+
+
+def attend_x(x, v8, v_exp, split_len=None, tile=0, pow2=False):
+    """One query's attention over given log2-domain scores x [T] (fp32) and
+    INT8 value rows v8 [T, 64] with exponents v_exp [T]. Returns (out fp64
+    [64], M)."""
+    x = _c(x, np.float32)
+    T = x.shape[0]
+    out = np.empty(DIM, np.float64)
+    m = np.empty(1, np.int32)
+    rc = _load().oracle_attend_x(_ptr(x), _ptr(_c(v8, np.int8)), _ptr(_c(v_exp, np.int8)), T,
+                                 T if split_len is None else int(split_len), int(tile),
+                                 int(pow2), _ptr(m), _ptr(out))
+    if rc:
+        raise ValueError(f"oracle_attend_x failed: {rc}")
+    return out, int(m[0])
 
 
 def int8_encode_keys(k_fp16_bits, hadamard=False):

@@ -305,8 +305,19 @@ static double value_at(const value_row* r, int d) {
   return (double)oracle_half_to_float(r->v16[d]);
 }
 
+/* Weight of a key with log2-domain score x under the integer maximum M.     */
+/*  pow2 = 0: the softmax weight 2^(x - M) (eq. logsm with exact exp2).     */
+/*  pow2 = 1: the power-of-two weight A~ = 2^-k of eq. logsm, k = M - c with  */
+/*  c = ceil(x - 1/2) computed in fp32, i.e. k = M - x rounded half up.      */
+/*  (The paper says "round"; rounding half up makes k - M a function of x    */
+/*  alone, so a running maximum that rises by any integer rescales exactly.) */
+static double key_weight(float x, int32_t M, int pow2) {
+  if (pow2) return ldexp(1.0, (int)ceilf(x - 0.5f) - M);
+  return exp2((double)x - (double)M);
+}
+
 static void softmax_av(const float* x, const value_row* vrows, int T,
-                       int split_len, int tile, int32_t* m_final,
+                       int split_len, int tile, int pow2, int32_t* m_final,
                        int32_t* m_split, double* out) {
   float xmax = -INFINITY;
   for (int t = 0; t < T; ++t)
@@ -326,7 +337,7 @@ static void softmax_av(const float* x, const value_row* vrows, int T,
   if (tile <= 0) {
     double l = 0.0, o[DIM] = {0};
     for (int t = 0; t < T; ++t) {
-      double w = exp2((double)x[t] - (double)M);
+      double w = key_weight(x[t], M, pow2);
       l += w;
       for (int d = 0; d < DIM; ++d) o[d] += w * value_at(&vrows[t], d);
     }
@@ -356,7 +367,7 @@ static void softmax_av(const float* x, const value_row* vrows, int T,
         Mrun = Mt;
       }
       for (int t = t0; t < t1; ++t) {
-        double w = exp2((double)x[t] - (double)Mrun);
+        double w = key_weight(x[t], Mrun, pow2);
         l += w;
         for (int d = 0; d < DIM; ++d) o[d] += w * value_at(&vrows[t], d);
       }
@@ -393,7 +404,7 @@ static int pot_decode_impl(int mant_bits, int frac_bits, int hadamard,
                            const uint8_t* codes_m, const float* key_scale,
                            const uint16_t* v, const int8_t* v8, const int8_t* v_exp,
                            int64_t t_cap, const int32_t* kv_head_of_q,
-                           int B, int Hq, int Hkv, int T, int split_len, int tile,
+                           int B, int Hq, int Hkv, int T, int split_len, int tile, int pow2,
                            int8_t* qhat_out, float* delta_out, int32_t* scores_out,
                            float* x_out, int32_t* m_final, int32_t* m_split,
                            double* out) {
@@ -427,7 +438,7 @@ static int pot_decode_impl(int mant_bits, int frac_bits, int hadamard,
         vrows[t].g = v8 ? v_exp[row] : 0;
       }
       if (rc) break;
-      softmax_av(x, vrows, T, split_len, tile, m_final ? m_final + bh : NULL,
+      softmax_av(x, vrows, T, split_len, tile, pow2, m_final ? m_final + bh : NULL,
                  m_split ? m_split + bh * n_split : NULL,
                  out ? out + bh * DIM : NULL);
     }
@@ -446,7 +457,7 @@ int oracle_pot_decode(int mant_bits, int frac_bits, int hadamard,
                       float* x_out, int32_t* m_final, int32_t* m_split,
                       double* out) {
   return pot_decode_impl(mant_bits, frac_bits, hadamard, q, codes_se, codes_m, key_scale, v,
-                         NULL, NULL, t_cap, kv_head_of_q, B, Hq, Hkv, T, split_len, tile,
+                         NULL, NULL, t_cap, kv_head_of_q, B, Hq, Hkv, T, split_len, tile, 0,
                          qhat_out, delta_out, scores_out, x_out, m_final, m_split, out);
 }
 
@@ -461,8 +472,42 @@ int oracle_pot_decode_v8(int mant_bits, int frac_bits, int hadamard,
                          int32_t* scores_out, float* x_out, int32_t* m_final,
                          int32_t* m_split, double* out) {
   return pot_decode_impl(mant_bits, frac_bits, hadamard, q, codes_se, codes_m, key_scale, NULL,
-                         v8, v_exp, t_cap, kv_head_of_q, B, Hq, Hkv, T, split_len, tile,
+                         v8, v_exp, t_cap, kv_head_of_q, B, Hq, Hkv, T, split_len, tile, 0,
                          qhat_out, delta_out, scores_out, x_out, m_final, m_split, out);
+}
+
+/* Both products by powers of two (Sec. II-E, eq. logsm and eq. av): the     */
+/* same scores, INT8 values v8 * 2^-v_exp, and the power-of-two weights      */
+/* A~_t = 2^-k_t: O = sum_t A~_t v_t / sum_t A~_t (the normalisation eq. av   */
+/* leaves out), every product A~_t v_t exact, sums in fp64. No k_max cut.     */
+int oracle_pot_decode_v8_pow2(int mant_bits, int frac_bits, int hadamard,
+                              const float* q, const uint8_t* codes_se,
+                              const uint8_t* codes_m, const float* key_scale,
+                              const int8_t* v8, const int8_t* v_exp, int64_t t_cap,
+                              const int32_t* kv_head_of_q, int B, int Hq, int Hkv, int T,
+                              int split_len, int tile, int8_t* qhat_out, float* delta_out,
+                              int32_t* scores_out, float* x_out, int32_t* m_final,
+                              int32_t* m_split, double* out) {
+  return pot_decode_impl(mant_bits, frac_bits, hadamard, q, codes_se, codes_m, key_scale, NULL,
+                         v8, v_exp, t_cap, kv_head_of_q, B, Hq, Hkv, T, split_len, tile, 1,
+                         qhat_out, delta_out, scores_out, x_out, m_final, m_split, out);
+}
+
+/* Attention of one query over given log2-domain scores x[T] and INT8 value  */
+/* rows v8[T][64] * 2^-v_exp[t] (test hook for the weight rules): pow2 = 0   */
+/* softmax weights, 1 power-of-two weights; tile > 0 runs the online form.   */
+int oracle_attend_x(const float* x, const int8_t* v8, const int8_t* v_exp, int T,
+                    int split_len, int tile, int pow2, int32_t* m_final, double* out) {
+  if (T < 1 || split_len < 1) return -1;
+  value_row* vrows = (value_row*)malloc(sizeof(value_row) * T);
+  for (int t = 0; t < T; ++t) {
+    vrows[t].v16 = NULL;
+    vrows[t].v8 = v8 + (int64_t)t * DIM;
+    vrows[t].g = v_exp[t];
+  }
+  softmax_av(x, vrows, T, split_len, tile, pow2, m_final, NULL, out);
+  free(vrows);
+  return 0;
 }
 
 /* ---------------------------------------------------------------------- */
@@ -547,7 +592,7 @@ int oracle_int8_decode(int hadamard, const float* q, const int8_t* codes,
         vrows[t].v8 = NULL;
         vrows[t].g = 0;
       }
-      softmax_av(x, vrows, T, split_len, 0, m_final ? m_final + bh : NULL,
+      softmax_av(x, vrows, T, split_len, 0, 0, m_final ? m_final + bh : NULL,
                  m_split ? m_split + bh * n_split : NULL,
                  out ? out + bh * DIM : NULL);
     }
