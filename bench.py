@@ -274,6 +274,9 @@ def comparators(pa, lay, dev):
     engines["pot_v8"] = lambda i: pa.pot_decode_attention_v8(
         lay.fmt, 0, cl[i]["q"], cl[i]["codes_se"], cl[i]["codes_m"], cl[i]["key_scale"],
         v8[i][0], v8[i][1], T, heads, B, HQ, HKV, T, out, ws)
+    engines["pot_v8_pow2"] = lambda i: pa.pot_decode_attention_v8_pow2(
+        lay.fmt, 0, cl[i]["q"], cl[i]["codes_se"], cl[i]["codes_m"], cl[i]["key_scale"],
+        v8[i][0], v8[i][1], T, heads, B, HQ, HKV, T, out, ws)
     if lay.k == 0:  # byte decode + v_dot4 on the same PoT-4 caches (a multiply path)
         engines["ds4a"] = lambda i: pa.pot_ds4a_decode_attention(
             lay.fmt, cl[i]["q"], cl[i]["codes_se"], cl[i]["key_scale"], cl[i]["v"], T, heads,
@@ -288,7 +291,7 @@ def comparators(pa, lay, dev):
             runs[name].append(timed_calls(fn, len(cl), reps=10, warm=4))
     med = {name: float(sorted(v)[len(v) // 2]) for name, v in runs.items()}
     pot_us, f16_us, i8_us, ds4a_us = med["pot"], med["fp16"], med["int8"], med.get("ds4a")
-    pv8_us, dv8_us = med["pot_v8"], med.get("ds4a_v8")
+    pv8_us, dv8_us, pw_us = med["pot_v8"], med.get("ds4a_v8"), med["pot_v8_pow2"]
 
     def frac(per_row, us):
         return algorithmic_bytes(B, T, per_row) / (us * 1e-6) / 1e9 / HBM_PEAK_GBS
@@ -310,7 +313,10 @@ def comparators(pa, lay, dev):
                 "ds4a_us_per_layer": dv8_us,
                 "ds4a_hbm_frac": frac(row_bytes_v8(0), dv8_us) if dv8_us else None,
                 "ds4a_speedup_vs_fp16": f16_us / dv8_us if dv8_us else None,
-                "note": "INT8 values with a power-of-two per-token scale (pot_store_values_int8)"},
+                "pot_pow2_weights_us_per_layer": pw_us,
+                "note": "INT8 values with a power-of-two per-token scale (pot_store_values_int8); "
+                        "pow2 weights: both products by powers of two "
+                        "(pot_decode_attention_v8_pow2)"},
             "timing": f"median of {COMPARE_ROUNDS} interleaved rounds of 10 passes over the "
                       f"{len(cl)} layers per engine"}
 

@@ -276,6 +276,25 @@ pot_status pot_decode_attention_v8(const pot_format* fmt, int32_t engine, const 
                                    int32_t Hkv, int32_t T, float* out, void* workspace,
                                    size_t ws_bytes, pot_debug* dbg, void* stream);
 
+/* Both products by powers of two (Sec. II-E, the option eq. logsm and eq. av
+ * describe): the scores as pot_decode_attention_v8 (engine 0 or 1), INT8
+ * values, and the power-of-two weights A~_t = 2^-k_t of eq. logsm in place
+ * of the softmax weights: k_t = M - ceil(x_t - 1/2) (M - x_t rounded half up,
+ * so a rising running maximum rescales every earlier weight exactly), and
+ * O = sum_t A~_t v^_t 2^-g_t / sum_t A~_t (eq. av leaves the normalisation
+ * out; no k_max cut: weights below 2^-36 of the largest vanish in the fp16
+ * weight operand). Every product A~_t v^_t 2^-g_t is exact; the sums are fp32
+ * on the matrix cores. Arguments, layout, workspace, taps and errors as
+ * pot_decode_attention_v8. */
+pot_status pot_decode_attention_v8_pow2(const pot_format* fmt, int32_t engine,
+                                        const float* q, const uint8_t* codes_se,
+                                        const uint8_t* codes_m, const float* key_scale,
+                                        const uint8_t* v_u8, const int8_t* v_exp,
+                                        int64_t t_cap, const int32_t* kv_head_of_q,
+                                        int32_t B, int32_t Hq, int32_t Hkv, int32_t T,
+                                        float* out, void* workspace, size_t ws_bytes,
+                                        pot_debug* dbg, void* stream);
+
 /* pot_append_decode_attention on a cache with INT8 values: the new token's
  * values are quantised as by pot_store_values_int8 and stored with their
  * exponent at position T - 1, then pot_decode_attention_v8 runs with the

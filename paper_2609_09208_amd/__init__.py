@@ -75,6 +75,8 @@ def _load_library():
         "pot_store_values_int8": (i32, [P, i64, i64, i64, i64, P, P, P]),
         "pot_decode_attention_v8": (i32, [fmt_p, i32, P, P, P, P, P, P, i64, P, i32, i32,
                                           i32, i32, P, P, S, dbg_p, P]),
+        "pot_decode_attention_v8_pow2": (i32, [fmt_p, i32, P, P, P, P, P, P, i64, P, i32, i32,
+                                               i32, i32, P, P, S, dbg_p, P]),
         "pot_decode_attention": (i32, [fmt_p, P, P, P, P, P, i64, P, i32, i32,
                                        i32, i32, P, P, S, dbg_p, P]),
         "pot_append_decode_attention": (i32, [fmt_p, P, P, P, P, P, P, P, i64, P, i32, i32,
@@ -175,6 +177,19 @@ def pot_decode_attention_v8(fmt: pot_format, engine: int, q, codes_se, codes_m, 
     _, hp = _heads(kv_head_of_q)
     nbytes = workspace.numel() * workspace.element_size() if ws_bytes is None else ws_bytes
     _check(_lib.pot_decode_attention_v8(
+        ctypes.byref(fmt), int(engine), _ptr(q), _ptr(codes_se), _ptr(codes_m),
+        _ptr(key_scale), _ptr(v_u8), _ptr(v_exp), int(t_cap), hp, B, Hq, Hkv, T, _ptr(out),
+        _ptr(workspace), nbytes, ctypes.byref(dbg) if dbg is not None else None,
+        _stream(stream)))
+
+
+def pot_decode_attention_v8_pow2(fmt: pot_format, engine: int, q, codes_se, codes_m, key_scale,
+                                 v_u8, v_exp, t_cap: int, kv_head_of_q, B: int, Hq: int,
+                                 Hkv: int, T: int, out, workspace, ws_bytes=None,
+                                 dbg: pot_debug | None = None, stream=None) -> None:
+    _, hp = _heads(kv_head_of_q)
+    nbytes = workspace.numel() * workspace.element_size() if ws_bytes is None else ws_bytes
+    _check(_lib.pot_decode_attention_v8_pow2(
         ctypes.byref(fmt), int(engine), _ptr(q), _ptr(codes_se), _ptr(codes_m),
         _ptr(key_scale), _ptr(v_u8), _ptr(v_exp), int(t_cap), hp, B, Hq, Hkv, T, _ptr(out),
         _ptr(workspace), nbytes, ctypes.byref(dbg) if dbg is not None else None,

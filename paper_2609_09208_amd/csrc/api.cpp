@@ -93,10 +93,10 @@ Plan plan_bound(int B, int Hkv, int T) {
 }
 
 std::atomic<int> g_cus[64];
-// [score mode][INT8 values][G][mant_bits]
-std::atomic<int> g_occ[4][2][9][5];
+// [score mode][value format][G][mant_bits]
+std::atomic<int> g_occ[4][3][9][5];
 
-long device_slots(int mode, int G, int mant_bits, bool v8) {
+long device_slots(int mode, int G, int mant_bits, int vf) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
   int cus = g_cus[dev].load(std::memory_order_relaxed);
@@ -106,10 +106,10 @@ long device_slots(int mode, int G, int mant_bits, bool v8) {
       cus = 256;
     g_cus[dev].store(cus, std::memory_order_relaxed);
   }
-  std::atomic<int>& slot = g_occ[mode][v8 ? 1 : 0][G][mant_bits];
+  std::atomic<int>& slot = g_occ[mode][vf][G][mant_bits];
   int occ = slot.load(std::memory_order_relaxed);
   if (occ <= 0) {
-    occ = decode_occupancy(mode, G, mant_bits, v8);
+    occ = decode_occupancy(mode, G, mant_bits, vf);
     if (occ <= 0) occ = 2;
     slot.store(occ, std::memory_order_relaxed);
   }
@@ -160,7 +160,8 @@ pot_status check_heads(const int32_t* map, int Hq, int Hkv, DecodeArgs* a, int* 
 // Shared tail of the three decode entry points.
 pot_status decode_common(int mode, int mant_bits, DecodeArgs& a, const int32_t* map, int B,
                          int Hq, int Hkv, int T, int64_t t_cap, void* workspace,
-                         size_t ws_bytes, pot_debug* dbg, void* stream, bool v8 = false) {
+                         size_t ws_bytes, pot_debug* dbg, void* stream, int vf = 0) {
+  const bool v8 = vf != 0;
   if (!shape_ok(B, Hq, Hkv, T))
     return fail(POT_ERR_INVALID_ARG, "bad shape B=%d Hq=%d Hkv=%d T=%d", B, Hq, Hkv, T);
   if (t_cap < T) return fail(POT_ERR_INVALID_ARG, "T %d > t_cap %lld", T, (long long)t_cap);
@@ -189,7 +190,7 @@ pot_status decode_common(int mode, int mant_bits, DecodeArgs& a, const int32_t* 
     p = plan_from_count(T, force);
   } else {
     const int mbits = mode == kScorePot ? mant_bits : 0;
-    const int S = split_count_for_slots((long)B * Hkv, device_slots(mode, G, mbits, v8));
+    const int S = split_count_for_slots((long)B * Hkv, device_slots(mode, G, mbits, vf));
     p = plan_from_count(T, std::min(S, plan_bound(B, Hkv, T).n_splits));
   }
   const WsLayout w = ws_layout(B, Hq, Hkv, p.n_splits);
@@ -223,8 +224,42 @@ pot_status decode_common(int mode, int mant_bits, DecodeArgs& a, const int32_t* 
       return fail(POT_ERR_UNSUPPORTED, "debug taps are not available on the fp16 path");
   }
   return hip_status(
-      launch_decode(mode, G, mant_bits, debug, v8, a, static_cast<hipStream_t>(stream)),
+      launch_decode(mode, G, mant_bits, debug, vf, a, static_cast<hipStream_t>(stream)),
       "decode launch");
+}
+
+// Shared body of the INT8-value entry points; vf 1: softmax weights, 2:
+// power-of-two weights.
+pot_status decode_v8(int vf, const pot_format* fmt, int32_t engine, const float* q,
+                                   const uint8_t* codes_se, const uint8_t* codes_m,
+                                   const float* key_scale, const uint8_t* v_u8,
+                                   const int8_t* v_exp, int64_t t_cap,
+                                   const int32_t* kv_head_of_q, int32_t B, int32_t Hq,
+                                   int32_t Hkv, int32_t T, float* out, void* workspace,
+                                   size_t ws_bytes, pot_debug* dbg, void* stream) {
+  pot_status st = check_format(fmt);
+  if (st != POT_OK) return st;
+  if (engine != 0 && engine != 1)
+    return fail(POT_ERR_INVALID_ARG, "engine %d (0 shift-accumulate, 1 byte decode)", engine);
+  if (engine == 1 && fmt->mant_bits != 0)
+    return fail(POT_ERR_UNSUPPORTED, "the byte-decode path scores PoT-4 codes only (mant_bits 0)");
+  if (!codes_se || !key_scale) return fail(POT_ERR_INVALID_ARG, "codes_se or key_scale is NULL");
+  if ((fmt->mant_bits > 0) != (codes_m != nullptr))
+    return fail(POT_ERR_INVALID_ARG, "codes_m must be non-NULL exactly when mant_bits > 0");
+  if (!aligned(codes_se, 16) || !aligned(key_scale, 4) || (codes_m && !aligned(codes_m, 8)))
+    return fail(POT_ERR_INVALID_ARG, "misaligned codes_se / key_scale / codes_m");
+  DecodeArgs a{};
+  a.q = q;
+  a.codes_se = codes_se;
+  a.codes_m = codes_m;
+  a.key_scale = key_scale;
+  a.v8 = v_u8;
+  a.v_exp = v_exp;
+  a.out = out;
+  a.frac_bits = fmt->frac_bits;
+  a.hadamard = fmt->hadamard;
+  return decode_common(engine == 0 ? kScorePot : kScoreDs4a, fmt->mant_bits, a, kv_head_of_q, B,
+                       Hq, Hkv, T, t_cap, workspace, ws_bytes, dbg, stream, vf);
 }
 
 }  // namespace
@@ -407,29 +442,19 @@ pot_status pot_decode_attention_v8(const pot_format* fmt, int32_t engine, const 
                                    const int32_t* kv_head_of_q, int32_t B, int32_t Hq,
                                    int32_t Hkv, int32_t T, float* out, void* workspace,
                                    size_t ws_bytes, pot_debug* dbg, void* stream) {
-  pot_status st = check_format(fmt);
-  if (st != POT_OK) return st;
-  if (engine != 0 && engine != 1)
-    return fail(POT_ERR_INVALID_ARG, "engine %d (0 shift-accumulate, 1 byte decode)", engine);
-  if (engine == 1 && fmt->mant_bits != 0)
-    return fail(POT_ERR_UNSUPPORTED, "the byte-decode path scores PoT-4 codes only (mant_bits 0)");
-  if (!codes_se || !key_scale) return fail(POT_ERR_INVALID_ARG, "codes_se or key_scale is NULL");
-  if ((fmt->mant_bits > 0) != (codes_m != nullptr))
-    return fail(POT_ERR_INVALID_ARG, "codes_m must be non-NULL exactly when mant_bits > 0");
-  if (!aligned(codes_se, 16) || !aligned(key_scale, 4) || (codes_m && !aligned(codes_m, 8)))
-    return fail(POT_ERR_INVALID_ARG, "misaligned codes_se / key_scale / codes_m");
-  DecodeArgs a{};
-  a.q = q;
-  a.codes_se = codes_se;
-  a.codes_m = codes_m;
-  a.key_scale = key_scale;
-  a.v8 = v_u8;
-  a.v_exp = v_exp;
-  a.out = out;
-  a.frac_bits = fmt->frac_bits;
-  a.hadamard = fmt->hadamard;
-  return decode_common(engine == 0 ? kScorePot : kScoreDs4a, fmt->mant_bits, a, kv_head_of_q, B,
-                       Hq, Hkv, T, t_cap, workspace, ws_bytes, dbg, stream, true);
+  return decode_v8(1, fmt, engine, q, codes_se, codes_m, key_scale, v_u8, v_exp, t_cap,
+                   kv_head_of_q, B, Hq, Hkv, T, out, workspace, ws_bytes, dbg, stream);
+}
+
+pot_status pot_decode_attention_v8_pow2(const pot_format* fmt, int32_t engine, const float* q,
+                                        const uint8_t* codes_se, const uint8_t* codes_m,
+                                        const float* key_scale, const uint8_t* v_u8,
+                                        const int8_t* v_exp, int64_t t_cap,
+                                        const int32_t* kv_head_of_q, int32_t B, int32_t Hq,
+                                        int32_t Hkv, int32_t T, float* out, void* workspace,
+                                        size_t ws_bytes, pot_debug* dbg, void* stream) {
+  return decode_v8(2, fmt, engine, q, codes_se, codes_m, key_scale, v_u8, v_exp, t_cap,
+                   kv_head_of_q, B, Hq, Hkv, T, out, workspace, ws_bytes, dbg, stream);
 }
 
 pot_status pot_append_decode_attention_v8(const pot_format* fmt, int32_t engine,
@@ -473,7 +498,7 @@ pot_status pot_append_decode_attention_v8(const pot_format* fmt, int32_t engine,
   a.app_v_exp = v_exp;
   a.app_tab = make_encode_tables(fmt->mant_bits);
   return decode_common(engine == 0 ? kScorePot : kScoreDs4a, fmt->mant_bits, a, kv_head_of_q, B,
-                       Hq, Hkv, T, t_cap, workspace, ws_bytes, dbg, stream, true);
+                       Hq, Hkv, T, t_cap, workspace, ws_bytes, dbg, stream, 1);
 }
 
 pot_status pot_ds4a_decode_attention(const pot_format* fmt, const float* q,

@@ -328,7 +328,9 @@ struct alignas(16) DecodeSmem {
   int last;
 };
 
-template <int MODE, int G, int K, bool DEBUG, bool V8>
+// VF: value format, 0 fp16 values, 1 INT8 values, 2 INT8 values with the
+// power-of-two weights of eq. logsm.
+template <int MODE, int G, int K, bool DEBUG, int VF>
 // qbuf is passed on its own as a restrict parameter: the prepared query
 // operands are never written here, which lets the compiler read them through
 // the scalar cache even in the debug variants that store score taps.
@@ -336,6 +338,8 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
                                                         const int32_t* __restrict__ qbuf) {
   using QL = QLayout<MODE, G, K>;
   __shared__ DecodeSmem sm;
+  constexpr bool V8 = VF != 0;
+  constexpr bool kPow2 = VF == 2;
   constexpr bool kPk = QL::kPk;
   constexpr int kCols = QL::kCols;
 
@@ -703,8 +707,21 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
     uint32_t hw[4], lw[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      float p0 = __builtin_amdgcn_exp2f(xv[2 * i] + bias);
-      float p1 = __builtin_amdgcn_exp2f(xv[2 * i + 1] + bias);
+      float p0, p1;
+      if constexpr (kPow2) {
+        // A~ = 2^-k with k = M - ceil(x - 1/2) (M - x rounded half up):
+        // p = 2^(ceil(x - 1/2) - M + 12), exact; keys masked to -inf get 0
+        auto pw = [&](float x) -> float {
+          return x > -INFINITY
+                     ? __builtin_amdgcn_ldexpf(1.0f, (int)ceilf(x - 0.5f) - m_run + (int)kPScale)
+                     : 0.0f;
+        };
+        p0 = pw(xv[2 * i]);
+        p1 = pw(xv[2 * i + 1]);
+      } else {
+        p0 = __builtin_amdgcn_exp2f(xv[2 * i] + bias);
+        p1 = __builtin_amdgcn_exp2f(xv[2 * i + 1] + bias);
+      }
       if constexpr (V8) {
         // the softmax sum takes p; A.V takes p 2^(g_ref - g) (exact scaling)
         lsum += p0;
@@ -851,9 +868,9 @@ __global__ __launch_bounds__(64) void combine_kernel(const DecodeArgs a) {
   }
 }
 
-template <int MODE, int G, int K, bool DEBUG, bool V8>
+template <int MODE, int G, int K, bool DEBUG, int VF>
 static hipError_t launch_t(const DecodeArgs& a, hipStream_t stream) {
-  if constexpr (V8 && MODE != kScorePot && MODE != kScoreDs4a) {
+  if constexpr (VF != 0 && MODE != kScorePot && MODE != kScoreDs4a) {
     return hipErrorInvalidValue;
   } else {
   hipLaunchKernelGGL((prep_queries_kernel<MODE, G, K, DEBUG>), dim3((uint32_t)a.Hkv, (uint32_t)a.B),
@@ -861,7 +878,7 @@ static hipError_t launch_t(const DecodeArgs& a, hipStream_t stream) {
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const dim3 grid((uint32_t)a.n_splits, (uint32_t)a.Hkv, (uint32_t)a.B);
-  hipLaunchKernelGGL((decode_kernel<MODE, G, K, DEBUG, V8>), grid, dim3(kBlock), 0, stream, a,
+  hipLaunchKernelGGL((decode_kernel<MODE, G, K, DEBUG, VF>), grid, dim3(kBlock), 0, stream, a,
                      static_cast<const int32_t*>(a.qbuf));
   if (a.n_splits == 1) return hipGetLastError();
   const hipError_t e2 = hipGetLastError();
@@ -872,31 +889,31 @@ static hipError_t launch_t(const DecodeArgs& a, hipStream_t stream) {
   }
 }
 
-template <int MODE, int G, int K, bool V8>
+template <int MODE, int G, int K, int VF>
 static int occupancy_t() {
   int n = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
-          &n, reinterpret_cast<const void*>(&decode_kernel<MODE, G, K, false, V8>), kBlock, 0) !=
+          &n, reinterpret_cast<const void*>(&decode_kernel<MODE, G, K, false, VF>), kBlock, 0) !=
       hipSuccess)
     return 0;
   return n;
 }
 
-template <bool V8>
+template <int VF>
 static int occupancy_v(int mode, int G, int mant_bits) {
   auto by_k = [&](auto g_tag) -> int {
     constexpr int GG = decltype(g_tag)::value;
-    if (mode == kScoreDs4a) return occupancy_t<kScoreDs4a, GG, 0, V8>();
-    if constexpr (!V8) {
-      if (mode == kScoreInt8) return occupancy_t<kScoreInt8, GG, 0, false>();
-      if (mode == kScoreFp16) return occupancy_t<kScoreFp16, GG, 0, false>();
+    if (mode == kScoreDs4a) return occupancy_t<kScoreDs4a, GG, 0, VF>();
+    if constexpr (VF == 0) {
+      if (mode == kScoreInt8) return occupancy_t<kScoreInt8, GG, 0, 0>();
+      if (mode == kScoreFp16) return occupancy_t<kScoreFp16, GG, 0, 0>();
     }
     switch (mant_bits) {
-      case 0: return occupancy_t<kScorePot, GG, 0, V8>();
-      case 1: return occupancy_t<kScorePot, GG, 1, V8>();
-      case 2: return occupancy_t<kScorePot, GG, 2, V8>();
-      case 3: return occupancy_t<kScorePot, GG, 3, V8>();
-      default: return occupancy_t<kScorePot, GG, 4, V8>();
+      case 0: return occupancy_t<kScorePot, GG, 0, VF>();
+      case 1: return occupancy_t<kScorePot, GG, 1, VF>();
+      case 2: return occupancy_t<kScorePot, GG, 2, VF>();
+      case 3: return occupancy_t<kScorePot, GG, 3, VF>();
+      default: return occupancy_t<kScorePot, GG, 4, VF>();
     }
   };
   switch (G) {
@@ -907,64 +924,72 @@ static int occupancy_v(int mode, int G, int mant_bits) {
   }
 }
 
-int decode_occupancy(int mode, int G, int mant_bits, bool v8) {
-  return v8 ? occupancy_v<true>(mode, G, mant_bits) : occupancy_v<false>(mode, G, mant_bits);
+int decode_occupancy(int mode, int G, int mant_bits, int vf) {
+  switch (vf) {
+    case 1: return occupancy_v<1>(mode, G, mant_bits);
+    case 2: return occupancy_v<2>(mode, G, mant_bits);
+    default: return occupancy_v<0>(mode, G, mant_bits);
+  }
 }
 
-template <int MODE, int G, bool DEBUG, bool V8>
+template <int MODE, int G, bool DEBUG, int VF>
 static hipError_t launch_k(int mant_bits, const DecodeArgs& a, hipStream_t stream) {
   if constexpr (MODE != kScorePot) {
-    return launch_t<MODE, G, 0, DEBUG, V8>(a, stream);
+    return launch_t<MODE, G, 0, DEBUG, VF>(a, stream);
   } else {
     switch (mant_bits) {
-      case 0: return launch_t<MODE, G, 0, DEBUG, V8>(a, stream);
-      case 1: return launch_t<MODE, G, 1, DEBUG, V8>(a, stream);
-      case 2: return launch_t<MODE, G, 2, DEBUG, V8>(a, stream);
-      case 3: return launch_t<MODE, G, 3, DEBUG, V8>(a, stream);
-      case 4: return launch_t<MODE, G, 4, DEBUG, V8>(a, stream);
+      case 0: return launch_t<MODE, G, 0, DEBUG, VF>(a, stream);
+      case 1: return launch_t<MODE, G, 1, DEBUG, VF>(a, stream);
+      case 2: return launch_t<MODE, G, 2, DEBUG, VF>(a, stream);
+      case 3: return launch_t<MODE, G, 3, DEBUG, VF>(a, stream);
+      case 4: return launch_t<MODE, G, 4, DEBUG, VF>(a, stream);
       default: return hipErrorInvalidValue;
     }
   }
 }
 
-template <int MODE, bool DEBUG, bool V8>
+template <int MODE, bool DEBUG, int VF>
 static hipError_t launch_g(int G, int mant_bits, const DecodeArgs& a, hipStream_t stream) {
   switch (G) {
-    case 1: return launch_k<MODE, 1, DEBUG, V8>(mant_bits, a, stream);
-    case 2: return launch_k<MODE, 2, DEBUG, V8>(mant_bits, a, stream);
-    case 4: return launch_k<MODE, 4, DEBUG, V8>(mant_bits, a, stream);
-    case 8: return launch_k<MODE, 8, DEBUG, V8>(mant_bits, a, stream);
+    case 1: return launch_k<MODE, 1, DEBUG, VF>(mant_bits, a, stream);
+    case 2: return launch_k<MODE, 2, DEBUG, VF>(mant_bits, a, stream);
+    case 4: return launch_k<MODE, 4, DEBUG, VF>(mant_bits, a, stream);
+    case 8: return launch_k<MODE, 8, DEBUG, VF>(mant_bits, a, stream);
     default: return hipErrorInvalidValue;
   }
 }
 
-template <bool V8>
+template <int VF>
 static hipError_t launch_v(int mode, int G, int mant_bits, bool debug, const DecodeArgs& a,
                            hipStream_t stream) {
   switch (mode) {
     case kScorePot:
-      return debug ? launch_g<kScorePot, true, V8>(G, mant_bits, a, stream)
-                   : launch_g<kScorePot, false, V8>(G, mant_bits, a, stream);
+      return debug ? launch_g<kScorePot, true, VF>(G, mant_bits, a, stream)
+                   : launch_g<kScorePot, false, VF>(G, mant_bits, a, stream);
     case kScoreDs4a:
-      return debug ? launch_g<kScoreDs4a, true, V8>(G, 0, a, stream)
-                   : launch_g<kScoreDs4a, false, V8>(G, 0, a, stream);
+      return debug ? launch_g<kScoreDs4a, true, VF>(G, 0, a, stream)
+                   : launch_g<kScoreDs4a, false, VF>(G, 0, a, stream);
     case kScoreInt8:
-      if constexpr (V8) return hipErrorInvalidValue;
+      if constexpr (VF != 0) return hipErrorInvalidValue;
       else
-        return debug ? launch_g<kScoreInt8, true, false>(G, 0, a, stream)
-                     : launch_g<kScoreInt8, false, false>(G, 0, a, stream);
+        return debug ? launch_g<kScoreInt8, true, 0>(G, 0, a, stream)
+                     : launch_g<kScoreInt8, false, 0>(G, 0, a, stream);
     case kScoreFp16:
-      if constexpr (V8) return hipErrorInvalidValue;
-      else return launch_g<kScoreFp16, false, false>(G, 0, a, stream);
+      if constexpr (VF != 0) return hipErrorInvalidValue;
+      else return launch_g<kScoreFp16, false, 0>(G, 0, a, stream);
     default:
       return hipErrorInvalidValue;
   }
 }
 
-hipError_t launch_decode(int mode, int G, int mant_bits, bool debug, bool v8,
+hipError_t launch_decode(int mode, int G, int mant_bits, bool debug, int vf,
                          const DecodeArgs& a, hipStream_t stream) {
-  return v8 ? launch_v<true>(mode, G, mant_bits, debug, a, stream)
-            : launch_v<false>(mode, G, mant_bits, debug, a, stream);
+  switch (vf) {
+    case 0: return launch_v<0>(mode, G, mant_bits, debug, a, stream);
+    case 1: return launch_v<1>(mode, G, mant_bits, debug, a, stream);
+    case 2: return launch_v<2>(mode, G, mant_bits, debug, a, stream);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace potattn

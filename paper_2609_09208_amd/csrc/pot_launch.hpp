@@ -97,11 +97,12 @@ constexpr int query_words(int G) { return ((5 * 64 + 1) * G + 63) / 64 * 64; }
 
 // Resident workgroups per CU of the (non-debug) decode kernel for this
 // variant, from the HIP occupancy calculator; 0 if the query fails.
-int decode_occupancy(int mode, int G, int mant_bits, bool v8);
+int decode_occupancy(int mode, int G, int mant_bits, int vf);
 
-// v8: INT8 value cache (a.v8, a.v_exp) instead of fp16 (a.v); score modes
-// kScorePot and kScoreDs4a only.
-hipError_t launch_decode(int mode, int G, int mant_bits, bool debug, bool v8,
+// vf: value format. 0: fp16 value cache (a.v); 1: INT8 value cache (a.v8,
+// a.v_exp); 2: INT8 values with the power-of-two weights of eq. logsm.
+// Formats 1 and 2 exist for the score modes kScorePot and kScoreDs4a only.
+hipError_t launch_decode(int mode, int G, int mant_bits, bool debug, int vf,
                          const DecodeArgs& a, hipStream_t stream);
 
 }  // namespace potattn

@@ -234,3 +234,19 @@ def test_int8_values_reject_bad_arguments():
     assert D(*args(ws=16)) == pa.POT_ERR_WORKSPACE
     # byte-decode engine: PoT-4 only
     assert D(*args(fmt=pa.make_format(mant_bits=1), engine=1)) == pa.POT_ERR_UNSUPPORTED
+
+
+def test_pow2_rejects_bad_arguments():
+    hm = (np.arange(32, dtype=np.int32) // 8)
+    hp = hm.ctypes.data_as(ctypes.c_void_p)
+    D = pa._lib.pot_decode_attention_v8_pow2
+
+    def args(fmt=None, engine=0, vu=FAKE, ve=FAKE, T=4096):
+        fmt = fmt if fmt is not None else pa.make_format()
+        return (ctypes.byref(fmt), engine, FAKE, FAKE, None, FAKE, vu, ve, 4096, hp, 1, 32, 4,
+                T, FAKE, FAKE, 1 << 30, None, None)
+    assert D(*args(engine=3)) == pa.POT_ERR_INVALID_ARG
+    assert D(*args(vu=None)) == pa.POT_ERR_INVALID_ARG
+    assert D(*args(ve=FAKE + 2)) == pa.POT_ERR_INVALID_ARG
+    assert D(*args(T=4097)) == pa.POT_ERR_INVALID_ARG
+    assert D(*args(fmt=pa.make_format(mant_bits=2), engine=1)) == pa.POT_ERR_UNSUPPORTED

@@ -48,7 +48,8 @@ def _taps(B, Hq, T):
     return dbg, bufs
 
 
-def assert_v8_parity(d, engine=0, mant_bits=0, hadamard=False, force_splits=0, tol=O_TOL):
+def assert_v8_parity(d, engine=0, mant_bits=0, hadamard=False, force_splits=0, tol=O_TOL,
+                     pow2=False):
     B, Hq, Hkv, T, t_cap = d["B"], d["Hq"], d["Hkv"], d["T"], d["t_cap"]
     rows = d["k_bits"].reshape(-1, 64)
     se, cm, sc = gpu_encode(rows, mant_bits, hadamard)
@@ -67,13 +68,13 @@ def assert_v8_parity(d, engine=0, mant_bits=0, hadamard=False, force_splits=0, t
     ws = pa.alloc_workspace(nws, DEV)
     dbg, bufs = _taps(B, Hq, T)
     dbg.force_splits = force_splits
-    pa.pot_decode_attention_v8(fmt, engine, to_dev(d["q"]), to_dev(se),
-                               to_dev(cm) if cm is not None else None, to_dev(sc), vu, ve,
-                               t_cap, d["kv_head_of_q"], B, Hq, Hkv, T, out, ws, dbg=dbg)
+    call = pa.pot_decode_attention_v8_pow2 if pow2 else pa.pot_decode_attention_v8
+    call(fmt, engine, to_dev(d["q"]), to_dev(se), to_dev(cm) if cm is not None else None,
+         to_dev(sc), vu, ve, t_cap, d["kv_head_of_q"], B, Hq, Hkv, T, out, ws, dbg=dbg)
     torch.cuda.synchronize()
     o = oracle.pot_decode_v8(d["q"], o_se, o_cm, o_sc, o_vh, o_g, t_cap, d["kv_head_of_q"],
                              B, Hq, Hkv, T, mant_bits=mant_bits, hadamard=hadamard,
-                             split_len=dbg.split_len)
+                             split_len=dbg.split_len, pow2=pow2)
     assert np.array_equal(bufs["qhat"].cpu().numpy(), o["qhat"])
     assert np.array_equal(bufs["scores"].cpu().numpy(), o["scores"]), "int32 scores"
     assert np.array_equal(bufs["m_final"].cpu().numpy(), o["m_final"]), "M"
@@ -204,3 +205,69 @@ def test_v8_full_size_b64_t32768_sampled():
             worst = max(worst, err)
     assert worst <= O_TOL, worst
     print(f"INT8-V B=64 T=32768 sampled O err {worst:.3e}")
+
+
+# ---- power-of-two weights (eq. logsm A~ = 2^-k) over the INT8 values ----------------
+@pytest.mark.parametrize("engine", [0, 1])
+def test_pow2_tinyllama_layer_t4096(engine):
+    d = make_decode_inputs(570 + engine, B=1, Hq=32, Hkv=4, T=4096)
+    err, s = assert_v8_parity(d, engine=engine, pow2=True)
+    print(f"pow2 weights engine {engine} T=4096 splits={s} O err {err:.3e}")
+
+
+@pytest.mark.parametrize("T,t_cap", [(1, 8), (255, 264), (4099, 4104)])
+def test_pow2_ragged(T, t_cap):
+    d = make_decode_inputs(580 + T, B=2, Hq=8, Hkv=2, T=T, t_cap=t_cap)
+    assert_v8_parity(d, pow2=True)
+
+
+@pytest.mark.parametrize("splits", [1, 5, 16])
+def test_pow2_forced_splits(splits):
+    d = make_decode_inputs(590 + splits, B=1, Hq=32, Hkv=4, T=4000)
+    assert_v8_parity(d, engine=1, force_splits=splits, pow2=True)
+
+
+def test_pow2_mantissa_hadamard_and_groups():
+    d = make_decode_inputs(600, B=2, Hq=16, Hkv=4, T=1500)
+    assert_v8_parity(d, mant_bits=4, hadamard=True, pow2=True)
+
+
+def test_pow2_mixed_magnitudes():
+    T = 2000
+    d = make_decode_inputs(610, B=2, Hq=8, Hkv=2, T=T)
+    rng = np.random.default_rng(611)
+    v = d["v_bits"].view(np.float16).astype(np.float32)
+    sc = np.exp2(rng.integers(-20, 13, size=(2, 2, d["t_cap"], 1))).astype(np.float32)
+    v[:, :, :T] = v[:, :, :T] * sc[:, :, :T]
+    d["v_bits"] = v.astype(np.float16).view(np.uint16)
+    vmax = float(np.abs(v[:, :, :T]).max())
+    assert_v8_parity(d, tol=5e-4 * vmax, force_splits=2, pow2=True)
+
+
+def test_pow2_full_size_b64_t32768_sampled():
+    B, Hq, Hkv, T = 64, 32, 4, 32768
+    d = make_decode_inputs_device(620, B, Hq, Hkv, T, DEV)
+    fmt = pa.make_format(0)
+    cache = pa.alloc_pot_cache(B, Hkv, T, 0, DEV)
+    pa.pot_encode_keys(fmt, d["k"], B * Hkv * T, 1, 0, cache["key_scale"], cache["codes_se"],
+                       None)
+    vu, ve = pa.alloc_value_cache_int8(B, Hkv, T, DEV)
+    pa.pot_store_values_int8(d["v"], B * Hkv, T, T, 0, vu, ve)
+    ws = pa.alloc_workspace(pa.pot_decode_workspace_bytes(B, Hq, Hkv, T), DEV)
+    out = torch.empty((B, Hq, 64), dtype=torch.float32, device=DEV)
+    pa.pot_decode_attention_v8_pow2(fmt, 0, d["q"], cache["codes_se"], None, cache["key_scale"],
+                                    vu, ve, T, d["kv_head_of_q"], B, Hq, Hkv, T, out, ws)
+    torch.cuda.synchronize()
+    G = Hq // Hkv
+    worst = 0.0
+    for (b, h) in [(0, 0), (40, 2)]:
+        vb = d["v"][b, h].view(torch.uint16).cpu().numpy()
+        o_vh, o_g = oracle.quantize_values(vb)
+        o_se, _, o_sc = oracle.encode_keys(d["k"][b, h].view(torch.uint16).cpu().numpy())
+        qs = d["q"][b, h * G:(h + 1) * G].cpu().numpy()
+        r = oracle.pot_decode_v8(qs[None], o_se, None, o_sc, o_vh, o_g, T, np.zeros(G, np.int32),
+                                 1, G, 1, T, pow2=True)
+        worst = max(worst, float(np.abs(out[b, h * G:(h + 1) * G].cpu().numpy() -
+                                        r["out"][0]).max()))
+    assert worst <= O_TOL, worst
+    print(f"pow2 weights B=64 T=32768 sampled O err {worst:.3e}")
