@@ -11,16 +11,14 @@
 // Per 64-key tile and wave:
 //  1. Scores, one key per lane (Sec. II-B eq. sac). PoT-4: the key's 32 code
 //     bytes arrive as two 16-byte loads. Each query operand holds two
-//     elements of one head as 16-bit halves, (q + 128) 2^7 (prepared once per
+//     elements of one head as signed 16-bit halves, q 2^7 (prepared once per
 //     kv head, read through the scalar cache one code word's group at a
-//     time). v_pk_lshrrev_b16 shifts each half by its element's exponent e:
-//     (q + 128) 2^7 >> e = (q + 128) 2^(7 - e), exact since the low 7 bits
-//     are clear, so every product is formed by the shifter with head-room
-//     F_int = 7 >= e (eq. exact); the zero code gets the shift 15, which
-//     clears the operand. v_dot2_i32_i16 with weights sigma = +-1 flips the
-//     signs and adds both halves into the int32 sum (a signed add; no product
-//     q 2^k goes through a multiplier). A ninth column with q = 0 sums the
-//     +128 bias, 128 sigma 2^(7 - e), and is subtracted from every head.
+//     time). v_pk_ashrrev_i16 shifts each half by its element's exponent e:
+//     q 2^7 >> e = q 2^(7 - e), exact since the low 7 bits are clear, so
+//     every product is formed by the shifter with head-room F_int = 7 >= e
+//     (eq. exact). v_dot2_i32_i16 with weights sigma in {-1, +1} (0 for the
+//     zero code) flips the signs and adds both halves into the int32 sum (a
+//     signed add; no product q 2^k goes through a multiplier).
 //     PoT-Mk uses one int32 accumulator per head: v_alignbit(q, 0, e + 25) =
 //     q << (7 - e) (0 for e = 7), one more per mantissa bit, and v_xad_u32
 //     for the sign (ones' complement, +1 per negative element from a popcount).
@@ -52,7 +50,6 @@ namespace potattn {
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 typedef short s16x2 __attribute__((ext_vector_type(2)));
-typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
 typedef float float4v __attribute__((ext_vector_type(4)));
 
 constexpr int kWaves = kBlock / 64;
@@ -65,6 +62,12 @@ constexpr int kDppRowRor8 = 0x128;  // DPP row_ror:8: lane l reads lane l ^ 8 wi
 __device__ __forceinline__ uint32_t xad_u32(uint32_t a, uint32_t b, uint32_t c) {
   uint32_t r;
   asm("v_xad_u32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+// (m & a) | (~m & b) as one v_bfi_b32
+__device__ __forceinline__ uint32_t bfi_u32(uint32_t m, uint32_t a, uint32_t b) {
+  uint32_t r;
+  asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(r) : "v"(m), "v"(a), "v"(b));
   return r;
 }
 // max(a, b) for scores (never NaN) as v_max_f32 without operand canonicalisation
@@ -209,15 +212,15 @@ __device__ __forceinline__ void mask_values(int t0, int t_end, int lane, ValRegs
 }
 
 // ---- prepared query operands (workspace, one block per kv head) -------------
-// PoT-4: [(c * 4 + n) * (G + 1) + col] = (q + 128) 2^7 of elements 8c + n and
-// 8c + n + 4 as 16-bit halves (col = G: q = 0, the bias column); PoT-Mk:
+// PoT-4: [(c * 4 + n) * G + h] = q 2^7 of elements 8c + n and 8c + n + 4 as
+// signed 16-bit halves; PoT-Mk:
 // [(b' * 64 + m) * G + h] = q << b'; INT8: [i * G + h] four int8 per word;
 // byte decode: [(2c + o) * G + h] four int8 (elements 8c + o + 2t, t = 0..3);
 // fp16: [i * G + h] two fp16 per word. The G per-head score factors follow.
 template <int MODE, int G, int K>
 struct QLayout {
   static constexpr bool kPk = MODE == kScorePot && K == 0;  // packed 16-bit shift operands
-  static constexpr int kCols = G + 1;                          // G heads + the bias column
+  static constexpr int kCols = G;                              // one operand column per head
   static constexpr int kWords = MODE == kScorePot ? (kPk ? 32 * kCols : (K + 1) * kDim * G)
                                 : (MODE == kScoreInt8 || MODE == kScoreDs4a) ? (kDim / 4) * G
                                                      : (kDim / 2) * G;
@@ -297,16 +300,16 @@ __global__ __launch_bounds__(kBlock) void prep_queries_kernel(const DecodeArgs a
   if constexpr (MODE == kScorePot) {
     __syncthreads();
     if constexpr (QL::kPk) {
-      // word ((c * 4 + n) * (G + 1) + col) holds, for elements 8c + n (low
-      // half) and 8c + n + 4 (high half), (q + 128) 2^7 of head col, or
-      // 128 * 2^7 in the bias column col = G: 16-bit operands in [128, 32640]
-      // with 7 clear low bits, so a right shift by e <= 7 is exact
-      for (int i = tid; i < 32 * QL::kCols; i += kBlock) {
-        const int col = i % QL::kCols, cn = i / QL::kCols, n = cn & 3, c = cn >> 2;
+      // word ((c * 4 + n) * G + h) holds, for elements 8c + n (low half) and
+      // 8c + n + 4 (high half), q 2^7 of head h: signed 16-bit operands in
+      // [-16256, 16256] with 7 clear low bits, so an arithmetic right shift
+      // by e <= 6 is exact
+      for (int i = tid; i < 32 * G; i += kBlock) {
+        const int h = i % G, cn = i / G, n = cn & 3, c = cn >> 2;
         const int m = 8 * c + n;
-        const uint32_t lo = (uint32_t)((col < G ? qh[col * kDim + m] : 0) + 128) << 7;
-        const uint32_t hi = (uint32_t)((col < G ? qh[col * kDim + m + 4] : 0) + 128) << 7;
-        qb[i] = (int32_t)(lo | (hi << 16));
+        const uint32_t lo = (uint32_t)(qh[h * kDim + m] * 128) & 0xFFFFu;
+        const uint32_t hi = (uint32_t)(qh[h * kDim + m + 4] * 128) << 16;
+        qb[i] = (int32_t)(lo | hi);
       }
     } else {
       for (int i = tid; i < (K + 1) * kDim * G; i += kBlock) {
@@ -444,26 +447,29 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
       int32_t accv[G];
       if constexpr (kPk) {
         // Two elements of one head per 16-bit-pair operand (element 8c + n in
-        // the low half, 8c + n + 4 in the high half). v_pk_lshrrev_b16 shifts
-        // each half by its element's exponent: (q + 128) 2^7 >> e =
-        // (q + 128) 2^(7 - e), exact; the zero code (e = 7) is given the
-        // shift 15, which clears the operand. v_dot2_i32_i16 with weights
-        // sigma = +-1 per half then flips the signs and adds both halves into
-        // the int32 sum (a signed add: no product q 2^k goes through a
-        // multiplier). The bias column (q = 0) sums 128 sigma 2^(7 - e), which
-        // is subtracted from every head.
-        int32_t a9[kCols];
+        // the low half, 8c + n + 4 in the high half). v_pk_ashrrev_i16 shifts
+        // each half by its element's exponent: q 2^7 >> e = q 2^(7 - e),
+        // exact. v_dot2_i32_i16 with weights sigma = +-1 per half, and 0 for
+        // the zero code (e = 7, whose shifted operand is q), then flips the
+        // signs and adds both halves into the int32 sum (a signed add: no
+        // product q 2^k goes through a multiplier).
 #pragma unroll
-        for (int c = 0; c < kCols; ++c) a9[c] = 0;
+        for (int h = 0; h < G; ++h) accv[h] = 0;
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
           const uint32_t wi = w[i];
-          const uint32_t z = wi & (wi >> 1) & (wi >> 2) & 0x11111111u;  // e = 7 per nibble
-          const uint32_t x = (wi & 0x77777777u) | (z << 3);              // e, or 15 for zero
+          const uint32_t x = wi & 0x77777777u;  // e per nibble
+          // each element's weight as a 4-bit two's complement nibble: 1, -1
+          // for a negative element, 0 for the zero code (e = 7, never
+          // negative): bit 0 is "e != 7", bits 1..3 copy the sign bit
+          const uint32_t s1 = wi >> 1, s2 = wi >> 2;
+          const uint32_t sw = bfi_u32(0x77777777u,
+                                      bfi_u32(0x33333333u, bfi_u32(0x11111111u, ~(wi & s1 & s2), s2), s1),
+                                      wi);
           // this code word's operands, read as one scalar group per tile (a
           // zero offset that depends on the tile keeps the compiler from
-          // hoisting all 32 (G + 1) words out of the loop, where they would
-          // not fit in scalar registers and would spill into vector lanes)
+          // hoisting all 32 G words out of the loop, where they would not fit
+          // in scalar registers and would spill into vector lanes)
           int toff = 0;
           asm("" : "+s"(toff) : "s"(jt));
           uint32_t qq[4 * kCols];
@@ -471,19 +477,17 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
           for (int k = 0; k < 4 * kCols; ++k) qq[k] = (uint32_t)qb[toff + 4 * kCols * i + k];
 #pragma unroll
           for (int n = 0; n < 4; ++n) {
-            const u16x2 sh = __builtin_bit_cast(u16x2, x >> (4 * n)) & (unsigned short)15;
-            const s16x2 sgm = __builtin_bit_cast(s16x2, wi << (12 - 4 * n)) >> (short)15;
-            const s16x2 sg =
-                __builtin_bit_cast(s16x2, __builtin_bit_cast(uint32_t, sgm) | 0x00010001u);
+            const s16x2 sh = __builtin_bit_cast(s16x2, (x >> (4 * n)) & 0x000F000Fu);
+            // the weights of elements 8c + n and 8c + n + 4, sign-extended
+            // from the top nibble of each half
+            const s16x2 sg = __builtin_bit_cast(s16x2, sw << (12 - 4 * n)) >> (short)12;
 #pragma unroll
-            for (int c = 0; c < kCols; ++c) {
-              const u16x2 pv = __builtin_bit_cast(u16x2, qq[kCols * n + c]) >> sh;
-              a9[c] = __builtin_amdgcn_sdot2(__builtin_bit_cast(s16x2, pv), sg, a9[c], false);
+            for (int h = 0; h < G; ++h) {
+              const s16x2 pv = __builtin_bit_cast(s16x2, qq[kCols * n + h]) >> sh;
+              accv[h] = __builtin_amdgcn_sdot2(pv, sg, accv[h], false);
             }
           }
         }
-#pragma unroll
-        for (int h = 0; h < G; ++h) accv[h] = a9[h] - a9[G];
       } else {
         // one head per int32 accumulator; v_xad_u32 applies the sign as a
         // ones' complement and the missing +1 per negative element is added
