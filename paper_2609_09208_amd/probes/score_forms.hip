@@ -1,10 +1,10 @@
 // Score-form probe: the exact int32 PoT-4 score of G = 8 query heads per key
-// (Sec. II-B eq. sac, F = 7) in five gfx950 instruction forms, on the same
+// (Sec. II-B eq. sac, F = 7) in six gfx950 instruction forms, on the same
 // codes and queries. One key per lane, codes streamed from HBM once; every
 // form is checked against a host reference on the first 65536 keys, then
 // timed over 4M keys (128 MiB of codes), where VALU issue binds.
 //
-//  0 sdwa     the decode kernel's core: two heads per 32-bit operand
+//  0 sdwa     an earlier decode kernel core: two heads per 32-bit operand
 //             Q2 = 2 (q_a + 2^16 q_b), SDWA v_lshlrev_b32 reading the shift
 //             (6 - e) mod 32 from a byte, v_xad_u32 for the sign (ones'
 //             complement, +1 per negative element from a popcount), 16-bit
@@ -14,16 +14,21 @@
 //             from a VGPR (no byte select), and the ones' complement costs
 //             -2^s per negative element in the low field, summed by one more
 //             shift-add per element.
-//  2 pk16     v_pk_lshrrev_b16: two elements of one head per operand,
-//             (q + 128) 2^7 >> e = (q + 128) 2^(7 - e) exactly (a right shift
-//             of an operand with 7 clear low bits), zero codes shifted by 15
-//             to 0; v_dot2_i32_i16 with per-element weights +-1 applies the
-//             signs and accumulates both halves; a ninth column with q = 0
-//             removes the +128 bias.
+//  2 pk16     v_pk_lshrrev_b16 (the decode kernel's core before form 5):
+//             two elements of one head per operand, (q + 128) 2^7 >> e =
+//             (q + 128) 2^(7 - e) exactly (a right shift of an operand with 7
+//             clear low bits), zero codes shifted by 15 to 0; v_dot2_i32_i16
+//             with per-element weights +-1 applies the signs and accumulates
+//             both halves; a ninth column with q = 0 removes the +128 bias.
 //  3 ds4a     byte decode (v_perm_b32 table sigma 2^(6 - e)) and v_dot4_i32_i8
 //             (the software packed shift-dot of eq. ds4a; a multiply path).
 //  4 int8     v_dot4_i32_i8 on pre-decoded int8 codes (64 bytes per key): the
 //             INT8 MAC baseline.
+//  5 pk16s    signed operands q 2^7 shifted by v_pk_ashrrev_i16 (exact for
+//             e <= 7), v_dot2_i32_i16 with weights 1 / -1 and 0 for the zero
+//             code, formed per element as 4-bit nibbles by three v_bfi_b32 per
+//             code word and sign-extended per half: no bias column (the
+//             decode kernel's current core).
 // Forms 3 and 4 produce the score at F = 6 and double it.
 //
 // Build and run on a gfx950 device:
@@ -56,7 +61,8 @@ constexpr int kOffSdwa = 0;      // [code word i][32]: 4 steps x (4 pairs elem m
 constexpr int kOffPk = 256;      // [code word i][pair n][9]: 8 heads + the bias column
 constexpr int kOffDs4a = 544;    // [(2c + o) * 8 + h]
 constexpr int kOffInt8 = 672;    // [i * 8 + h], elements 4i .. 4i+3
-constexpr int kOps = 800;
+constexpr int kOffPkS = 800;     // [code word i][pair n][8]: signed q 2^7 halves
+constexpr int kOps = 1056;
 
 typedef short s16x2 __attribute__((ext_vector_type(2)));
 typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
@@ -214,6 +220,36 @@ __device__ __forceinline__ void score_pk16(const uint32_t (&w)[8], const uint32_
   for (int h = 0; h < kG; ++h) acc[h] = a9[h] - a9[kG];
 }
 
+// ---- form 5: signed v_pk_ashrrev_i16 + v_dot2_i32_i16, weights 1 / 0 / -1 ----------
+__device__ __forceinline__ uint32_t bfi_u32(uint32_t m, uint32_t a, uint32_t b) {
+  uint32_t r;
+  asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(r) : "v"(m), "v"(a), "v"(b));
+  return r;
+}
+__device__ __forceinline__ void score_pk16s(const uint32_t (&w)[8], const uint32_t* __restrict__ q,
+                                            int32_t (&acc)[kG]) {
+#pragma unroll
+  for (int h = 0; h < kG; ++h) acc[h] = 0;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const uint32_t wi = w[i];
+    // weight nibble: bit 0 = (e != 7), bits 1..3 = the sign bit
+    const uint32_t s1 = wi >> 1, s2 = wi >> 2;
+    const uint32_t sw =
+        bfi_u32(0x77777777u, bfi_u32(0x33333333u, bfi_u32(0x11111111u, ~(wi & s1 & s2), s2), s1), wi);
+#pragma unroll
+    for (int n = 0; n < 4; ++n) {
+      const s16x2 sh = __builtin_bit_cast(s16x2, (wi >> (4 * n)) & 0x00070007u);
+      const s16x2 sg = __builtin_bit_cast(s16x2, sw << (12 - 4 * n)) >> (short)12;
+#pragma unroll
+      for (int h = 0; h < kG; ++h) {
+        const s16x2 p = __builtin_bit_cast(s16x2, q[kOffPkS + 32 * i + 8 * n + h]) >> sh;
+        acc[h] = __builtin_amdgcn_sdot2(p, sg, acc[h], false);
+      }
+    }
+  }
+}
+
 // ---- form 3: byte decode + v_dot4 (software DS4A) ---------------------------------
 __device__ __forceinline__ void score_ds4a(const uint32_t (&w)[8], const uint32_t* __restrict__ q,
                                            int32_t (&acc)[kG]) {
@@ -282,6 +318,7 @@ __global__ __launch_bounds__(256) void k_score(const uint4* __restrict__ codes,
       if constexpr (FORM == 1) score_lshl_add(w, qk, acc);
       if constexpr (FORM == 2) score_pk16(w, qk, acc);
       if constexpr (FORM == 3) score_ds4a(w, qk, acc);
+      if constexpr (FORM == 5) score_pk16s(w, qk, acc);
     }
     uint32_t s = 0;
 #pragma unroll
@@ -294,9 +331,11 @@ __global__ __launch_bounds__(256) void k_score(const uint4* __restrict__ codes,
 }
 
 typedef void (*KernelFn)(const uint4*, const uint4*, const uint32_t*, int, int32_t*, uint32_t*);
-static const KernelFn kForms[5] = {k_score<0>, k_score<1>, k_score<2>, k_score<3>, k_score<4>};
-static const char* kNames[5] = {"sdwa (decode kernel core)", "lshl_add", "pk16 + dot2",
-                                "ds4a byte decode + dot4", "int8 dot4 (64 B/key)"};
+static const KernelFn kForms[6] = {k_score<0>, k_score<1>, k_score<2>,
+                                   k_score<3>, k_score<4>, k_score<5>};
+static const char* kNames[6] = {"sdwa", "lshl_add", "pk16 + dot2 (bias column)",
+                                "ds4a byte decode + dot4", "int8 dot4 (64 B/key)",
+                                "pk16s signed + dot2"};
 
 static uint64_t g_rng = 0x9E3779B97F4A7C15ull;
 static uint32_t rnd() {
@@ -345,6 +384,12 @@ int main(int argc, char** argv) {
         auto qb = [&](int m) { return (uint32_t)((h < kG ? qh[h][m] : 0) + 128) << 7; };
         ops[kOffPk + 36 * i + 9 * n + h] = qb(8 * i + n) | (qb(8 * i + n + 4) << 16);
       }
+  for (int i = 0; i < 8; ++i)
+    for (int n = 0; n < 4; ++n)
+      for (int h = 0; h < kG; ++h) {
+        auto qs = [&](int m) { return (uint32_t)(qh[h][m] * 128) & 0xFFFFu; };
+        ops[kOffPkS + 32 * i + 8 * n + h] = qs(8 * i + n) | (qs(8 * i + n + 4) << 16);
+      }
   for (int c = 0; c < 8; ++c)
     for (int o = 0; o < 2; ++o)
       for (int h = 0; h < kG; ++h) {
@@ -389,7 +434,7 @@ int main(int argc, char** argv) {
   CHECK(hipEventCreate(&e1));
   std::vector<int32_t> got((size_t)kCheck * kG);
   printf("%-26s %10s %10s %12s %8s\n", "form", "best us", "median us", "keys/ns", "check");
-  for (int f = 0; f < 5; ++f) {
+  for (int f = 0; f < 6; ++f) {
     if (only >= 0 && f != only) continue;
     const dim3 grid_chk(kCheck / 256), grid(cus * 8);
     hipLaunchKernelGGL(kForms[f], grid_chk, dim3(256), 0, 0, d_codes, d_codes8, d_ops, kCheck,

@@ -220,6 +220,26 @@ def test_degenerate_rows_and_query():
     assert_pot_parity(d, mant_bits=1)
 
 
+@pytest.mark.parametrize("engine", ["sac", "ds4a"])
+def test_scores_reach_the_bound(engine):
+    # q^ = +-127 everywhere and keys of equal magnitudes (every code e = 0)
+    # with the signs of the query (and the opposite ones): the scores are the
+    # printed bound +-64 * 127 * 2^7 = +-1 040 384 (Sec. II-C); a third row
+    # runs through every exponent and the zero code, a fourth is all zero
+    d = make_decode_inputs(46, B=1, Hq=8, Hkv=1, T=64)
+    rng = np.random.default_rng(46)
+    sgn = np.where(rng.random(64) < 0.5, -1.0, 1.0)
+    d["q"][0, 0] = sgn.astype(np.float32)
+    k = d["k_bits"].view(np.float16)
+    k[0, 0, 0] = sgn.astype(np.float16)
+    k[0, 0, 1] = (-sgn).astype(np.float16)
+    k[0, 0, 2] = (sgn * np.exp2(-(np.arange(64) % 8))).astype(np.float16)
+    k[0, 0, 3] = 0
+    _, g = assert_pot_parity(d, engine=engine)
+    assert g["scores"][0, 0, 0] == 1040384 and g["scores"][0, 0, 1] == -1040384
+    assert g["scores"][0, 0, 3] == 0
+
+
 @pytest.mark.parametrize("S", [1, 2, 3, 7, 16])
 def test_forced_splits(S):
     d = make_decode_inputs(44, B=1, Hq=32, Hkv=4, T=4000)
