@@ -18,10 +18,11 @@
 //     every product is formed by the shifter with head-room F_int = 7 >= e
 //     (eq. exact). v_dot2_i32_i16 with weights sigma in {-1, +1} (0 for the
 //     zero code) flips the signs and adds both halves into the int32 sum (a
-//     signed add; no product q 2^k goes through a multiplier).
-//     PoT-Mk uses one int32 accumulator per head: v_alignbit(q, 0, e + 25) =
-//     q << (7 - e) (0 for e = 7), one more per mantissa bit, and v_xad_u32
-//     for the sign (ones' complement, +1 per negative element from a popcount).
+//     signed add; no product q 2^k goes through a multiplier). PoT-Mk (Sec.
+//     II-D) adds one sum per mantissa bit plane b over the same shifted
+//     operands, with weight sigma where bit b of the element's mantissa is
+//     set and 0 elsewhere; the key's sum is 2^k S_lead + sum_b 2^b S_b, the
+//     per-bit shifts of eq. sac regrouped by plane.
 //  2. x = fl32(fl32(float(acc) * s) * c), c = fl32(fl32(Delta * log2 e) *
 //     2^-(F+k+3)) in this order; x is staged transposed in wave-private LDS.
 //  3. Integer running maximum M = max(M, ceil(max x)) per head (eq. logsm);
@@ -50,6 +51,7 @@ namespace potattn {
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 typedef short s16x2 __attribute__((ext_vector_type(2)));
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
 typedef float float4v __attribute__((ext_vector_type(4)));
 
 constexpr int kWaves = kBlock / 64;
@@ -212,16 +214,15 @@ __device__ __forceinline__ void mask_values(int t0, int t_end, int lane, ValRegs
 }
 
 // ---- prepared query operands (workspace, one block per kv head) -------------
-// PoT-4: [(c * 4 + n) * G + h] = q 2^7 of elements 8c + n and 8c + n + 4 as
-// signed 16-bit halves; PoT-Mk:
-// [(b' * 64 + m) * G + h] = q << b'; INT8: [i * G + h] four int8 per word;
+// PoT-4 and PoT-Mk: [(c * 4 + n) * G + h] = q 2^7 of elements 8c + n and
+// 8c + n + 4 as signed 16-bit halves;
+// INT8: [i * G + h] four int8 per word;
 // byte decode: [(2c + o) * G + h] four int8 (elements 8c + o + 2t, t = 0..3);
 // fp16: [i * G + h] two fp16 per word. The G per-head score factors follow.
 template <int MODE, int G, int K>
 struct QLayout {
-  static constexpr bool kPk = MODE == kScorePot && K == 0;  // packed 16-bit shift operands
   static constexpr int kCols = G;                              // one operand column per head
-  static constexpr int kWords = MODE == kScorePot ? (kPk ? 32 * kCols : (K + 1) * kDim * G)
+  static constexpr int kWords = MODE == kScorePot ? 32 * kCols
                                 : (MODE == kScoreInt8 || MODE == kScoreDs4a) ? (kDim / 4) * G
                                                      : (kDim / 2) * G;
 };
@@ -299,23 +300,16 @@ __global__ __launch_bounds__(kBlock) void prep_queries_kernel(const DecodeArgs a
   }
   if constexpr (MODE == kScorePot) {
     __syncthreads();
-    if constexpr (QL::kPk) {
-      // word ((c * 4 + n) * G + h) holds, for elements 8c + n (low half) and
-      // 8c + n + 4 (high half), q 2^7 of head h: signed 16-bit operands in
-      // [-16256, 16256] with 7 clear low bits, so an arithmetic right shift
-      // by e <= 6 is exact
-      for (int i = tid; i < 32 * G; i += kBlock) {
-        const int h = i % G, cn = i / G, n = cn & 3, c = cn >> 2;
-        const int m = 8 * c + n;
-        const uint32_t lo = (uint32_t)(qh[h * kDim + m] * 128) & 0xFFFFu;
-        const uint32_t hi = (uint32_t)(qh[h * kDim + m + 4] * 128) << 16;
-        qb[i] = (int32_t)(lo | hi);
-      }
-    } else {
-      for (int i = tid; i < (K + 1) * kDim * G; i += kBlock) {
-        const int h = i % G, bm = i / G, bb = bm / kDim, m = bm % kDim;
-        qb[i] = qh[h * kDim + m] * (1 << bb);
-      }
+    // word ((c * 4 + n) * G + h) holds, for elements 8c + n (low half) and
+    // 8c + n + 4 (high half), q 2^7 of head h: signed 16-bit operands in
+    // [-16256, 16256] with 7 clear low bits, so an arithmetic right shift by
+    // e <= 7 is exact
+    for (int i = tid; i < 32 * G; i += kBlock) {
+      const int h = i % G, cn = i / G, n = cn & 3, c = cn >> 2;
+      const int m = 8 * c + n;
+      const uint32_t lo = (uint32_t)(qh[h * kDim + m] * 128) & 0xFFFFu;
+      const uint32_t hi = (uint32_t)(qh[h * kDim + m + 4] * 128) << 16;
+      qb[i] = (int32_t)(lo | hi);
     }
   }
 }
@@ -343,7 +337,6 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
   __shared__ DecodeSmem sm;
   constexpr bool V8 = VF != 0;
   constexpr bool kPow2 = VF == 2;
-  constexpr bool kPk = QL::kPk;
   constexpr int kCols = QL::kCols;
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -445,85 +438,87 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
       const uint32_t w[8] = {ks.c0.x, ks.c0.y, ks.c0.z, ks.c0.w,
                              ks.c1.x, ks.c1.y, ks.c1.z, ks.c1.w};
       int32_t accv[G];
-      if constexpr (kPk) {
-        // Two elements of one head per 16-bit-pair operand (element 8c + n in
-        // the low half, 8c + n + 4 in the high half). v_pk_ashrrev_i16 shifts
-        // each half by its element's exponent: q 2^7 >> e = q 2^(7 - e),
-        // exact. v_dot2_i32_i16 with weights sigma = +-1 per half, and 0 for
-        // the zero code (e = 7, whose shifted operand is q), then flips the
-        // signs and adds both halves into the int32 sum (a signed add: no
-        // product q 2^k goes through a multiplier).
+      // Two elements of one head per 16-bit-pair operand (element 8c + n in
+      // the low half, 8c + n + 4 in the high half). v_pk_ashrrev_i16 shifts
+      // each half by its element's exponent: q 2^7 >> e = q 2^(7 - e), exact.
+      // v_dot2_i32_i16 with weights sigma = +-1 per half, and 0 for the zero
+      // code (e = 7, whose shifted operand is q), then flips the signs and
+      // adds both halves into the int32 sum (a signed add: no product q 2^k
+      // goes through a multiplier). PoT-Mk: the value is sigma (2^k + j)
+      // 2^-e, so the key's sum is 2^k times the leading sum plus 2^b times
+      // the sum over the elements whose mantissa j has bit b set, each over
+      // the same shifted operands with weights sigma or 0.
+      constexpr int KP = K > 0 ? K : 1;
+      int32_t accm[KP][G];
 #pragma unroll
-        for (int h = 0; h < G; ++h) accv[h] = 0;
+      for (int h = 0; h < G; ++h) {
+        accv[h] = 0;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const uint32_t wi = w[i];
-          const uint32_t x = wi & 0x77777777u;  // e per nibble
-          // each element's weight as a 4-bit two's complement nibble: 1, -1
-          // for a negative element, 0 for the zero code (e = 7, never
-          // negative): bit 0 is "e != 7", bits 1..3 copy the sign bit
-          const uint32_t s1 = wi >> 1, s2 = wi >> 2;
-          const uint32_t sw = bfi_u32(0x77777777u,
-                                      bfi_u32(0x33333333u, bfi_u32(0x11111111u, ~(wi & s1 & s2), s2), s1),
-                                      wi);
-          // this code word's operands, read as one scalar group per tile (a
-          // zero offset that depends on the tile keeps the compiler from
-          // hoisting all 32 G words out of the loop, where they would not fit
-          // in scalar registers and would spill into vector lanes)
-          int toff = 0;
-          asm("" : "+s"(toff) : "s"(jt));
-          uint32_t qq[4 * kCols];
+        for (int bb = 0; bb < KP; ++bb) accm[bb][h] = 0;
+      }
 #pragma unroll
-          for (int k = 0; k < 4 * kCols; ++k) qq[k] = (uint32_t)qb[toff + 4 * kCols * i + k];
+      for (int i = 0; i < 8; ++i) {
+        const uint32_t wi = w[i];
+        const uint32_t x = wi & 0x77777777u;  // e per nibble
+        // each element's weight as a 4-bit two's complement nibble: 1, -1
+        // for a negative element, 0 for the zero code (e = 7, never
+        // negative): bit 0 is "e != 7", bits 1..3 copy the sign bit
+        const uint32_t s1 = wi >> 1, s2 = wi >> 2;
+        const uint32_t sw = bfi_u32(0x77777777u,
+                                    bfi_u32(0x33333333u, bfi_u32(0x11111111u, ~(wi & s1 & s2), s2), s1),
+                                    wi);
+        // the mantissa bits of this code word's 8 elements, one byte per
+        // plane, copied into both halves (bit n for element 8c + n in the
+        // low half, bit n + 4 in the high half)
+        uint32_t pb[KP];
 #pragma unroll
-          for (int n = 0; n < 4; ++n) {
-            const s16x2 sh = __builtin_bit_cast(s16x2, (x >> (4 * n)) & 0x000F000Fu);
-            // the weights of elements 8c + n and 8c + n + 4, sign-extended
-            // from the top nibble of each half
-            const s16x2 sg = __builtin_bit_cast(s16x2, sw << (12 - 4 * n)) >> (short)12;
-#pragma unroll
-            for (int h = 0; h < G; ++h) {
-              const s16x2 pv = __builtin_bit_cast(s16x2, qq[kCols * n + h]) >> sh;
-              accv[h] = __builtin_amdgcn_sdot2(pv, sg, accv[h], false);
-            }
-          }
+        for (int bb = 0; bb < K; ++bb) {
+          const uint32_t pw = (i < 4) ? ks.pl[bb].x : ks.pl[bb].y;
+          pb[bb] = __builtin_amdgcn_perm(pw, pw, (uint32_t)(i & 3) * 0x00010001u | 0x0C000C00u);
         }
-      } else {
-        // one head per int32 accumulator; v_xad_u32 applies the sign as a
-        // ones' complement and the missing +1 per negative element is added
-        // once per key from a popcount of the sign bits
-        int nneg = 0;
+        // this code word's operands, read as one scalar group per tile (a
+        // zero offset that depends on the tile keeps the compiler from
+        // hoisting all 32 G words out of the loop, where they would not fit
+        // in scalar registers and would spill into vector lanes)
+        int toff = 0;
+        asm("" : "+s"(toff) : "s"(jt));
+        uint32_t qq[4 * kCols];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) nneg += __popc(w[i] & 0x88888888u);
-        uint32_t accu[G];
+        for (int k = 0; k < 4 * kCols; ++k) qq[k] = (uint32_t)qb[toff + 4 * kCols * i + k];
 #pragma unroll
-        for (int h = 0; h < G; ++h) accu[h] = 0u;
-#pragma unroll
-        for (int m = 0; m < kDim; ++m) {
-          const uint32_t word = w[m >> 3];
-          const int pos = 4 * (m & 7);
-          const uint32_t sh = ((word >> pos) & 7u) + 25u;
-          const uint32_t sgn = (uint32_t)((int32_t)(word << (28 - pos)) >> 31);
-          uint32_t shb[K > 0 ? K : 1];
+        for (int n = 0; n < 4; ++n) {
+          const s16x2 sh = __builtin_bit_cast(s16x2, (x >> (4 * n)) & 0x000F000Fu);
+          // the weights of elements 8c + n and 8c + n + 4, sign-extended
+          // from the top nibble of each half
+          const s16x2 sg = __builtin_bit_cast(s16x2, sw << (12 - 4 * n)) >> (short)12;
+          s16x2 mw[KP];
 #pragma unroll
           for (int bb = 0; bb < K; ++bb) {
-            const uint32_t plw = (m < 32) ? ks.pl[bb].x : ks.pl[bb].y;
-            const uint32_t msk = (uint32_t)((int32_t)(plw << (31 - (m & 31))) >> 31);
-            // once per element: left to itself the compiler moves this mask
-            // behind the shift and repeats it for every head
-            asm("v_and_b32 %0, %1, %2" : "=v"(shb[bb]) : "v"(sh), "v"(msk));
+            // mantissa bit of each half moved to bit 15 and spread: the
+            // plane's weight is sigma where the bit is set, else 0
+            const u16x2 amt = {(unsigned short)(15 - n), (unsigned short)(11 - n)};
+            const s16x2 bit =
+                __builtin_bit_cast(s16x2, __builtin_bit_cast(u16x2, pb[bb]) << amt) >> (short)15;
+            mw[bb] = bit & sg;
           }
 #pragma unroll
           for (int h = 0; h < G; ++h) {
-            uint32_t term = __builtin_amdgcn_alignbit((uint32_t)qb[(K * kDim + m) * G + h], 0u, sh);
+            const s16x2 pv = __builtin_bit_cast(s16x2, qq[kCols * n + h]) >> sh;
+            accv[h] = __builtin_amdgcn_sdot2(pv, sg, accv[h], false);
 #pragma unroll
             for (int bb = 0; bb < K; ++bb)
-              term += __builtin_amdgcn_alignbit((uint32_t)qb[(bb * kDim + m) * G + h], 0u, shb[bb]);
-            accu[h] = xad_u32(term, sgn, accu[h]);
+              accm[bb][h] = __builtin_amdgcn_sdot2(pv, mw[bb], accm[bb][h], false);
           }
         }
+      }
+      if constexpr (K > 0) {
 #pragma unroll
-        for (int h = 0; h < G; ++h) accv[h] = (int32_t)(accu[h] + (uint32_t)nneg);
+        for (int h = 0; h < G; ++h) {
+          uint32_t t = (uint32_t)accv[h] << K;
+#pragma unroll
+          for (int bb = 0; bb < K; ++bb) t += (uint32_t)accm[bb][h] << bb;
+          accv[h] = (int32_t)t;
+        }
       }
       if (a.frac_bits != kFInt) {  // uniform: rescale to head-room F exactly
 #pragma unroll

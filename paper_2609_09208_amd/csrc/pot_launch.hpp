@@ -91,9 +91,10 @@ struct DecodeArgs {
 };
 
 // 32-bit words of prepared query operands per kv head for group size G:
-// room for the largest layout ((k+1) shifted copies x 64 elements x G heads)
-// plus the G per-head score factors.
-constexpr int query_words(int G) { return ((5 * 64 + 1) * G + 63) / 64 * 64; }
+// room for the largest layout (32 words per head: 16-bit operand pairs for
+// the PoT codes, fp16 pairs for the fp16 comparator) plus the G per-head
+// score factors.
+constexpr int query_words(int G) { return (33 * G + 63) / 64 * 64; }
 
 // Resident workgroups per CU of the (non-debug) decode kernel for this
 // variant, from the HIP occupancy calculator; 0 if the query fails.

@@ -198,6 +198,15 @@ def test_group_sizes(Hq, Hkv):
     assert_pot_parity(d)
 
 
+@pytest.mark.parametrize("k", [0, 1, 2, 3, 4])
+@pytest.mark.parametrize("G", [1, 2, 4, 8])
+def test_every_mantissa_width_and_group(k, G):
+    # every PoT / PoT-Mk score variant of the decode kernel (one per k and
+    # group size), a ragged tail of 700 = 2 * 256 + 188 keys
+    d = make_decode_inputs(60 + 8 * k + G, B=2, Hq=2 * G, Hkv=2, T=700, t_cap=704)
+    assert_pot_parity(d, mant_bits=k)
+
+
 def test_interleaved_head_map():
     d = make_decode_inputs(41, B=2, Hq=8, Hkv=2, T=300)
     d["kv_head_of_q"] = (np.arange(8) % 2).astype(np.int32)
