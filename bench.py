@@ -24,6 +24,9 @@ The line reports:
 - the single-layer configurations (B = 1, T = 4096 PoT-4; B = 1, T = 32768
   PoT-M1; B = 8, T = 32768 Hadamard + PoT-M4 with the fp16 and INT8
   comparators on the same seeds).
+--sweep-point B,T,k (repeatable) and --sweep-layers N restrict the sweep to
+those 22-layer points and change their layer count (one point per process for
+counter runs).
 """
 from __future__ import annotations
 
@@ -325,7 +328,9 @@ def fmt_name(k: int, had: bool) -> str:
     return ("Hadamard + " if had else "") + ("PoT-4" if k == 0 else f"PoT-M{k}")
 
 
-def sweep(pa, dev, steps, warmup):
+def sweep(pa, dev, steps, warmup, only=None, layers=None):
+    """only: keep the points whose (B, T, k) is in this set; layers: layer
+    count override (the counter runs profile one point per process)."""
     import numpy as np
     import torch
     pts = []
@@ -337,7 +342,11 @@ def sweep(pa, dev, steps, warmup):
             dict(B=1, T=32768, k=1, had=False, L=4, compare=True),
             dict(B=8, T=32768, k=4, had=True, L=4, compare=True),
             dict(B=8, T=32768, k=0, had=False, L=4, compare=True)]
+    if only is not None:
+        pts = [p for p in pts if (p["B"], p["T"], p["k"]) in only and not p["compare"]]
     for p in pts:
+        if layers is not None:
+            p["L"] = layers
         lay = Layers(pa, p["B"], p["T"], p["L"], p["k"], p["had"], dev, distinct=False,
                      keep_k16=4 if p["compare"] else 0)
         elapsed, us = time_steps(lay, steps, warmup)
@@ -370,6 +379,10 @@ def main() -> int:
     ap.add_argument("--no-compare", action="store_true")
     ap.add_argument("--sweep", action="store_true",
                     help="one JSON line per workload point instead of the headline line")
+    ap.add_argument("--sweep-point", action="append", default=None, metavar="B,T,k",
+                    help="with --sweep: run only this 22-layer point (repeatable)")
+    ap.add_argument("--sweep-layers", type=int, default=None,
+                    help="with --sweep: layers per point instead of 22")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run device-to-device copies of BYTES bytes (calibrates "
                          "the FETCH_SIZE / WRITE_SIZE counters against a known size)")
@@ -397,7 +410,11 @@ def main() -> int:
         print(json.dumps({"copy_probe_bytes": n, "copies": 3}), flush=True)
         return 0
     if args.sweep:
-        sweep(pa, dev, max(2, min(args.steps, 5)), max(1, min(args.warmup, 2)))
+        only = None
+        if args.sweep_point:
+            only = {tuple(int(v) for v in sp.split(",")) for sp in args.sweep_point}
+        sweep(pa, dev, max(2, min(args.steps, 5)), max(1, min(args.warmup, 2)), only,
+              args.sweep_layers)
         return 0
 
     B, T, L, k = args.batch, args.seq, args.layers, args.mant_bits
