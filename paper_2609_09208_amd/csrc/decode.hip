@@ -451,12 +451,6 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
       constexpr int KP = K > 0 ? K : 1;
       int32_t accm[KP][G];
 #pragma unroll
-      for (int h = 0; h < G; ++h) {
-        accv[h] = 0;
-#pragma unroll
-        for (int bb = 0; bb < KP; ++bb) accm[bb][h] = 0;
-      }
-#pragma unroll
       for (int i = 0; i < 8; ++i) {
         const uint32_t wi = w[i];
         const uint32_t x = wi & 0x77777777u;  // e per nibble
@@ -501,13 +495,19 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
                 __builtin_bit_cast(s16x2, __builtin_bit_cast(u16x2, pb[bb]) << amt) >> (short)15;
             mw[bb] = bit & sg;
           }
+          // the first pair starts each sum from the constant 0; with clamp
+          // set (|sum| <= 2 * 16256, never reached) the compiler emits the
+          // three-operand form instead of zeroing the accumulator first
 #pragma unroll
           for (int h = 0; h < G; ++h) {
             const s16x2 pv = __builtin_bit_cast(s16x2, qq[kCols * n + h]) >> sh;
-            accv[h] = __builtin_amdgcn_sdot2(pv, sg, accv[h], false);
+            accv[h] = (i == 0 && n == 0) ? __builtin_amdgcn_sdot2(pv, sg, 0, true)
+                                         : __builtin_amdgcn_sdot2(pv, sg, accv[h], false);
 #pragma unroll
             for (int bb = 0; bb < K; ++bb)
-              accm[bb][h] = __builtin_amdgcn_sdot2(pv, mw[bb], accm[bb][h], false);
+              accm[bb][h] = (i == 0 && n == 0)
+                                ? __builtin_amdgcn_sdot2(pv, mw[bb], 0, true)
+                                : __builtin_amdgcn_sdot2(pv, mw[bb], accm[bb][h], false);
           }
         }
       }
