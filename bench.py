@@ -12,8 +12,11 @@ calls never hit the previous layer's data in the 256 MB last-level cache.
 
 The line reports:
 - keys scored per second (B * Hq * T * layers per step);
-- the roofline of the decode call: algorithmic bytes per launch over the mean
-  launch time from HIP events on the launch stream, with median and best;
+- the roofline of the decode kernel: algorithmic bytes per launch over its
+  mean time from HIP events that the library records on the launch stream
+  right before and after that kernel (pot_debug.decode_begin / decode_end),
+  with median and best; the whole call (query prep with the append, decode,
+  split combine) is reported beside it as call_us / frac_call;
 - speed-up over the in-repo fp16 and INT8 kernels on the same shape;
 - the CPU oracle timed on host cores on a bounded sample, with one thread and
   with all threads.
@@ -199,21 +202,28 @@ class Layers:
                                      c["key_scale"], c["v"], self.T, self.heads, self.B, HQ,
                                      HKV, self.T, self.out, self.ws)
 
-    def step(self, events=None):
+    def step(self, events=None, kernel_events=None):
+        """events[i]: HIP events recorded around layer i's call; kernel_events[i]:
+        pot_debug structs whose decode_begin / decode_end events the library
+        records around the decode kernel alone."""
         pa, T, B = self.pa, self.T, self.B
         for i, c in enumerate(self.layers):
             if events is not None:
                 events[i][0].record()
             pa.pot_append_decode_attention(self.fmt, c["q"], c["new_k"], c["new_v"],
                                            c["codes_se"], c["codes_m"], c["key_scale"], c["v"],
-                                           T, self.heads, B, HQ, HKV, T, self.out, self.ws)
+                                           T, self.heads, B, HQ, HKV, T, self.out, self.ws,
+                                           dbg=kernel_events[i] if kernel_events else None)
             if events is not None:
                 events[i][1].record()
 
 
-def time_steps(lay, steps, warmup):
-    """Wall time of `steps` steps and the per-launch decode times (us) from
-    HIP events recorded on the launch stream."""
+def time_steps(lay, steps, warmup, kernel_times=False):
+    """Wall time of `steps` steps and the per-call decode times (us) from HIP
+    events recorded on the launch stream around each call (query prep with
+    the append, decode kernel, split combine). With kernel_times, also the
+    decode kernel's own times (us), from events the library records on the
+    same stream right before and after that kernel."""
     import numpy as np
     import torch
     for _ in range(warmup):
@@ -221,13 +231,31 @@ def time_steps(lay, steps, warmup):
     torch.cuda.synchronize()
     ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
            for _ in range(lay.L)] for _ in range(steps)]
+    kev = kdbg = None
+    if kernel_times:
+        kev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                for _ in range(lay.L)] for _ in range(steps)]
+        kdbg = []
+        for row in kev:
+            dl = []
+            for a, b in row:
+                a.record()  # creates the HIP events behind the handles
+                b.record()
+                d = lay.pa.pot_debug()
+                d.decode_begin, d.decode_end = a.cuda_event, b.cuda_event
+                dl.append(d)
+            kdbg.append(dl)
+        torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(steps):
-        lay.step(ev[s])
+        lay.step(ev[s], kdbg[s] if kdbg else None)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     us = np.array([a.elapsed_time(b) for row in ev for (a, b) in row]) * 1e3
-    return elapsed, us
+    if not kernel_times:
+        return elapsed, us
+    kus = np.array([a.elapsed_time(b) for row in kev for (a, b) in row]) * 1e3
+    return elapsed, us, kus
 
 
 def timed_calls(fn, n_layers, reps=10, warm=2):
@@ -421,8 +449,9 @@ def main() -> int:
     lay = Layers(pa, B, T, L, k, False, dev, distinct=True,
                  keep_k16=0 if args.no_compare else 4)
     torch.cuda.synchronize()
-    elapsed, us = time_steps(lay, args.steps, args.warmup)
-    kern_s = float(us.mean()) * 1e-6
+    elapsed, us, kus = time_steps(lay, args.steps, args.warmup, kernel_times=True)
+    kern_s = float(kus.mean()) * 1e-6
+    call_s = float(us.mean()) * 1e-6
     alg = algorithmic_bytes(B, T, row_bytes(k))
     achieved = alg / kern_s / 1e9
 
@@ -440,13 +469,16 @@ def main() -> int:
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": read_traffic() if (B, T, k) == (64, 32768, 0) else None,
-                     "kernel": "potattn::decode_kernel<PoT,G=8> (+ query prep with the fused append, and combine)",
+                     "kernel": f"potattn::decode_kernel<0, 8, {k}, false, 0> (SAC, G = 8, fp16 V)",
                      "alg_bytes_per_launch": alg, "launch_us": kern_s * 1e6,
-                     "launch_us_median": float(np.median(us)), "launch_us_best": float(us.min()),
-                     "launches_timed": int(us.size),
+                     "launch_us_median": float(np.median(kus)), "launch_us_best": float(kus.min()),
+                     "launches_timed": int(kus.size),
+                     "call_us": call_s * 1e6, "call_us_median": float(np.median(us)),
+                     "frac_call": alg / call_s / 1e9 / HBM_PEAK_GBS,
                      "read_ceiling_gbs": read_ceiling(),
                      "frac_of_read_ceiling": achieved / read_ceiling() if read_ceiling() else None,
-                     "keys_scored_per_s_kernel": B * HQ * T / kern_s},
+                     "keys_scored_per_s_kernel": B * HQ * T / kern_s,
+                     "keys_scored_per_s_call": B * HQ * T / call_s},
     }
     if not args.no_compare:
         result["comparators"] = comparators(pa, lay, dev)

@@ -106,6 +106,12 @@ typedef struct pot_format {
  *  force_splits (in)  if > 0, use this many key splits instead of the planner
  *  n_splits     (out) the number of key splits used (written on the host)
  *  split_len    (out) keys per split (the last split may be shorter)
+ *  decode_begin, decode_end (in) NULL, or hipEvent_t handles the caller
+ *               created: the call records decode_begin on its stream right
+ *               before the decode kernel and decode_end right after it (before
+ *               the split combine), so that kernel can be timed alone. They
+ *               do not select the instrumented build. A failed record returns
+ *               POT_ERR_HIP.
  */
 typedef struct pot_debug {
   int8_t* qhat;
@@ -116,6 +122,8 @@ typedef struct pot_debug {
   int32_t force_splits;
   int32_t n_splits;
   int32_t split_len;
+  void* decode_begin;
+  void* decode_end;
 } pot_debug;
 
 /* Static string for a status code. Never NULL. */

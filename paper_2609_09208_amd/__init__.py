@@ -41,7 +41,8 @@ class pot_debug(ctypes.Structure):
     _fields_ = [("qhat", ctypes.c_void_p), ("delta", ctypes.c_void_p),
                 ("scores", ctypes.c_void_p), ("m_final", ctypes.c_void_p),
                 ("m_split", ctypes.c_void_p), ("force_splits", ctypes.c_int32),
-                ("n_splits", ctypes.c_int32), ("split_len", ctypes.c_int32)]
+                ("n_splits", ctypes.c_int32), ("split_len", ctypes.c_int32),
+                ("decode_begin", ctypes.c_void_p), ("decode_end", ctypes.c_void_p)]
 
 
 def make_format(mant_bits: int = 0, frac_bits: int = 7, hadamard: bool = False,

@@ -211,7 +211,10 @@ pot_status decode_common(int mode, int mant_bits, DecodeArgs& a, const int32_t* 
   a.n_splits = p.n_splits;
   a.split_len = p.split_len;
   bool debug = false;
+  hipEvent_t ev_begin = nullptr, ev_end = nullptr;
   if (dbg) {
+    ev_begin = static_cast<hipEvent_t>(dbg->decode_begin);
+    ev_end = static_cast<hipEvent_t>(dbg->decode_end);
     a.dbg_qhat = dbg->qhat;
     a.dbg_delta = dbg->delta;
     a.dbg_scores = dbg->scores;
@@ -224,7 +227,8 @@ pot_status decode_common(int mode, int mant_bits, DecodeArgs& a, const int32_t* 
       return fail(POT_ERR_UNSUPPORTED, "debug taps are not available on the fp16 path");
   }
   return hip_status(
-      launch_decode(mode, G, mant_bits, debug, vf, a, static_cast<hipStream_t>(stream)),
+      launch_decode(mode, G, mant_bits, debug, vf, a, static_cast<hipStream_t>(stream), ev_begin,
+                    ev_end),
       "decode launch");
 }
 

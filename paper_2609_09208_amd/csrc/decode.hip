@@ -868,20 +868,22 @@ __global__ __launch_bounds__(64) void combine_kernel(const DecodeArgs a) {
 }
 
 template <int MODE, int G, int K, bool DEBUG, int VF>
-static hipError_t launch_t(const DecodeArgs& a, hipStream_t stream) {
+static hipError_t launch_t(const DecodeArgs& a, hipStream_t stream, hipEvent_t ev_begin,
+                           hipEvent_t ev_end) {
   if constexpr (VF != 0 && MODE != kScorePot && MODE != kScoreDs4a) {
     return hipErrorInvalidValue;
   } else {
   hipLaunchKernelGGL((prep_queries_kernel<MODE, G, K, DEBUG>), dim3((uint32_t)a.Hkv, (uint32_t)a.B),
                      dim3(kBlock), 0, stream, a);
-  const hipError_t e = hipGetLastError();
+  hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (ev_begin != nullptr && (e = hipEventRecord(ev_begin, stream)) != hipSuccess) return e;
   const dim3 grid((uint32_t)a.n_splits, (uint32_t)a.Hkv, (uint32_t)a.B);
   hipLaunchKernelGGL((decode_kernel<MODE, G, K, DEBUG, VF>), grid, dim3(kBlock), 0, stream, a,
                      static_cast<const int32_t*>(a.qbuf));
-  if (a.n_splits == 1) return hipGetLastError();
-  const hipError_t e2 = hipGetLastError();
-  if (e2 != hipSuccess) return e2;
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (ev_end != nullptr && (e = hipEventRecord(ev_end, stream)) != hipSuccess) return e;
+  if (a.n_splits == 1) return hipSuccess;
   hipLaunchKernelGGL((combine_kernel<DEBUG>), dim3((uint32_t)(a.B * a.Hq)), dim3(64), 0, stream,
                      a);
   return hipGetLastError();
@@ -932,61 +934,64 @@ int decode_occupancy(int mode, int G, int mant_bits, int vf) {
 }
 
 template <int MODE, int G, bool DEBUG, int VF>
-static hipError_t launch_k(int mant_bits, const DecodeArgs& a, hipStream_t stream) {
+static hipError_t launch_k(int mant_bits, const DecodeArgs& a, hipStream_t stream, hipEvent_t e0,
+                           hipEvent_t e1) {
   if constexpr (MODE != kScorePot) {
-    return launch_t<MODE, G, 0, DEBUG, VF>(a, stream);
+    return launch_t<MODE, G, 0, DEBUG, VF>(a, stream, e0, e1);
   } else {
     switch (mant_bits) {
-      case 0: return launch_t<MODE, G, 0, DEBUG, VF>(a, stream);
-      case 1: return launch_t<MODE, G, 1, DEBUG, VF>(a, stream);
-      case 2: return launch_t<MODE, G, 2, DEBUG, VF>(a, stream);
-      case 3: return launch_t<MODE, G, 3, DEBUG, VF>(a, stream);
-      case 4: return launch_t<MODE, G, 4, DEBUG, VF>(a, stream);
+      case 0: return launch_t<MODE, G, 0, DEBUG, VF>(a, stream, e0, e1);
+      case 1: return launch_t<MODE, G, 1, DEBUG, VF>(a, stream, e0, e1);
+      case 2: return launch_t<MODE, G, 2, DEBUG, VF>(a, stream, e0, e1);
+      case 3: return launch_t<MODE, G, 3, DEBUG, VF>(a, stream, e0, e1);
+      case 4: return launch_t<MODE, G, 4, DEBUG, VF>(a, stream, e0, e1);
       default: return hipErrorInvalidValue;
     }
   }
 }
 
 template <int MODE, bool DEBUG, int VF>
-static hipError_t launch_g(int G, int mant_bits, const DecodeArgs& a, hipStream_t stream) {
+static hipError_t launch_g(int G, int mant_bits, const DecodeArgs& a, hipStream_t stream,
+                           hipEvent_t e0, hipEvent_t e1) {
   switch (G) {
-    case 1: return launch_k<MODE, 1, DEBUG, VF>(mant_bits, a, stream);
-    case 2: return launch_k<MODE, 2, DEBUG, VF>(mant_bits, a, stream);
-    case 4: return launch_k<MODE, 4, DEBUG, VF>(mant_bits, a, stream);
-    case 8: return launch_k<MODE, 8, DEBUG, VF>(mant_bits, a, stream);
+    case 1: return launch_k<MODE, 1, DEBUG, VF>(mant_bits, a, stream, e0, e1);
+    case 2: return launch_k<MODE, 2, DEBUG, VF>(mant_bits, a, stream, e0, e1);
+    case 4: return launch_k<MODE, 4, DEBUG, VF>(mant_bits, a, stream, e0, e1);
+    case 8: return launch_k<MODE, 8, DEBUG, VF>(mant_bits, a, stream, e0, e1);
     default: return hipErrorInvalidValue;
   }
 }
 
 template <int VF>
 static hipError_t launch_v(int mode, int G, int mant_bits, bool debug, const DecodeArgs& a,
-                           hipStream_t stream) {
+                           hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
   switch (mode) {
     case kScorePot:
-      return debug ? launch_g<kScorePot, true, VF>(G, mant_bits, a, stream)
-                   : launch_g<kScorePot, false, VF>(G, mant_bits, a, stream);
+      return debug ? launch_g<kScorePot, true, VF>(G, mant_bits, a, stream, e0, e1)
+                   : launch_g<kScorePot, false, VF>(G, mant_bits, a, stream, e0, e1);
     case kScoreDs4a:
-      return debug ? launch_g<kScoreDs4a, true, VF>(G, 0, a, stream)
-                   : launch_g<kScoreDs4a, false, VF>(G, 0, a, stream);
+      return debug ? launch_g<kScoreDs4a, true, VF>(G, 0, a, stream, e0, e1)
+                   : launch_g<kScoreDs4a, false, VF>(G, 0, a, stream, e0, e1);
     case kScoreInt8:
       if constexpr (VF != 0) return hipErrorInvalidValue;
       else
-        return debug ? launch_g<kScoreInt8, true, 0>(G, 0, a, stream)
-                     : launch_g<kScoreInt8, false, 0>(G, 0, a, stream);
+        return debug ? launch_g<kScoreInt8, true, 0>(G, 0, a, stream, e0, e1)
+                     : launch_g<kScoreInt8, false, 0>(G, 0, a, stream, e0, e1);
     case kScoreFp16:
       if constexpr (VF != 0) return hipErrorInvalidValue;
-      else return launch_g<kScoreFp16, false, 0>(G, 0, a, stream);
+      else return launch_g<kScoreFp16, false, 0>(G, 0, a, stream, e0, e1);
     default:
       return hipErrorInvalidValue;
   }
 }
 
 hipError_t launch_decode(int mode, int G, int mant_bits, bool debug, int vf,
-                         const DecodeArgs& a, hipStream_t stream) {
+                         const DecodeArgs& a, hipStream_t stream, hipEvent_t ev_begin,
+                         hipEvent_t ev_end) {
   switch (vf) {
-    case 0: return launch_v<0>(mode, G, mant_bits, debug, a, stream);
-    case 1: return launch_v<1>(mode, G, mant_bits, debug, a, stream);
-    case 2: return launch_v<2>(mode, G, mant_bits, debug, a, stream);
+    case 0: return launch_v<0>(mode, G, mant_bits, debug, a, stream, ev_begin, ev_end);
+    case 1: return launch_v<1>(mode, G, mant_bits, debug, a, stream, ev_begin, ev_end);
+    case 2: return launch_v<2>(mode, G, mant_bits, debug, a, stream, ev_begin, ev_end);
     default: return hipErrorInvalidValue;
   }
 }

@@ -103,7 +103,10 @@ int decode_occupancy(int mode, int G, int mant_bits, int vf);
 // vf: value format. 0: fp16 value cache (a.v); 1: INT8 value cache (a.v8,
 // a.v_exp); 2: INT8 values with the power-of-two weights of eq. logsm.
 // Formats 1 and 2 exist for the score modes kScorePot and kScoreDs4a only.
+// ev_begin / ev_end (may be null) are recorded on the stream right before and
+// right after the decode kernel.
 hipError_t launch_decode(int mode, int G, int mant_bits, bool debug, int vf,
-                         const DecodeArgs& a, hipStream_t stream);
+                         const DecodeArgs& a, hipStream_t stream, hipEvent_t ev_begin = nullptr,
+                         hipEvent_t ev_end = nullptr);
 
 }  // namespace potattn

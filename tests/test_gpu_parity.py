@@ -273,6 +273,42 @@ def test_split_invariance_and_determinism():
     assert np.abs(outs[0] - outs[1]).max() < 1e-5
 
 
+@pytest.mark.parametrize("S", [1, 4])
+def test_decode_kernel_events(S):
+    # pot_debug.decode_begin / decode_end: the library records the caller's
+    # events around the decode kernel alone; the output is unchanged and the
+    # kernel's time lies inside the call's
+    d = make_decode_inputs(47, B=4, Hq=32, Hkv=4, T=4096)
+    B, Hq, Hkv, T = 4, 32, 4, 4096
+    se, _, sc = gpu_encode(d["k_bits"].reshape(-1, 64), 0)
+    fmt = pa.make_format(0)
+    q, se_d, sc_d = to_dev(d["q"]), to_dev(se), to_dev(sc)
+    v = store_values(d["v_bits"], B, Hkv, d["t_cap"])
+    ws = pa.alloc_workspace(pa.pot_decode_workspace_bytes_for_splits(B, Hq, Hkv, T, S), DEV)
+    outs = []
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    for with_events in (False, True):
+        out = torch.empty((B, Hq, 64), dtype=torch.float32, device=DEV)
+        dbg = pa.pot_debug()
+        dbg.force_splits = S
+        if with_events:
+            for e in ev:
+                e.record()  # creates the HIP events
+            dbg.decode_begin, dbg.decode_end = ev[1].cuda_event, ev[2].cuda_event
+            ev[0].record()
+        pa.pot_decode_attention(fmt, q, se_d, None, sc_d, v, d["t_cap"], d["kv_head_of_q"], B,
+                                Hq, Hkv, T, out, ws, dbg=dbg)
+        if with_events:
+            ev[3].record()
+        torch.cuda.synchronize()
+        outs.append(out.cpu().numpy())
+        assert dbg.n_splits == S
+    assert np.array_equal(outs[0], outs[1])
+    call_ms, kern_ms = ev[0].elapsed_time(ev[3]), ev[1].elapsed_time(ev[2])
+    assert 0 < kern_ms <= call_ms
+    assert ev[0].elapsed_time(ev[1]) >= 0 and ev[2].elapsed_time(ev[3]) >= 0
+
+
 # ---- comparison kernels ------------------------------------------------------------
 @pytest.mark.parametrize("had", [False, True])
 def test_int8_decode_parity(had):
