@@ -217,10 +217,11 @@ pot_status pot_workspace_init(void* workspace, size_t ws_bytes, void* stream);
  *               time.
  * Steps: q is rotated (if hadamard) and quantised to int8 with step
  * Delta = amax/127; each score is the exact int32 sum of sign-flipped
- * shifts of q^ (eq. sac: q^ 2^(F-e), for PoT-4 formed by packed 16-bit shifts
- * and summed with +-1 weights by v_dot2_i32_i16); x = acc * s * Delta *
- * log2(e) * 2^-(F+k) / 8 in a
- * fixed fp32 order; the running maximum is the integer M = ceil(max x)
+ * shifts of q^ (eq. sac: q^ 2^(F-e), formed by packed 16-bit arithmetic
+ * shifts of q^ 2^7 and summed with weights +-1, 0 for the zero code, by
+ * v_dot2_i32_i16; PoT-Mk adds one such sum per mantissa bit plane, combined
+ * by shifts); x = acc * s * Delta * log2(e) * 2^-(F+k) / 8 in a fixed fp32
+ * order; the running maximum is the integer M = ceil(max x)
  * (eq. logsm) so rescales are exact powers of two; weights 2^(x-M) multiply
  * the fp16 values with fp32 accumulation (matrix cores, weights split into
  * fp16 high and low parts); key splits (chosen to fill the GPU's resident
