@@ -179,7 +179,8 @@ pot_status decode_common(int mode, int mant_bits, DecodeArgs& a, const int32_t* 
       return fail(POT_ERR_INVALID_ARG, "q, v and out must be 16-byte aligned");
   }
   if (!workspace) return fail(POT_ERR_INVALID_ARG, "workspace is NULL");
-  if (!aligned(workspace, 256)) return fail(POT_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  if (!aligned(workspace, 256))
+    return fail(POT_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
   int G = 0;
   pot_status st = check_heads(map, Hq, Hkv, &a, &G);
   if (st != POT_OK) return st;

@@ -458,9 +458,8 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
         // for a negative element, 0 for the zero code (e = 7, never
         // negative): bit 0 is "e != 7", bits 1..3 copy the sign bit
         const uint32_t s1 = wi >> 1, s2 = wi >> 2;
-        const uint32_t sw = bfi_u32(0x77777777u,
-                                    bfi_u32(0x33333333u, bfi_u32(0x11111111u, ~(wi & s1 & s2), s2), s1),
-                                    wi);
+        const uint32_t sw0 = bfi_u32(0x11111111u, ~(wi & s1 & s2), s2);
+        const uint32_t sw = bfi_u32(0x77777777u, bfi_u32(0x33333333u, sw0, s1), wi);
         // the mantissa bits of this code word's 8 elements, one byte per
         // plane, copied into both halves (bit n for element 8c + n in the
         // low half, bit n + 4 in the high half)
@@ -738,7 +737,8 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
     uint32_t a0w[4], a1w[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const uint32_t rl = (uint32_t)__builtin_amdgcn_mov_dpp((int)lw[i], kDppRowRor8, 0xF, 0xF, true);
+      const uint32_t rl =
+          (uint32_t)__builtin_amdgcn_mov_dpp((int)lw[i], kDppRowRor8, 0xF, 0xF, true);
       a0w[i] = part ? rl : hw[i];
       a1w[i] = part ? hw[i] : rl;
     }

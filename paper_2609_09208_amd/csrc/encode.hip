@@ -43,42 +43,54 @@ EncodeTables make_encode_tables(int mant_bits) {
   return t;
 }
 
+// The row-per-wave kernels below step over rows with the grid's stride: a
+// launch has at most kMaxGrid workgroups, since a dispatch is limited to
+// 2^32 work-items per dimension (2^26 rows of one wave each).
+constexpr int64_t kMaxGrid = 1 << 20;
+
+inline uint32_t bounded_grid(int64_t blocks) {
+  return (uint32_t)(blocks < kMaxGrid ? blocks : kMaxGrid);
+}
+
 __global__ __launch_bounds__(kBlock) void encode_pot_kernel(
     const __half* __restrict__ k, int64_t n_rows, int64_t out_stride, int scale_mode,
     int hadamard, float* __restrict__ key_scale, uint8_t* __restrict__ codes_se,
     uint8_t* __restrict__ codes_m, EncodeTables tab) {
-  const int64_t row = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
-  if (row >= n_rows) return;  // uniform per wave
-  const int64_t orow = row * out_stride;
-  encode_key_row_wave(k + row * kDim, hadamard, scale_mode, key_scale + orow,
-                      codes_se + orow * (kDim / 2), codes_m + orow * 8 * tab.mant_bits, tab);
+  const int64_t stride = (int64_t)gridDim.x * (kBlock / 64);
+  for (int64_t row = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6); row < n_rows;
+       row += stride) {  // uniform per wave
+    const int64_t orow = row * out_stride;
+    encode_key_row_wave(k + row * kDim, hadamard, scale_mode, key_scale + orow,
+                        codes_se + orow * (kDim / 2), codes_m + orow * 8 * tab.mant_bits, tab);
+  }
 }
 
 __global__ __launch_bounds__(kBlock) void encode_int8_kernel(
     const __half* __restrict__ k, int64_t n_rows, int64_t out_stride, int hadamard,
     float* __restrict__ key_scale, int8_t* __restrict__ codes) {
   const int lane = lane_id();
-  const int64_t row = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
-  if (row >= n_rows) return;
-  float x = __half2float(k[row * kDim + lane]);
-  if (hadamard) x = (float)(wave_fwht64((double)x) * 0.125);
-  float step;
-  const int c = wave_quantize_int8(x, &step);
-  const int64_t orow = row * out_stride;
-  codes[orow * kDim + lane] = (int8_t)c;
-  if (lane == 0) key_scale[orow] = step;
+  const int64_t stride = (int64_t)gridDim.x * (kBlock / 64);
+  for (int64_t row = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6); row < n_rows;
+       row += stride) {  // uniform per wave
+    float x = __half2float(k[row * kDim + lane]);
+    if (hadamard) x = (float)(wave_fwht64((double)x) * 0.125);
+    float step;
+    const int c = wave_quantize_int8(x, &step);
+    const int64_t orow = row * out_stride;
+    codes[orow * kDim + lane] = (int8_t)c;
+    if (lane == 0) key_scale[orow] = step;
+  }
 }
 
 // Value-cache store: token t of sequence s, dim d lives at
 // ((s * t_cap + (t/8)*8) * 64 + d * 8 + t % 8) halves. One thread per
 // (sequence, 8-token group, dim) gathers the group's 8 tokens of its dim and
 // writes them as one 16-byte word (or only the tokens inside [t0, t0+n_tok)
-// at the ends of the range).
-__global__ __launch_bounds__(256) void store_values_kernel(
-    const uint16_t* __restrict__ src, int64_t n_seq, int64_t n_tok, int64_t t_cap, int64_t t0,
-    int64_t g_first, int64_t n_groups, uint16_t* __restrict__ dst) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n_seq * n_groups * kDim) return;
+// at the ends of the range). i indexes (sequence, group, dim).
+__device__ __forceinline__ void store_value_group(const uint16_t* __restrict__ src, int64_t n_tok,
+                                                  int64_t t_cap, int64_t t0, int64_t g_first,
+                                                  int64_t n_groups, uint16_t* __restrict__ dst,
+                                                  int64_t i) {
   const int d = (int)(i % kDim);
   const int64_t sg = i / kDim;
   const int64_t s = sg / n_groups, g = g_first + sg % n_groups;
@@ -108,6 +120,15 @@ __global__ __launch_bounds__(256) void store_values_kernel(
   }
 }
 
+__global__ __launch_bounds__(256) void store_values_kernel(
+    const uint16_t* __restrict__ src, int64_t n_seq, int64_t n_tok, int64_t t_cap, int64_t t0,
+    int64_t g_first, int64_t n_groups, uint16_t* __restrict__ dst) {
+  const int64_t n = n_seq * n_groups * kDim;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    store_value_group(src, n_tok, t_cap, t0, g_first, n_groups, dst, i);
+}
+
 hipError_t launch_store_values(const uint16_t* src, int64_t n_seq, int64_t n_tok, int64_t t_cap,
                                int64_t t0, uint16_t* dst, hipStream_t stream) {
   if (n_seq == 0 || n_tok == 0) return hipSuccess;
@@ -115,8 +136,8 @@ hipError_t launch_store_values(const uint16_t* src, int64_t n_seq, int64_t n_tok
   const int64_t n_groups = g_last - g_first + 1;
   const int64_t n = n_seq * n_groups * kDim;
   const int64_t grid = (n + 255) / 256;
-  hipLaunchKernelGGL(store_values_kernel, dim3((uint32_t)grid), dim3(256), 0, stream, src, n_seq,
-                     n_tok, t_cap, t0, g_first, n_groups, dst);
+  hipLaunchKernelGGL(store_values_kernel, dim3(bounded_grid(grid)), dim3(256), 0, stream, src,
+                     n_seq, n_tok, t_cap, t0, g_first, n_groups, dst);
   return hipGetLastError();
 }
 
@@ -125,10 +146,12 @@ hipError_t launch_store_values(const uint16_t* src, int64_t n_seq, int64_t n_tok
 __global__ __launch_bounds__(kBlock) void store_values_i8_kernel(
     const uint16_t* __restrict__ src, int64_t n_seq, int64_t n_tok, int64_t t_cap, int64_t t0,
     uint8_t* __restrict__ v_u8, int8_t* __restrict__ v_exp) {
-  const int64_t r = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
-  if (r >= n_seq * n_tok) return;  // uniform per wave
-  const int64_t s = r / n_tok, t = t0 + r % n_tok;
-  store_value_token_i8_wave(src + r * kDim, v_u8 + s * t_cap * kDim, v_exp + s * t_cap, t);
+  const int64_t stride = (int64_t)gridDim.x * (kBlock / 64);
+  for (int64_t r = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6); r < n_seq * n_tok;
+       r += stride) {  // uniform per wave
+    const int64_t s = r / n_tok, t = t0 + r % n_tok;
+    store_value_token_i8_wave(src + r * kDim, v_u8 + s * t_cap * kDim, v_exp + s * t_cap, t);
+  }
 }
 
 hipError_t launch_store_values_i8(const uint16_t* src, int64_t n_seq, int64_t n_tok,
@@ -137,16 +160,18 @@ hipError_t launch_store_values_i8(const uint16_t* src, int64_t n_seq, int64_t n_
   if (n_seq == 0 || n_tok == 0) return hipSuccess;
   const int64_t rows = n_seq * n_tok;
   const int64_t grid = (rows + kBlock / 64 - 1) / (kBlock / 64);
-  hipLaunchKernelGGL(store_values_i8_kernel, dim3((uint32_t)grid), dim3(kBlock), 0, stream, src,
-                     n_seq, n_tok, t_cap, t0, v_u8, v_exp);
+  hipLaunchKernelGGL(store_values_i8_kernel, dim3(bounded_grid(grid)), dim3(kBlock), 0, stream,
+                     src, n_seq, n_tok, t_cap, t0, v_u8, v_exp);
   return hipGetLastError();
 }
 
 __global__ void fill_zero_kernel(uint32_t* __restrict__ p, size_t n_words, uint8_t* tail,
                                  size_t tail_bytes) {
-  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n_words) p[i] = 0u;
-  if (i < tail_bytes) tail[i] = 0;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_words || i < tail_bytes;
+       i += (size_t)gridDim.x * blockDim.x) {
+    if (i < n_words) p[i] = 0u;
+    if (i < tail_bytes) tail[i] = 0;
+  }
 }
 
 hipError_t launch_encode_pot(const uint16_t* k, int64_t n_rows, int64_t out_stride,
@@ -156,7 +181,7 @@ hipError_t launch_encode_pot(const uint16_t* k, int64_t n_rows, int64_t out_stri
   if (n_rows == 0) return hipSuccess;
   const int64_t rows_per_block = kBlock / 64;
   const int64_t grid = (n_rows + rows_per_block - 1) / rows_per_block;
-  hipLaunchKernelGGL(encode_pot_kernel, dim3((uint32_t)grid), dim3(kBlock), 0, stream,
+  hipLaunchKernelGGL(encode_pot_kernel, dim3(bounded_grid(grid)), dim3(kBlock), 0, stream,
                      reinterpret_cast<const __half*>(k), n_rows, out_stride, scale_mode,
                      hadamard, key_scale, codes_se, codes_m, tab);
   return hipGetLastError();
@@ -168,7 +193,7 @@ hipError_t launch_encode_int8(const uint16_t* k, int64_t n_rows, int64_t out_str
   if (n_rows == 0) return hipSuccess;
   const int64_t rows_per_block = kBlock / 64;
   const int64_t grid = (n_rows + rows_per_block - 1) / rows_per_block;
-  hipLaunchKernelGGL(encode_int8_kernel, dim3((uint32_t)grid), dim3(kBlock), 0, stream,
+  hipLaunchKernelGGL(encode_int8_kernel, dim3(bounded_grid(grid)), dim3(kBlock), 0, stream,
                      reinterpret_cast<const __half*>(k), n_rows, out_stride, hadamard,
                      key_scale, codes);
   return hipGetLastError();
@@ -180,7 +205,7 @@ hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream) {
   const size_t tail = bytes - n_words * 4;
   const size_t n = n_words > tail ? n_words : tail;
   const size_t grid = (n + 255) / 256;
-  hipLaunchKernelGGL(fill_zero_kernel, dim3((uint32_t)grid), dim3(256), 0, stream,
+  hipLaunchKernelGGL(fill_zero_kernel, dim3(bounded_grid((int64_t)grid)), dim3(256), 0, stream,
                      reinterpret_cast<uint32_t*>(ptr), n_words,
                      reinterpret_cast<uint8_t*>(ptr) + n_words * 4, tail);
   return hipGetLastError();

@@ -179,6 +179,49 @@ def test_full_size_b64_t32768_pot4_sampled():
     print(f"B=64 T=32768 PoT-4 sampled O err {err:.3e}")
 
 
+def test_longest_context_b1_t1m_pot4_sampled():
+    # 2^20 keys per sequence (4096 tiles of 256 keys): the longest ranges per
+    # split the planner makes, and the largest cache of the suite (4 * 2^20
+    # rows, 512 MiB of values)
+    err = _sampled_full_size(1, 1 << 20, 0, False, [(0, 0), (0, 3)], 12)
+    print(f"B=1 T=2^20 PoT-4 sampled O err {err:.3e}")
+
+
+def test_cache_offsets_beyond_4gib():
+    # t_cap = 2^24 keys per sequence: the last sequences' rows start past
+    # 2^27 rows, so their value bytes lie beyond 16 GiB and their code bytes
+    # beyond 4 GiB (64-bit address arithmetic in every kernel); only the first
+    # T keys of each sequence are attended
+    B, Hq, Hkv, T, t_cap = 2, 32, 4, 1000, 1 << 24
+    d = make_decode_inputs_device(13, B, Hq, Hkv, T, DEV, t_cap=t_cap)
+    fmt = pa.make_format(1)
+    cache = pa.alloc_pot_cache(B, Hkv, t_cap, 1, DEV)
+    pa.pot_encode_keys(fmt, d["k"], B * Hkv * t_cap, 1, 0, cache["key_scale"],
+                       cache["codes_se"], cache["codes_m"])
+    vcache = pa.alloc_value_cache(B, Hkv, t_cap, DEV)
+    pa.pot_store_values(d["v"], B * Hkv, t_cap, t_cap, 0, vcache)
+    out = torch.empty((B, Hq, 64), dtype=torch.float32, device=DEV)
+    ws = pa.alloc_workspace(pa.pot_decode_workspace_bytes(B, Hq, Hkv, T), DEV)
+    pa.pot_decode_attention(fmt, d["q"], cache["codes_se"], cache["codes_m"],
+                            cache["key_scale"], vcache, t_cap, d["kv_head_of_q"], B, Hq, Hkv,
+                            T, out, ws)
+    torch.cuda.synchronize()
+    G = Hq // Hkv
+    for (b, h) in [(0, 0), (1, 3)]:
+        kb = d["k"][b, h, :T].view(torch.uint16).cpu().numpy()
+        vb = d["v"][b, h, :T].view(torch.uint16).cpu().numpy()
+        qs = d["q"][b, h * G:(h + 1) * G].cpu().numpy()
+        o_se, o_cm, o_sc = oracle.encode_keys(kb, mant_bits=1)
+        assert np.array_equal(cache["codes_se"][b, h, :T].cpu().numpy(), o_se)
+        assert np.array_equal(cache["codes_m"][b, h, :T].cpu().numpy(), o_cm)
+        r = oracle.pot_decode(qs[None], o_se, o_cm, o_sc, vb, T, np.zeros(G, np.int32),
+                              1, G, 1, T, mant_bits=1)
+        err = float(np.abs(out[b, h * G:(h + 1) * G].cpu().numpy() - r["out"][0]).max())
+        assert err <= O_TOL, err
+    del d, cache, vcache
+    torch.cuda.empty_cache()
+
+
 def test_full_size_b8_t32768_hadamard_potm4_sampled():
     err = _sampled_full_size(8, 32768, 4, True, [(0, 1), (7, 3)], 11)
     print(f"B=8 T=32768 H+PoT-M4 sampled O err {err:.3e}")
