@@ -17,6 +17,7 @@ The line reports:
   right before and after that kernel (pot_debug.decode_begin / decode_end),
   with median and best; the whole call (query prep with the append, decode,
   split combine) is reported beside it as call_us / frac_call;
+- the same step captured once as a HIP graph and replayed (graph);
 - speed-up over the in-repo fp16 and INT8 kernels on the same shape;
 - the CPU oracle timed on host cores on a bounded sample, with one thread and
   with all threads.
@@ -258,6 +259,29 @@ def time_steps(lay, steps, warmup, kernel_times=False):
     return elapsed, us, kus
 
 
+def time_graph(lay, steps, warmup):
+    """Milliseconds per step when the whole step (every layer's call) is
+    captured once as a HIP graph and replayed: the launch gaps between the
+    kernels shrink, the kernels are the same. Events around all replays."""
+    import torch
+    lay.step()  # eager first: the library caches its occupancy queries
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        lay.step()
+    for _ in range(warmup):
+        g.replay()
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(steps):
+        g.replay()
+    e.record()
+    torch.cuda.synchronize()
+    del g
+    return s.elapsed_time(e) / steps
+
+
 def timed_calls(fn, n_layers, reps=10, warm=2):
     """Mean microseconds per call of fn(layer) over reps passes of n_layers."""
     import torch
@@ -378,11 +402,12 @@ def sweep(pa, dev, steps, warmup, only=None, layers=None):
         lay = Layers(pa, p["B"], p["T"], p["L"], p["k"], p["had"], dev, distinct=False,
                      keep_k16=4 if p["compare"] else 0)
         elapsed, us = time_steps(lay, steps, warmup)
+        graph_ms = time_graph(lay, steps, warmup)
         alg = algorithmic_bytes(p["B"], p["T"], row_bytes(p["k"]))
         foot = p["L"] * alg
         rec = {"B": p["B"], "T": p["T"], "format": fmt_name(p["k"], p["had"]), "layers": p["L"],
                "keys_per_s_step": p["B"] * HQ * p["T"] * p["L"] * steps / elapsed,
-               "ms_per_step": elapsed / steps * 1e3,
+               "ms_per_step": elapsed / steps * 1e3, "graph_ms_per_step": graph_ms,
                "decode_us_mean": float(us.mean()), "decode_us_median": float(np.median(us)),
                "decode_us_best": float(us.min()),
                "hbm_frac_mean": alg / (us.mean() * 1e-6) / 1e9 / HBM_PEAK_GBS,
@@ -480,6 +505,10 @@ def main() -> int:
                      "keys_scored_per_s_kernel": B * HQ * T / kern_s,
                      "keys_scored_per_s_call": B * HQ * T / call_s},
     }
+    graph_ms = time_graph(lay, args.steps, args.warmup)
+    result["graph"] = {"ms_per_step": graph_ms,
+                       "keys_per_s": B * HQ * T * L / (graph_ms * 1e-3),
+                       "note": "the same step captured once as a HIP graph and replayed"}
     if not args.no_compare:
         result["comparators"] = comparators(pa, lay, dev)
     if args.cpu_budget > 0:
