@@ -84,6 +84,22 @@ __device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// ---- streaming loads -----------------------------------------------------------
+// The cache is read once per call, so its loads carry the non-temporal hint.
+// It pays for the value fragments of every engine and for the 32-byte PoT
+// code rows; the fp16 comparator's 128-byte key rows are read by eight
+// 16-byte loads per lane that revisit the same lines, and stay plain there.
+typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint4 ld_nt(const uint4* p) {
+  const u32x4v v = __builtin_nontemporal_load(reinterpret_cast<const u32x4v*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ uint2 ld_nt(const uint2* p) {
+  const u32x2v v = __builtin_nontemporal_load(reinterpret_cast<const u32x2v*>(p));
+  return make_uint2(v.x, v.y);
+}
+
 // ---- per-tile register payloads -----------------------------------------------
 template <int MODE, int K>
 struct KeyRegs;
@@ -126,17 +142,17 @@ template <int MODE, int K>
 __device__ __forceinline__ void load_keys(const DecodeArgs& a, int64_t row, KeyRegs<MODE, K>& r) {
   if constexpr (MODE == kScorePot) {
     const uint4* cp = reinterpret_cast<const uint4*>(a.codes_se + row * (kDim / 2));
-    r.c0 = cp[0];
-    r.c1 = cp[1];
+    r.c0 = ld_nt(cp);
+    r.c1 = ld_nt(cp + 1);
 #pragma unroll
     for (int bb = 0; bb < K; ++bb)
-      r.pl[bb] = reinterpret_cast<const uint2*>(a.codes_m + row * 8 * K)[bb];
-    r.s = a.key_scale[row];
+      r.pl[bb] = ld_nt(reinterpret_cast<const uint2*>(a.codes_m + row * 8 * K) + bb);
+    r.s = __builtin_nontemporal_load(a.key_scale + row);
   } else if constexpr (MODE == kScoreDs4a) {
     const uint4* cp = reinterpret_cast<const uint4*>(a.codes_se + row * (kDim / 2));
-    r.c0 = cp[0];
-    r.c1 = cp[1];
-    r.s = a.key_scale[row];
+    r.c0 = ld_nt(cp);
+    r.c1 = ld_nt(cp + 1);
+    r.s = __builtin_nontemporal_load(a.key_scale + row);
   } else if constexpr (MODE == kScoreInt8) {
     const int4* kp = reinterpret_cast<const int4*>(a.codes_i8 + row * kDim);
 #pragma unroll
@@ -165,12 +181,12 @@ __device__ __forceinline__ void load_values(const void* vseq, const int8_t* eseq
       const uint2* base =
           reinterpret_cast<const uint2*>(static_cast<const uint8_t*>(vseq) + (int64_t)g8 * kDim);
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb) v.f[kb][nb] = base[nb * 16 + (lane & 15)];
+      for (int nb = 0; nb < 4; ++nb) v.f[kb][nb] = ld_nt(base + nb * 16 + (lane & 15));
     } else {
       const uint4* base = reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(vseq) +
                                                          (int64_t)g8 * kDim);
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb) v.f[kb][nb] = base[nb * 16 + (lane & 15)];
+      for (int nb = 0; nb < 4; ++nb) v.f[kb][nb] = ld_nt(base + nb * 16 + (lane & 15));
     }
   }
   if constexpr (V8) {

@@ -2,7 +2,9 @@
 // loads over a buffer far larger than the last-level cache and folds them into
 // a register; one word per workgroup is written at the end. The grid is a few
 // workgroups per CU with a grid-stride loop, the same access shape as the
-// decode kernels' code and value streams (one 16-byte load per lane).
+// decode kernels' code and value streams (one 16-byte load per lane). Each
+// grid is run with plain loads and with non-temporal loads (the nt hint the
+// decode kernels put on their streams).
 //
 // Build and run on a gfx950 device:
 //   hipcc --offload-arch=gfx950 -O3 -Xclang -target-feature -Xclang -packed-fp32-ops \
@@ -11,6 +13,19 @@
 
 #include <cstdio>
 
+typedef unsigned u32x4v __attribute__((ext_vector_type(4)));
+
+template <bool NT>
+__device__ __forceinline__ uint4 ld(const uint4* p) {
+  if constexpr (NT) {
+    const u32x4v v = __builtin_nontemporal_load(reinterpret_cast<const u32x4v*>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+  } else {
+    return *p;
+  }
+}
+
+template <bool NT>
 __global__ __launch_bounds__(256) void read_kernel(const uint4* __restrict__ src, size_t n16,
                                                    unsigned* __restrict__ out) {
   const size_t stride = (size_t)gridDim.x * blockDim.x;
@@ -18,12 +33,13 @@ __global__ __launch_bounds__(256) void read_kernel(const uint4* __restrict__ src
   size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   // four independent loads in flight per lane per iteration
   for (; i + 3 * stride < n16; i += 4 * stride) {
-    const uint4 a = src[i], b = src[i + stride], c = src[i + 2 * stride], d = src[i + 3 * stride];
+    const uint4 a = ld<NT>(src + i), b = ld<NT>(src + i + stride), c = ld<NT>(src + i + 2 * stride),
+                d = ld<NT>(src + i + 3 * stride);
     acc ^= a.x ^ a.y ^ a.z ^ a.w ^ b.x ^ b.y ^ b.z ^ b.w ^ c.x ^ c.y ^ c.z ^ c.w ^ d.x ^ d.y ^
            d.z ^ d.w;
   }
   for (; i < n16; i += stride) {
-    const uint4 a = src[i];
+    const uint4 a = ld<NT>(src + i);
     acc ^= a.x ^ a.y ^ a.z ^ a.w;
   }
   __shared__ unsigned red[256];
@@ -48,6 +64,7 @@ int main() {
   hipEvent_t e0, e1;
   if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) return 1;
   printf("%d CUs, %zu MiB read per launch\n", cus, bytes >> 20);
+  for (int nt = 0; nt < 2; ++nt)
   for (int per_cu : {2, 4, 8, 16}) {
     const int blocks = cus * per_cu;
     if (hipMalloc(&out, (size_t)blocks * sizeof(unsigned)) != hipSuccess) return 1;
@@ -55,7 +72,10 @@ int main() {
     const int reps = 10;
     for (int r = 0; r < reps + 2; ++r) {
       if (hipEventRecord(e0) != hipSuccess) return 1;
-      hipLaunchKernelGGL(read_kernel, dim3(blocks), dim3(256), 0, 0, src, n16, out);
+      if (nt)
+        hipLaunchKernelGGL(read_kernel<true>, dim3(blocks), dim3(256), 0, 0, src, n16, out);
+      else
+        hipLaunchKernelGGL(read_kernel<false>, dim3(blocks), dim3(256), 0, 0, src, n16, out);
       if (hipEventRecord(e1) != hipSuccess || hipEventSynchronize(e1) != hipSuccess) return 1;
       float ms = 0.0f;
       if (hipEventElapsedTime(&ms, e0, e1) != hipSuccess) return 1;
@@ -64,8 +84,9 @@ int main() {
         best = ms < best ? ms : best;
       }
     }
-    printf("workgroups/CU %2d: mean %.3f ms = %.0f GB/s, best %.3f ms = %.0f GB/s\n", per_cu,
-           sum / reps, bytes / (sum / reps * 1e-3) / 1e9, best, bytes / (best * 1e-3) / 1e9);
+    printf("%s loads, workgroups/CU %2d: mean %.3f ms = %.0f GB/s, best %.3f ms = %.0f GB/s\n",
+           nt ? "nt   " : "plain", per_cu, sum / reps, bytes / (sum / reps * 1e-3) / 1e9, best,
+           bytes / (best * 1e-3) / 1e9);
     if (hipFree(out) != hipSuccess) return 1;
   }
   if (hipFree(src) != hipSuccess) return 1;
