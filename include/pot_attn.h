@@ -210,7 +210,9 @@ pot_status pot_workspace_init(void* workspace, size_t ws_bytes, void* stream);
  *  kv_head_of_q HOST int32 [Hq]: kv head serving each query head (GQA). Every
  *               kv head must serve the same number G = Hq/Hkv of query heads,
  *               G in {1, 2, 4, 8}.
- *  T            keys attended, 1 <= T <= t_cap.
+ *  T            keys attended, 1 <= T <= t_cap and T <= 2^24 - 8
+ *               (POT_ERR_UNSUPPORTED above: the kernel addresses a
+ *               sequence's rows with 32-bit byte offsets).
  *  out          [B][Hq][d] fp32: O = softmax(S^ / sqrt(d)) V.
  *  workspace    >= pot_decode_workspace_bytes(B, Hq, Hkv, T) bytes, 256-byte
  *               aligned. Calls that share a workspace must not overlap in

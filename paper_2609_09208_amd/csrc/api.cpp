@@ -165,6 +165,9 @@ pot_status decode_common(int mode, int mant_bits, DecodeArgs& a, const int32_t* 
   if (!shape_ok(B, Hq, Hkv, T))
     return fail(POT_ERR_INVALID_ARG, "bad shape B=%d Hq=%d Hkv=%d T=%d", B, Hq, Hkv, T);
   if (t_cap < T) return fail(POT_ERR_INVALID_ARG, "T %d > t_cap %lld", T, (long long)t_cap);
+  if (T > kMaxKeys)
+    return fail(POT_ERR_UNSUPPORTED, "T %d > %d keys per sequence (32-bit buffer ranges)", T,
+                kMaxKeys);
   if (t_cap % 8)
     return fail(POT_ERR_INVALID_ARG, "t_cap %lld is not a multiple of 8 (value-cache groups)",
                 (long long)t_cap);

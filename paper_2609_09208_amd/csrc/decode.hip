@@ -91,14 +91,25 @@ __device__ __forceinline__ void wave_sync_lds() {
 // 16-byte loads per lane that revisit the same lines, and stay plain there.
 typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ uint4 ld_nt(const uint4* p) {
-  const u32x4v v = __builtin_nontemporal_load(reinterpret_cast<const u32x4v*>(p));
-  return make_uint4(v.x, v.y, v.z, v.w);
+
+// Raw buffer resources over one sequence's cache rows (gfx9 descriptor word 3
+// = 0x00020000: untyped records, byte-granular range). A load at or past the
+// resource's size returns zeros and touches no memory, so tiles past the end
+// of a key range need no clamped addresses, and every offset is 32-bit: a
+// lane-constant part in a vector register and the tile start in a scalar one.
+typedef __amdgpu_buffer_rsrc_t BufRsrc;
+constexpr int kBufWord3 = 0x00020000;
+constexpr int kAuxNt = 2;  // cache policy of the loads: non-temporal
+__device__ __forceinline__ BufRsrc buf_rsrc(const void* base, int64_t n_bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n_bytes,
+                                           kBufWord3);
 }
-__device__ __forceinline__ uint2 ld_nt(const uint2* p) {
-  const u32x2v v = __builtin_nontemporal_load(reinterpret_cast<const u32x2v*>(p));
-  return make_uint2(v.x, v.y);
-}
+
+// The streams of one (batch, kv head) sequence that a workgroup reads.
+struct Streams {
+  BufRsrc codes, planes, scales;  // PoT code rows, mantissa planes, key scales
+  BufRsrc values, exps;           // value groups (fp16 or bytes), INT8 exponents
+};
 
 // ---- per-tile register payloads -----------------------------------------------
 template <int MODE, int K>
@@ -134,26 +145,15 @@ struct ValRegs<true> {
   uint2 g;        // exponents g of the 8 keys whose weights this lane forms
 };
 
-// Loads are unconditional (addresses clamped into the valid range) so that
-// the compiler can count outstanding loads statically and keep the prefetch
-// of the next tile in flight while the current one is processed; keys past
-// the range are masked when the tile is consumed.
+// Loads are unconditional (addresses clamped into the valid range, or reads
+// past a buffer resource's end, which return zeros) so that the compiler can
+// count outstanding loads statically and keep the prefetch of the next tile in
+// flight while the current one is processed; keys past the range are masked
+// when the tile is consumed.
+// Key rows of the comparators (INT8 codes, fp16 keys).
 template <int MODE, int K>
 __device__ __forceinline__ void load_keys(const DecodeArgs& a, int64_t row, KeyRegs<MODE, K>& r) {
-  if constexpr (MODE == kScorePot) {
-    const uint4* cp = reinterpret_cast<const uint4*>(a.codes_se + row * (kDim / 2));
-    r.c0 = ld_nt(cp);
-    r.c1 = ld_nt(cp + 1);
-#pragma unroll
-    for (int bb = 0; bb < K; ++bb)
-      r.pl[bb] = ld_nt(reinterpret_cast<const uint2*>(a.codes_m + row * 8 * K) + bb);
-    r.s = __builtin_nontemporal_load(a.key_scale + row);
-  } else if constexpr (MODE == kScoreDs4a) {
-    const uint4* cp = reinterpret_cast<const uint4*>(a.codes_se + row * (kDim / 2));
-    r.c0 = ld_nt(cp);
-    r.c1 = ld_nt(cp + 1);
-    r.s = __builtin_nontemporal_load(a.key_scale + row);
-  } else if constexpr (MODE == kScoreInt8) {
+  if constexpr (MODE == kScoreInt8) {
     const int4* kp = reinterpret_cast<const int4*>(a.codes_i8 + row * kDim);
 #pragma unroll
     for (int i = 0; i < 4; ++i) r.k[i] = kp[i];
@@ -165,33 +165,58 @@ __device__ __forceinline__ void load_keys(const DecodeArgs& a, int64_t row, KeyR
   }
 }
 
+// PoT codes of keys t0 + lane (PoT and byte-decode engines): keys at or past
+// the range's end read zeros (they are masked when the tile is consumed).
+template <int MODE, int K>
+__device__ __forceinline__ void load_keys_buf(const Streams& st, int t0, int lane,
+                                              KeyRegs<MODE, K>& r) {
+  const u32x4v c0 = __builtin_amdgcn_raw_buffer_load_b128(st.codes, lane * 32, t0 * 32, kAuxNt);
+  const u32x4v c1 =
+      __builtin_amdgcn_raw_buffer_load_b128(st.codes, lane * 32 + 16, t0 * 32, kAuxNt);
+  r.c0 = make_uint4(c0.x, c0.y, c0.z, c0.w);
+  r.c1 = make_uint4(c1.x, c1.y, c1.z, c1.w);
+  if constexpr (MODE == kScorePot) {
+#pragma unroll
+    for (int bb = 0; bb < K; ++bb) {
+      const u32x2v p = __builtin_amdgcn_raw_buffer_load_b64(st.planes, lane * 8 * K + 8 * bb,
+                                                            t0 * 8 * K, kAuxNt);
+      r.pl[bb] = make_uint2(p.x, p.y);
+    }
+  }
+  r.s = __builtin_bit_cast(float,
+                           __builtin_amdgcn_raw_buffer_load_b32(st.scales, lane * 4, t0 * 4, kAuxNt));
+}
+
 // B fragments of one 64-key tile: lane l takes keys t0 + 32*kb + 8*(l/16) ..+7
 // of dim 16*nb + l%16, one 16-byte (fp16) or 8-byte (INT8) load each from the
-// token-interleaved cache. Groups past the range read the range's last group
-// instead. With INT8 values the lane also loads the exponents of the 8 keys
-// t0 + 32*part + 8*grp ..+7 whose weights it forms in stage 2.
-// vseq: the sequence's first value (fp16 or byte); eseq: its first exponent.
+// token-interleaved cache, through the sequence's value resource: groups past
+// the range's last group read zeros (their weights are 0). With INT8 values
+// the lane also loads the exponents of the 8 keys t0 + 32*part + 8*grp ..+7
+// whose weights it forms in stage 2.
 template <bool V8>
-__device__ __forceinline__ void load_values(const void* vseq, const int8_t* eseq, int t0,
-                                            int g_last, int lane, ValRegs<V8>& v) {
+__device__ __forceinline__ void load_values_buf(const Streams& st, int t0, int lane,
+                                                ValRegs<V8>& v) {
+  constexpr int kGroupBytes = V8 ? 8 * kDim : 16 * kDim;  // one 8-token group
+  const int voff = (lane >> 4) * kGroupBytes + (lane & 15) * (V8 ? 8 : 16);
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) {
-    const int g8 = min(t0 + 32 * kb + 8 * (lane >> 4), g_last);
-    if constexpr (V8) {
-      const uint2* base =
-          reinterpret_cast<const uint2*>(static_cast<const uint8_t*>(vseq) + (int64_t)g8 * kDim);
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb) v.f[kb][nb] = ld_nt(base + nb * 16 + (lane & 15));
-    } else {
-      const uint4* base = reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(vseq) +
-                                                         (int64_t)g8 * kDim);
-#pragma unroll
-      for (int nb = 0; nb < 4; ++nb) v.f[kb][nb] = ld_nt(base + nb * 16 + (lane & 15));
+    for (int nb = 0; nb < 4; ++nb) {
+      const int off = voff + kb * 4 * kGroupBytes + nb * 16 * (V8 ? 8 : 16);
+      if constexpr (V8) {
+        const u32x2v w = __builtin_amdgcn_raw_buffer_load_b64(st.values, off, t0 * kDim, kAuxNt);
+        v.f[kb][nb] = make_uint2(w.x, w.y);
+      } else {
+        const u32x4v w =
+            __builtin_amdgcn_raw_buffer_load_b128(st.values, off, t0 * 2 * kDim, kAuxNt);
+        v.f[kb][nb] = make_uint4(w.x, w.y, w.z, w.w);
+      }
     }
   }
   if constexpr (V8) {
     const int part = (lane & 15) >> 3, grp = lane >> 4;
-    v.g = *reinterpret_cast<const uint2*>(eseq + min(t0 + 32 * part + 8 * grp, g_last));
+    const u32x2v g = __builtin_amdgcn_raw_buffer_load_b64(st.exps, 32 * part + 8 * grp, t0, 0);
+    v.g = make_uint2(g.x, g.y);
   }
 }
 
@@ -362,8 +387,6 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
   const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int64_t seq = (int64_t)b * a.Hkv + kvh;
   const int64_t row0 = seq * a.t_cap;
-  const void* vseq = V8 ? static_cast<const void*>(a.v8 + row0 * kDim)
-                        : static_cast<const void*>(a.v + row0 * kDim);
   const int8_t* eseq = V8 ? a.v_exp + row0 : nullptr;
   // query operands and score factors: uniform, read-only here -> scalar loads
   const int32_t* __restrict__ qb = qbuf + seq * a.qstride;
@@ -412,10 +435,26 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
 
   KeyRegs<MODE, K> kr[2];
   const int g_last = (t_end - 1) & ~7;  // first token of the range's last 8-token group
-  // key codes of tile jt; keys past the range load the range's last key
+  Streams st;
+  if constexpr (MODE == kScorePot || MODE == kScoreDs4a) {
+    st.codes = buf_rsrc(a.codes_se + row0 * (kDim / 2), (int64_t)t_end * (kDim / 2));
+    st.scales = buf_rsrc(a.key_scale + row0, (int64_t)t_end * 4);
+    if constexpr (K > 0) st.planes = buf_rsrc(a.codes_m + row0 * 8 * K, (int64_t)t_end * 8 * K);
+  }
+  if constexpr (V8) {
+    st.values = buf_rsrc(a.v8 + row0 * kDim, (int64_t)(g_last + 8) * kDim);
+    st.exps = buf_rsrc(a.v_exp + row0, g_last + 8);
+  } else {
+    st.values = buf_rsrc(a.v + row0 * kDim, (int64_t)(g_last + 8) * kDim * 2);
+  }
+  // key codes of tile jt; keys past the range read zeros (PoT, byte decode)
+  // or the range's last key (INT8, fp16)
   auto load_keys_tile = [&](int jt, KeyRegs<MODE, K>& kk) {
     const int t0 = t_begin + kWTile * jt;
-    load_keys<MODE, K>(a, row0 + min(t0 + lane, t_end - 1), kk);
+    if constexpr (MODE == kScorePot || MODE == kScoreDs4a)
+      load_keys_buf<MODE, K>(st, t0, lane, kk);
+    else
+      load_keys<MODE, K>(a, row0 + min(t0 + lane, t_end - 1), kk);
   };
   int j = wave;
   const int j_last = n_tiles - 1;
@@ -427,7 +466,7 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
   constexpr bool kPrefetchV = MODE != kScorePot;
   ValRegs<V8> vr[kPrefetchV ? 2 : 1];
   if constexpr (kPrefetchV) {
-    if (j < n_tiles) load_values<V8>(vseq, eseq, t_begin + kWTile * j, g_last, lane, vr[0]);
+    if (j < n_tiles) load_values_buf<V8>(st, t_begin + kWTile * j, lane, vr[0]);
   }
 
   // Stage 1 of a tile: issue the loads it still needs and those of this
@@ -441,9 +480,9 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
     const int jn = min(jt + kWaves, j_last);
     if constexpr (kPrefetchV) {
       load_keys_tile(jn, knext);
-      load_values<V8>(vseq, eseq, t_begin + kWTile * jn, g_last, lane, vnext);
+      load_values_buf<V8>(st, t_begin + kWTile * jn, lane, vnext);
     } else {
-      load_values<V8>(vseq, eseq, t0, g_last, lane, vs);
+      load_values_buf<V8>(st, t0, lane, vs);
       load_keys_tile(jn, knext);
     }
     const int t = t0 + lane;

@@ -90,6 +90,11 @@ struct DecodeArgs {
   int32_t q_of_kv[kMaxHqArg];  // [Hkv][G] query heads served by each kv head
 };
 
+// Longest key range of one decode call: the decode kernel reads each
+// sequence's cache rows through buffer resources with 32-bit byte ranges
+// (fp16 values: 128 bytes per key, rounded up to whole 8-key groups).
+constexpr int kMaxKeys = (1 << 24) - 8;
+
 // 32-bit words of prepared query operands per kv head for group size G:
 // room for the largest layout (32 words per head: 16-bit operand pairs for
 // the PoT codes, fp16 pairs for the fp16 comparator) plus the G per-head

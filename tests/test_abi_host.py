@@ -111,6 +111,7 @@ def test_decode_rejects_bad_format(fmt, code):
     (dict(Hq=24, Hkv=4, heads=np.arange(24) // 6), pa.POT_ERR_UNSUPPORTED),  # G=6
     (dict(Hq=256, Hkv=32, heads=np.arange(256) // 8), pa.POT_ERR_UNSUPPORTED),
     (dict(ws_bytes=1000), pa.POT_ERR_WORKSPACE),
+    (dict(T=1 << 24, t_cap=1 << 24), pa.POT_ERR_UNSUPPORTED),  # past 2^24 - 8 keys
 ])
 def test_decode_rejects_bad_arguments(over, code):
     assert _decode(**over) == code
