@@ -552,9 +552,7 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
           // the first pair starts each sum from the constant 0; with clamp
           // set (|sum| <= 2 * 16256, never reached) the compiler emits the
           // three-operand form instead of zeroing the accumulator first
-#pragma unroll
-          for (int h = 0; h < G; ++h) {
-            const s16x2 pv = __builtin_bit_cast(s16x2, qq[kCols * n + h]) >> sh;
+          auto accumulate = [&](int h, s16x2 pv) {
             accv[h] = (i == 0 && n == 0) ? __builtin_amdgcn_sdot2(pv, sg, 0, true)
                                          : __builtin_amdgcn_sdot2(pv, sg, accv[h], false);
 #pragma unroll
@@ -562,6 +560,25 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
               accm[bb][h] = (i == 0 && n == 0)
                                 ? __builtin_amdgcn_sdot2(pv, mw[bb], 0, true)
                                 : __builtin_amdgcn_sdot2(pv, mw[bb], accm[bb][h], false);
+          };
+          // Two heads at a time: both shifts, then both heads' sums. The
+          // scheduling barriers keep this order, so the shifted operands
+          // alternate between two registers and no v_dot2 reads a register
+          // that the instruction just before it wrote while the v_dot2 before
+          // that read it (with one register the compiler puts a wait state
+          // before nearly every v_dot2).
+#pragma unroll
+          for (int h = 0; h < G; h += 2) {
+            const s16x2 pv0 = __builtin_bit_cast(s16x2, qq[kCols * n + h]) >> sh;
+            if constexpr (G > 1) {
+              const s16x2 pv1 = __builtin_bit_cast(s16x2, qq[kCols * n + h + 1]) >> sh;
+              __builtin_amdgcn_sched_barrier(0);
+              accumulate(h, pv0);
+              accumulate(h + 1, pv1);
+              __builtin_amdgcn_sched_barrier(0);
+            } else {
+              accumulate(h, pv0);
+            }
           }
         }
       }
