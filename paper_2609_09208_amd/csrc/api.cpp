@@ -84,6 +84,22 @@ int split_count_for_slots(long units, long slots) {
   return units >= slots ? 1 : (int)(slots / units);
 }
 
+// Split count when the grid would fill the GPU's resident slots with short
+// splits: a split shorter than four 256-key tiles costs more in the
+// workgroup's fixed work and in the combine than its extra parallelism gains
+// (B = 1, T = 32768: 50.6 us with 128 one-tile splits, 29.3 us with 32
+// four-tile splits, 33.5 us with 16 eight-tile splits), unless that would
+// leave fewer than 128 workgroups (half the CUs) when the keys allow more
+// (B = 1, T = 4096: 21.8 us with 16 one-tile splits, 25.5 us with 4).
+constexpr int kMinTilesPerSplit = 4;
+constexpr long kMinWorkgroups = 128;
+
+int split_count_short_ranges(long units, int tiles) {
+  const int s_len = std::max(1, tiles / kMinTilesPerSplit);
+  const int s_spread = (int)std::min<long>(tiles, (kMinWorkgroups + units - 1) / units);
+  return std::max(s_len, s_spread);
+}
+
 // Upper bound used to size workspaces without a device query: 256 CUs x 8
 // resident workgroups (the decode kernel reaches at most 3 per CU).
 constexpr long kMaxSlots = 256L * 8;
@@ -195,7 +211,9 @@ pot_status decode_common(int mode, int mant_bits, DecodeArgs& a, const int32_t* 
   } else {
     const int mbits = mode == kScorePot ? mant_bits : 0;
     const int S = split_count_for_slots((long)B * Hkv, device_slots(mode, G, mbits, vf));
-    p = plan_from_count(T, std::min(S, plan_bound(B, Hkv, T).n_splits));
+    const int tiles = (T + kTile - 1) / kTile;
+    const int s_short = split_count_short_ranges((long)B * Hkv, tiles);
+    p = plan_from_count(T, std::min({S, s_short, plan_bound(B, Hkv, T).n_splits}));
   }
   const WsLayout w = ws_layout(B, Hq, Hkv, p.n_splits);
   if (ws_bytes < w.total)
