@@ -281,6 +281,15 @@ __global__ __launch_bounds__(kBlock) void prep_queries_kernel(const DecodeArgs a
   const int64_t seq = (int64_t)b * a.Hkv + kvh;
   int32_t* qb = a.qbuf + seq * a.qstride;
   float* cb = reinterpret_cast<float*>(qb + QL::kWords);
+  // this wave's query elements, loaded before the append so that their
+  // latency overlaps it
+  constexpr int kHeadsPerWave = (G + kWaves - 1) / kWaves;
+  float qin[kHeadsPerWave];
+#pragma unroll
+  for (int i = 0; i < kHeadsPerWave; ++i) {
+    const int h = wave + kWaves * i;
+    qin[i] = h < G ? a.q[((int64_t)b * a.Hq + a.q_of_kv[kvh * G + h]) * kDim + lane] : 0.0f;
+  }
   if constexpr (MODE == kScorePot || MODE == kScoreDs4a) {
     // fused append of this sequence's new token at row T - 1: wave 0 encodes
     // the key (row absmax scale), wave 1 stores the values (fp16, or INT8
@@ -299,9 +308,12 @@ __global__ __launch_bounds__(kBlock) void prep_queries_kernel(const DecodeArgs a
                                a.T - 1);
     }
   }
-  for (int h = wave; h < G; h += kWaves) {
+#pragma unroll
+  for (int i = 0; i < kHeadsPerWave; ++i) {
+    const int h = wave + kWaves * i;
+    if (h >= G) break;
     const int64_t bq = (int64_t)b * a.Hq + a.q_of_kv[kvh * G + h];
-    float qv = a.q[bq * kDim + lane];
+    float qv = qin[i];
     if constexpr (MODE == kScoreFp16) {
       const uint32_t bits = __half_as_ushort(__float2half_rn(qv));
       const uint32_t other = __shfl_xor(bits, 1, 64);
@@ -928,6 +940,7 @@ __global__ __launch_bounds__(64) void combine_kernel(const DecodeArgs a) {
   int M = INT_MIN;
   for (int s = 0; s < Sn; ++s) M = max(M, pm[s]);
   float L = 0.0f, O = 0.0f;
+#pragma unroll 4
   for (int s = 0; s < Sn; ++s) {
     const float f = __builtin_amdgcn_ldexpf(1.0f, pm[s] - M);
     L = fmaf(f, pl[s], L);
