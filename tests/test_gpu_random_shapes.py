@@ -1,0 +1,44 @@
+"""GPU parity over seeded random shapes and formats.
+
+Each case draws a batch size, group size, kv-head count, key count T (ragged,
+with spare cache rows up to t_cap), mantissa width k, Hadamard rotation,
+head-room F, score engine and split count, and runs the full parity check
+against the oracle: codes, scales, q^, Delta, int32 scores and integer maxima
+bit-exact, O within 2e-3. The cases are fixed by their seeds, so the test is
+deterministic; together they cover combinations that the hand-written cases
+do not.
+"""
+import numpy as np
+import pytest
+
+from parity_util import assert_pot_parity
+from workloads import make_decode_inputs
+
+pytestmark = pytest.mark.gpu
+
+
+def _case(seed):
+    rng = np.random.default_rng(9000 + seed)
+    G = int(rng.choice([1, 2, 4, 8]))
+    Hkv = int(rng.choice([1, 2, 4]))
+    B = int(rng.integers(1, 4))
+    T = int(rng.integers(1, 3000))
+    t_cap = (T + 7) // 8 * 8 + 8 * int(rng.integers(0, 4))
+    engine = "ds4a" if rng.random() < 0.25 else "sac"
+    k = 0 if engine == "ds4a" else int(rng.integers(0, 5))
+    hadamard = bool(rng.random() < 0.3)
+    F = 7 if engine == "ds4a" else int(rng.choice([6, 7, 9, 12]))
+    tiles = -(-T // 256)
+    splits = 0 if rng.random() < 0.5 else int(rng.integers(1, tiles + 1))
+    return dict(G=G, Hkv=Hkv, B=B, T=T, t_cap=t_cap, engine=engine, k=k, hadamard=hadamard,
+                F=F, splits=splits)
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_random_shape(seed):
+    c = _case(seed)
+    d = make_decode_inputs(7000 + seed, B=c["B"], Hq=c["G"] * c["Hkv"], Hkv=c["Hkv"],
+                           T=c["T"], t_cap=c["t_cap"])
+    err, g = assert_pot_parity(d, mant_bits=c["k"], frac_bits=c["F"], hadamard=c["hadamard"],
+                               force_splits=c["splits"], engine=c["engine"])
+    print(f"seed {seed} {c} splits={g['n_splits']} O err {err:.2e}")
