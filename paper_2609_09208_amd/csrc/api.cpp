@@ -101,7 +101,7 @@ int split_count_short_ranges(long units, int tiles) {
 }
 
 // Upper bound used to size workspaces without a device query: 256 CUs x 8
-// resident workgroups (the decode kernel reaches at most 3 per CU).
+// resident workgroups (the decode kernels reach at most 4 per CU: 4 waves per SIMD).
 constexpr long kMaxSlots = 256L * 8;
 
 Plan plan_bound(int B, int Hkv, int T) {
