@@ -375,7 +375,6 @@ struct alignas(16) DecodeSmem {
   float wp[kWaves][64];  // INT8 values: per-lane sums of the unscaled weights
   int wm[kWaves][8];
   int gm[kWaves];        // INT8 values: per-wave minimum exponent
-  int last;
 };
 
 // VF: value format, 0 fp16 values, 1 INT8 values, 2 INT8 values with the

@@ -31,12 +31,6 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
-}
-
 // Radix-2 Walsh-Hadamard butterfly over one 64-vector held one element per
 // lane, in fp64, stages of span 1, 2, 4, ..., 32 mapping (a, b) to
 // (a + b, a - b). For fp16 inputs every partial sum is exact in fp64; for fp32
