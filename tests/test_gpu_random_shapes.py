@@ -7,7 +7,8 @@ against the oracle: codes, scales, q^, Delta, int32 scores and integer maxima
 bit-exact, O within 2e-3. The cases are fixed by their seeds, so the test is
 deterministic; together they cover combinations that the hand-written cases
 do not. A second set draws the same shapes over the INT8 value cache, with
-softmax or power-of-two weights and either score engine.
+softmax or power-of-two weights and either score engine, and a third the
+fused append of the new token.
 """
 import numpy as np
 import pytest
@@ -74,3 +75,22 @@ def test_random_shape_int8_values(seed):
     err, s = assert_v8_parity(d, engine=c["engine"], mant_bits=c["k"], hadamard=c["hadamard"],
                               force_splits=c["splits"], pow2=c["pow2"])
     print(f"seed {seed} {c} splits={s} O err {err:.2e}")
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_random_shape_fused_append(seed):
+    """The fused append + decode call over random draws: the appended row and
+    every output and tap equal those of the three separate calls bit for bit,
+    and the oracle's."""
+    from test_gpu_append import _run
+    rng = np.random.default_rng(9800 + seed)
+    G = int(rng.choice([1, 2, 4, 8]))
+    Hkv = int(rng.choice([1, 2, 4]))
+    B = int(rng.integers(1, 4))
+    T = int(rng.integers(1, 3000))
+    t_cap = (T + 7) // 8 * 8 + 8 * int(rng.integers(0, 4))
+    k = int(rng.integers(0, 5))
+    hadamard = bool(rng.random() < 0.3)
+    err, s = _run(7800 + seed, B, G * Hkv, Hkv, T, t_cap=t_cap, mant_bits=k, hadamard=hadamard)
+    print(f"seed {seed} G={G} Hkv={Hkv} B={B} T={T} t_cap={t_cap} k={k} had={hadamard} "
+          f"splits={s} O err {err:.2e}")
