@@ -441,9 +441,9 @@ def main() -> int:
                          "the FETCH_SIZE / WRITE_SIZE counters against a known size)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
-              "(the decode path shards over (batch, kv head) with no communication; "
-              "see DESIGN.md)", file=sys.stderr)
+        print(f"bench.py: measures one GPU; --gpus {args.gpus} is not supported "
+              "(the decode path shards over (batch, kv head) with no communication)",
+              file=sys.stderr)
         return 2
 
     import numpy as np

@@ -170,7 +170,7 @@ def test_int8_oracle_scores_bruteforce():
 
 
 def test_log2_domain_score_follows_the_recorded_fp32_order():
-    # reading recorded for this build: x = fl32(fl32(float(acc) * s) * c),
+    # the paper leaves the fp32 order open; the order fixed here is x = fl32(fl32(float(acc) * s) * c),
     # c = fl32(fl32(Delta * log2e_f32) * 2^-(F+k+3)); the GPU must match it
     d = make_decode_inputs(12, B=1, Hq=2, Hkv=1, T=500, t_cap=500)
     rows = d["k_bits"].reshape(-1, 64)
