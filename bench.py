@@ -219,6 +219,21 @@ class Layers:
                 events[i][1].record()
 
 
+def time_plain(lay, steps, warmup):
+    """Wall time of `steps` steps with only the library's calls in the timed
+    region (no timing events: each event record costs the step time on the
+    device, about 4% for the four per layer of the instrumented pass)."""
+    import torch
+    for _ in range(warmup):
+        lay.step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        lay.step()
+    torch.cuda.synchronize()
+    return time.perf_counter() - t0
+
+
 def time_steps(lay, steps, warmup, kernel_times=False):
     """Wall time of `steps` steps and the per-call decode times (us) from HIP
     events recorded on the launch stream around each call (query prep with
@@ -474,7 +489,10 @@ def main() -> int:
     lay = Layers(pa, B, T, L, k, False, dev, distinct=True,
                  keep_k16=0 if args.no_compare else 4)
     torch.cuda.synchronize()
-    elapsed, us, kus = time_steps(lay, args.steps, args.warmup, kernel_times=True)
+    # value: K steps with nothing else in the timed region; then K more steps
+    # with HIP events around every call and every decode kernel (roofline)
+    elapsed = time_plain(lay, args.steps, args.warmup)
+    elapsed_ev, us, kus = time_steps(lay, args.steps, 1, kernel_times=True)
     kern_s = float(kus.mean()) * 1e-6
     call_s = float(us.mean()) * 1e-6
     alg = algorithmic_bytes(B, T, row_bytes(k))
@@ -504,6 +522,11 @@ def main() -> int:
                      "frac_of_read_ceiling": achieved / read_ceiling() if read_ceiling() else None,
                      "keys_scored_per_s_kernel": B * HQ * T / kern_s,
                      "keys_scored_per_s_call": B * HQ * T / call_s},
+        "timing": {"value": f"{args.steps} steps after {args.warmup} warm-up steps, no events "
+                            "in the timed region",
+                   "roofline": f"{args.steps} further steps with HIP events around every "
+                               "call and every decode kernel",
+                   "ms_per_step_with_events": elapsed_ev / args.steps * 1e3},
     }
     graph_ms = time_graph(lay, args.steps, args.warmup)
     result["graph"] = {"ms_per_step": graph_ms,
