@@ -222,7 +222,7 @@ class Layers:
 def time_plain(lay, steps, warmup):
     """Wall time of `steps` steps with only the library's calls in the timed
     region (no timing events: each event record costs the step time on the
-    device, about 4% for the four per layer of the instrumented pass)."""
+    device, about 5% for the four per layer of the instrumented pass)."""
     import torch
     for _ in range(warmup):
         lay.step()
