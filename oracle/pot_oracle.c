@@ -308,11 +308,15 @@ static double value_at(const value_row* r, int d) {
 /* Weight of a key with log2-domain score x under the integer maximum M.     */
 /*  pow2 = 0: the softmax weight 2^(x - M) (eq. logsm with exact exp2).     */
 /*  pow2 = 1: the power-of-two weight A~ = 2^-k of eq. logsm, k = M - c with  */
-/*  c = ceil(x - 1/2) computed in fp32, i.e. k = M - x rounded half up.      */
+/*  c = ceil(x - 1/2), i.e. k = M - x rounded half up. x - 1/2 is formed in   */
+/*  fp64, where it is exact for every finite fp32 x (below 2^53 the two       */
+/*  operands fit 54 bits; above, x is an even integer and the tie rounds back */
+/*  to x, whose ceiling is still x - 1/2 rounded up); in fp32 it is not       */
+/*  (x = -0.5 + 2^-25 would round to -1).                                     */
 /*  (The paper says "round"; rounding half up makes k - M a function of x    */
 /*  alone, so a running maximum that rises by any integer rescales exactly.) */
 static double key_weight(float x, int32_t M, int pow2) {
-  if (pow2) return ldexp(1.0, (int)ceilf(x - 0.5f) - M);
+  if (pow2) return ldexp(1.0, (int)ceil((double)x - 0.5) - M);
   return exp2((double)x - (double)M);
 }
 

@@ -43,7 +43,8 @@ def _exact(x, v8, g):
 def test_rounding_rule_against_exact_rationals():
     rng = np.random.default_rng(1)
     x = (rng.standard_normal(300) * 6).astype(np.float32)
-    x[:6] = [2.5, -1.5, 0.5, 3.0, -2.0, 7.5]        # ties and integers
+    x[:8] = [2.5, -1.5, 0.5, 3.0, -2.0, 7.5,        # ties and integers
+             -0.49999997, 0.49999997]               # one fp32 ulp off a tie
     v8, g = _rows(rng, 300)
     out, M = oracle.attend_x(x, v8, g, pow2=True)
     ref, Mr, ks = _exact(x, v8, g)
@@ -56,6 +57,42 @@ def test_rounding_rule_against_exact_rationals():
         assert abs(kk - d) <= Fraction(1, 2)
         if d.denominator == 2:
             assert kk == d + Fraction(1, 2)
+
+
+def test_rounding_rule_near_ties():
+    """x = n + 1/2 and its fp32 neighbours on both sides, for scores of both
+    signs and magnitudes up to 2^22: every weight follows M - x rounded half up
+    exactly. (A rule that forms x - 1/2 in fp32 rounds -0.5 + 2^-25 to -1 and
+    halves that key's weight.)"""
+    base = []
+    for n in (-40, -7, -3, -2, -1, 0, 1, 2, 5, 300, 2 ** 21):
+        t = np.float32(n + 0.5)
+        base += [t, np.nextafter(t, np.float32(np.inf)), np.nextafter(t, np.float32(-np.inf))]
+    base += [np.float32(-0.49999997), np.float32(0.49999997), np.float32(-2.0 ** -25),
+             np.float32(2.0 ** 22 - 0.5)]
+    g = np.zeros(2, np.int8)
+    for a in base:
+        # two keys: the probed score and the maximum's key at ceil(a); one-hot
+        # values read the probed key's share, 1 / (1 + 2^k)
+        top = np.float32(np.ceil(np.float64(a)))
+        x = np.array([a, top], np.float32)
+        v = np.zeros((2, 64), np.int8)
+        v[0, 0] = 1
+        out, M = oracle.attend_x(x, v, g, pow2=True)
+        k = math.floor(Fraction(M) - Fraction(float(a)) + Fraction(1, 2))
+        assert M == int(top)
+        assert out[0] == 1.0 / (1.0 + 2.0 ** k), (float(a), k, out[0])
+
+
+def test_rounding_rule_printed_counterexample():
+    # x = -0.5 + 2^-25 and -0.1 under M = 0: both round to k = 0, so a one-hot
+    # value on the first key carries exactly half of the mass
+    x = np.array([-0.49999997, -0.1], np.float32)
+    assert float(x[0]) == -0.5 + 2.0 ** -25
+    v = np.zeros((2, 64), np.int8)
+    v[0, 0] = 1
+    out, M = oracle.attend_x(x, v, np.zeros(2, np.int8), pow2=True)
+    assert M == 0 and out[0] == 0.5
 
 
 def test_integer_scores_give_the_softmax():

@@ -55,6 +55,54 @@ def test_query_quantiser_error_bound():
     assert (err <= dl[:, None] * (0.5 + 1e-5)).all()
 
 
+def _rn_f32(fr):
+    """The fp32 nearest to the rational fr, ties to even, decided exactly."""
+    from fractions import Fraction
+    c = np.float32(float(fr))
+    cands = [c, np.nextafter(c, np.float32(np.inf)), np.nextafter(c, np.float32(-np.inf))]
+    best = min(cands, key=lambda f: (abs(Fraction(float(f)) - fr),
+                                     int(np.float32(f).view(np.uint32)) & 1))
+    return np.float32(best)
+
+
+def test_query_step_is_the_correctly_rounded_quotient():
+    """Delta = amax / 127 rounded once to fp32 (Sec. II-A: one step per vector),
+    bit for bit against the exact rational quotient. The amax values are chosen
+    so that amax * fl32(1/127) rounds differently, and so that a double-rounded
+    quotient would too, where such values exist among the samples."""
+    from fractions import Fraction
+    rng = np.random.default_rng(11)
+    cand = rng.uniform(0.1, 1e4, 20000).astype(np.float32)
+    recip = np.float32(1.0) / np.float32(127.0)
+    differ = cand[(cand * recip) != (cand / np.float32(127.0))][:40]
+    assert len(differ) >= 20
+    amax = np.concatenate([differ, np.float32([127.0, 1.0, 3.0e-38, 3.0e38])])
+    q = np.zeros((len(amax), 64), np.float32)
+    q[:, 5] = amax
+    q[:, 9] = -amax / np.float32(3.0)
+    _, dl, _ = oracle.quantize_query(q)
+    for a, d in zip(amax.tolist(), dl.tolist()):
+        want = _rn_f32(Fraction(a) / 127)
+        assert np.float32(d).view(np.uint32) == want.view(np.uint32), (a, d, want)
+
+
+def test_query_quantiser_ties_round_to_even():
+    """amax = 127 makes the scale 127/amax exactly 1, so q^ is q rounded to
+    the nearest integer with ties to even (Sec. II-A, INT8 query): 2.5 -> 2,
+    3.5 -> 4, -2.5 -> -2, 0.5 -> 0, 126.5 -> 126; the clamp keeps 127."""
+    q = np.zeros((1, 64), np.float32)
+    vals = {0: 127.0, 1: 2.5, 2: 3.5, 3: -2.5, 4: -3.5, 5: 0.5, 6: -0.5, 7: 1.5,
+            8: 126.5, 9: -126.5, 10: 2.4999998, 11: 2.5000002, 12: -1.5, 13: 4.5}
+    want = {0: 127, 1: 2, 2: 4, 3: -2, 4: -4, 5: 0, 6: 0, 7: 2, 8: 126, 9: -126,
+            10: 2, 11: 3, 12: -2, 13: 4}
+    for m, v in vals.items():
+        q[0, m] = v
+    qh, dl, _ = oracle.quantize_query(q)
+    assert dl[0] == np.float32(1.0)
+    for m, w in want.items():
+        assert int(qh[0, m]) == w, (m, vals[m], int(qh[0, m]))
+
+
 def test_query_quantiser_zero_vector():
     qh, dl, _ = oracle.quantize_query(np.zeros((2, 64), np.float32))
     assert not qh.any() and not dl.any()
