@@ -92,11 +92,13 @@ __device__ __forceinline__ void wave_sync_lds() {
 typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
 
-// Raw buffer resources over one sequence's cache rows (gfx9 descriptor word 3
-// = 0x00020000: untyped records, byte-granular range). A load at or past the
-// resource's size returns zeros and touches no memory, so tiles past the end
-// of a key range need no clamped addresses, and every offset is 32-bit: a
-// lane-constant part in a vector register and the tile start in a scalar one.
+// Raw buffer resources over the cache rows of one tile (gfx9 descriptor word
+// 3 = 0x00020000: untyped records, byte-granular range). Each load's resource
+// starts at the tile's first row and ends at the key range's last row, and
+// the whole offset is in the vector operand: the hardware compares only that
+// offset (not the scalar one) with the record count, so a lane whose key is
+// at or past the end reads zeros and touches no memory. The tile loops need
+// no clamped addresses, and every offset is 32-bit.
 typedef __amdgpu_buffer_rsrc_t BufRsrc;
 constexpr int kBufWord3 = 0x00020000;
 constexpr int kAuxNt = 2;  // cache policy of the loads: non-temporal
@@ -105,11 +107,25 @@ __device__ __forceinline__ BufRsrc buf_rsrc(const void* base, int64_t n_bytes) {
                                            kBufWord3);
 }
 
-// The streams of one (batch, kv head) sequence that a workgroup reads.
+// The streams of one (batch, kv head) sequence that a workgroup reads, as
+// byte pointers to the sequence's row 0 and the rows that exist: keys
+// (codes, mantissa planes, scales) below t_end, value groups (fp16 or
+// bytes, INT8 exponents) below v_end (the end of the range's last 8-key
+// group).
 struct Streams {
-  BufRsrc codes, planes, scales;  // PoT code rows, mantissa planes, key scales
-  BufRsrc values, exps;           // value groups (fp16 or bytes), INT8 exponents
+  const uint8_t* codes;
+  const uint8_t* planes;
+  const uint8_t* scales;
+  const uint8_t* values;
+  const uint8_t* exps;
+  int t_end, v_end;
 };
+
+// Resource over rows t0 .. lim - 1 of row_bytes bytes each (t0 < lim, both
+// wave-uniform, lim * row_bytes < 2^31).
+__device__ __forceinline__ BufRsrc tile_rsrc(const uint8_t* base, int t0, int lim, int row_bytes) {
+  return buf_rsrc(base + (uint32_t)(t0 * row_bytes), (int64_t)((lim - t0) * row_bytes));
+}
 
 // ---- per-tile register payloads -----------------------------------------------
 template <int MODE, int K>
@@ -170,26 +186,28 @@ __device__ __forceinline__ void load_keys(const DecodeArgs& a, int64_t row, KeyR
 template <int MODE, int K>
 __device__ __forceinline__ void load_keys_buf(const Streams& st, int t0, int lane,
                                               KeyRegs<MODE, K>& r) {
-  const u32x4v c0 = __builtin_amdgcn_raw_buffer_load_b128(st.codes, lane * 32, t0 * 32, kAuxNt);
-  const u32x4v c1 =
-      __builtin_amdgcn_raw_buffer_load_b128(st.codes, lane * 32 + 16, t0 * 32, kAuxNt);
+  const BufRsrc rc = tile_rsrc(st.codes, t0, st.t_end, kDim / 2);
+  const u32x4v c0 = __builtin_amdgcn_raw_buffer_load_b128(rc, lane * 32, 0, kAuxNt);
+  const u32x4v c1 = __builtin_amdgcn_raw_buffer_load_b128(rc, lane * 32 + 16, 0, kAuxNt);
   r.c0 = make_uint4(c0.x, c0.y, c0.z, c0.w);
   r.c1 = make_uint4(c1.x, c1.y, c1.z, c1.w);
   if constexpr (MODE == kScorePot) {
+    if constexpr (K > 0) {
+      const BufRsrc rp = tile_rsrc(st.planes, t0, st.t_end, 8 * K);
 #pragma unroll
-    for (int bb = 0; bb < K; ++bb) {
-      const u32x2v p = __builtin_amdgcn_raw_buffer_load_b64(st.planes, lane * 8 * K + 8 * bb,
-                                                            t0 * 8 * K, kAuxNt);
-      r.pl[bb] = make_uint2(p.x, p.y);
+      for (int bb = 0; bb < K; ++bb) {
+        const u32x2v p = __builtin_amdgcn_raw_buffer_load_b64(rp, lane * 8 * K + 8 * bb, 0, kAuxNt);
+        r.pl[bb] = make_uint2(p.x, p.y);
+      }
     }
   }
-  r.s = __builtin_bit_cast(float,
-                           __builtin_amdgcn_raw_buffer_load_b32(st.scales, lane * 4, t0 * 4, kAuxNt));
+  const BufRsrc rs = tile_rsrc(st.scales, t0, st.t_end, 4);
+  r.s = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, lane * 4, 0, kAuxNt));
 }
 
 // B fragments of one 64-key tile: lane l takes keys t0 + 32*kb + 8*(l/16) ..+7
 // of dim 16*nb + l%16, one 16-byte (fp16) or 8-byte (INT8) load each from the
-// token-interleaved cache, through the sequence's value resource: groups past
+// token-interleaved cache, through the tile's value resource: groups past
 // the range's last group read zeros (their weights are 0). With INT8 values
 // the lane also loads the exponents of the 8 keys t0 + 32*part + 8*grp ..+7
 // whose weights it forms in stage 2.
@@ -197,6 +215,7 @@ template <bool V8>
 __device__ __forceinline__ void load_values_buf(const Streams& st, int t0, int lane,
                                                 ValRegs<V8>& v) {
   constexpr int kGroupBytes = V8 ? 8 * kDim : 16 * kDim;  // one 8-token group
+  const BufRsrc rv = tile_rsrc(st.values, t0, st.v_end, kGroupBytes / 8);
   const int voff = (lane >> 4) * kGroupBytes + (lane & 15) * (V8 ? 8 : 16);
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) {
@@ -204,18 +223,18 @@ __device__ __forceinline__ void load_values_buf(const Streams& st, int t0, int l
     for (int nb = 0; nb < 4; ++nb) {
       const int off = voff + kb * 4 * kGroupBytes + nb * 16 * (V8 ? 8 : 16);
       if constexpr (V8) {
-        const u32x2v w = __builtin_amdgcn_raw_buffer_load_b64(st.values, off, t0 * kDim, kAuxNt);
+        const u32x2v w = __builtin_amdgcn_raw_buffer_load_b64(rv, off, 0, kAuxNt);
         v.f[kb][nb] = make_uint2(w.x, w.y);
       } else {
-        const u32x4v w =
-            __builtin_amdgcn_raw_buffer_load_b128(st.values, off, t0 * 2 * kDim, kAuxNt);
+        const u32x4v w = __builtin_amdgcn_raw_buffer_load_b128(rv, off, 0, kAuxNt);
         v.f[kb][nb] = make_uint4(w.x, w.y, w.z, w.w);
       }
     }
   }
   if constexpr (V8) {
     const int part = (lane & 15) >> 3, grp = lane >> 4;
-    const u32x2v g = __builtin_amdgcn_raw_buffer_load_b64(st.exps, 32 * part + 8 * grp, t0, 0);
+    const BufRsrc re = tile_rsrc(st.exps, t0, st.v_end, 1);
+    const u32x2v g = __builtin_amdgcn_raw_buffer_load_b64(re, 32 * part + 8 * grp, 0, 0);
     v.g = make_uint2(g.x, g.y);
   }
 }
@@ -446,17 +465,19 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
 
   KeyRegs<MODE, K> kr[2];
   const int g_last = (t_end - 1) & ~7;  // first token of the range's last 8-token group
-  Streams st;
+  Streams st{};
+  st.t_end = t_end;
+  st.v_end = g_last + 8;
   if constexpr (MODE == kScorePot || MODE == kScoreDs4a) {
-    st.codes = buf_rsrc(a.codes_se + row0 * (kDim / 2), (int64_t)t_end * (kDim / 2));
-    st.scales = buf_rsrc(a.key_scale + row0, (int64_t)t_end * 4);
-    if constexpr (K > 0) st.planes = buf_rsrc(a.codes_m + row0 * 8 * K, (int64_t)t_end * 8 * K);
+    st.codes = a.codes_se + row0 * (kDim / 2);
+    st.scales = reinterpret_cast<const uint8_t*>(a.key_scale + row0);
+    if constexpr (K > 0) st.planes = a.codes_m + row0 * 8 * K;
   }
   if constexpr (V8) {
-    st.values = buf_rsrc(a.v8 + row0 * kDim, (int64_t)(g_last + 8) * kDim);
-    st.exps = buf_rsrc(a.v_exp + row0, g_last + 8);
+    st.values = a.v8 + row0 * kDim;
+    st.exps = reinterpret_cast<const uint8_t*>(a.v_exp + row0);
   } else {
-    st.values = buf_rsrc(a.v + row0 * kDim, (int64_t)(g_last + 8) * kDim * 2);
+    st.values = reinterpret_cast<const uint8_t*>(a.v + row0 * kDim);
   }
   // key codes of tile jt; keys past the range read zeros (PoT, byte decode)
   // or the range's last key (INT8, fp16)
@@ -745,7 +766,8 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
     // ceil is monotonic, so M = max over lanes of ceil(x): the reduction over
     // the four rows of 16 lanes runs on int32 (swap odd with even rows, then
     // the two halves; v_permlane*_swap, no LDS)
-    int mt = hvalid ? (int)ceilf(mx) : INT_MIN;
+    // a lane whose keys are all past the range holds -inf (no int32 ceiling)
+    int mt = (hvalid && mx > -INFINITY) ? (int)ceilf(mx) : INT_MIN;
     {
       const auto r16 = __builtin_amdgcn_permlane16_swap((uint32_t)mt, (uint32_t)mt, false, false);
       mt = max((int)r16[0], (int)r16[1]);
@@ -791,10 +813,15 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
       float p0, p1;
       if constexpr (kPow2) {
         // A~ = 2^-k with k = M - ceil(x - 1/2) (M - x rounded half up):
-        // p = 2^(ceil(x - 1/2) - M + 12), exact; keys masked to -inf get 0
+        // p = 2^(ceil(x - 1/2) - M + 12), exact; keys masked to -inf get 0.
+        // ceil(x - 1/2) is ceil(x), less one when ceil(x) - x >= 1/2: that
+        // difference is exact in fp32 where it decides (x - 1/2 itself is
+        // not: -0.5 + 2^-25 would round to -1)
         auto pw = [&](float x) -> float {
+          const float c = ceilf(x);
+          const float r = (c - x >= 0.5f) ? c - 1.0f : c;
           return x > -INFINITY
-                     ? __builtin_amdgcn_ldexpf(1.0f, (int)ceilf(x - 0.5f) - m_run + (int)kPScale)
+                     ? __builtin_amdgcn_ldexpf(1.0f, (int)r - m_run + (int)kPScale)
                      : 0.0f;
         };
         p0 = pw(xv[2 * i]);
