@@ -322,6 +322,34 @@ pot_status pot_append_decode_attention_v8(const pot_format* fmt, int32_t engine,
                                           void* workspace, size_t ws_bytes,
                                           pot_debug* dbg, void* stream);
 
+/* Bytes of the static device scratch behind pot_decode_attention_noalloc
+ * (one copy per GPU, held until the process ends). */
+#define POT_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+
+/* pot_decode_attention for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the same computation, kernels and arguments, without the
+ * workspace arguments. The workspace is a static device array of
+ * POT_NOALLOC_SCRATCH_BYTES per GPU that the library owns; the call allocates
+ * nothing (no hipMalloc, no hipFree). Its device address is looked up once
+ * per GPU, on the first call with that GPU current; `stream` must belong to
+ * the current GPU.
+ * Errors: as pot_decode_attention; a shape whose workspace bound
+ * (pot_decode_workspace_bytes, or pot_decode_workspace_bytes_for_splits with
+ * dbg->force_splits) exceeds POT_NOALLOC_SCRATCH_BYTES -> POT_ERR_WORKSPACE,
+ * checked on the host before any HIP call. At the TinyLlama shape (Hq = 32,
+ * Hkv = 4) that bound is about 2.5 MB at B = 64 and grows by 264 bytes per
+ * query head and key split.
+ * Every call on one GPU shares that GPU's scratch, which keeps the previous
+ * call's contents (the kernels write every word they read, so nothing needs
+ * clearing): calls that overlap in time on one GPU race and must not be made. */
+pot_status pot_decode_attention_noalloc(const pot_format* fmt, const float* q,
+                                        const uint8_t* codes_se, const uint8_t* codes_m,
+                                        const float* key_scale, const uint16_t* v_cache,
+                                        int64_t t_cap, const int32_t* kv_head_of_q, int32_t B,
+                                        int32_t Hq, int32_t Hkv, int32_t T, float* out,
+                                        pot_debug* dbg, void* stream);
+
 /* ---- comparison paths on the same cache skeleton --------------------- */
 
 /* INT8 uniform key codes (the multiply-accumulate comparator of Sec. III and

@@ -84,6 +84,8 @@ def _load_library():
                                               i32, i32, P, P, S, dbg_p, P]),
         "pot_append_decode_attention_v8": (i32, [fmt_p, i32, P, P, P, P, P, P, P, P, i64, P,
                                                  i32, i32, i32, i32, P, P, S, dbg_p, P]),
+        "pot_decode_attention_noalloc": (i32, [fmt_p, P, P, P, P, P, i64, P, i32, i32,
+                                               i32, i32, P, dbg_p, P]),
         "pot_ds4a_decode_attention": (i32, [fmt_p, P, P, P, P, i64, P, i32, i32, i32, i32, P, P,
                                             S, dbg_p, P]),
         "pot_int8_encode_keys": (i32, [P, i64, i64, i32, P, P, P]),
@@ -217,6 +219,17 @@ def pot_decode_attention(fmt: pot_format, q, codes_se, codes_m, key_scale,
         _ptr(key_scale), _ptr(v_fp16), int(t_cap), hp, B, Hq, Hkv, T,
         _ptr(out), _ptr(workspace), nbytes,
         ctypes.byref(dbg) if dbg is not None else None, _stream(stream)))
+
+
+def pot_decode_attention_noalloc(fmt: pot_format, q, codes_se, codes_m, key_scale,
+                                 v_fp16, t_cap: int, kv_head_of_q, B: int, Hq: int,
+                                 Hkv: int, T: int, out, dbg: pot_debug | None = None,
+                                 stream=None) -> None:
+    _, hp = _heads(kv_head_of_q)
+    _check(_lib.pot_decode_attention_noalloc(
+        ctypes.byref(fmt), _ptr(q), _ptr(codes_se), _ptr(codes_m),
+        _ptr(key_scale), _ptr(v_fp16), int(t_cap), hp, B, Hq, Hkv, T,
+        _ptr(out), ctypes.byref(dbg) if dbg is not None else None, _stream(stream)))
 
 
 def pot_append_decode_attention(fmt: pot_format, q, k_new, v_new, codes_se, codes_m,

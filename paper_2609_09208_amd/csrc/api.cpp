@@ -32,6 +32,20 @@ pot_status fail(pot_status st, const char* fmt, ...) {
   return st;
 }
 
+}  // namespace
+
+pot_status potattn::report_error(pot_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+namespace {
+
 pot_status ok() {
   g_last_error.clear();
   return POT_OK;

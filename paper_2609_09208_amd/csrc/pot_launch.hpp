@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "pot_attn.h"
+
 namespace potattn {
 
 constexpr int kMaxHqArg = 128;  // query heads addressable through kernel args
@@ -42,6 +44,10 @@ hipError_t launch_store_values_i8(const uint16_t* src, int64_t n_seq, int64_t n_
                                   hipStream_t stream);
 
 hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream);
+
+// Records a printf-style detail for pot_last_error() on the calling thread and
+// returns st (api.cpp).
+pot_status report_error(pot_status st, const char* fmt, ...);
 
 // kScoreDs4a: PoT-4 codes decoded to int8 bytes and scored by v_dot4 (a
 // multiply path, kept beside the shift path for measurement)

@@ -253,3 +253,21 @@ def test_pow2_rejects_bad_arguments():
     assert D(*args(ve=FAKE + 2)) == pa.POT_ERR_INVALID_ARG
     assert D(*args(T=4097)) == pa.POT_ERR_INVALID_ARG
     assert D(*args(fmt=pa.make_format(mant_bits=2), engine=1)) == pa.POT_ERR_UNSUPPORTED
+
+
+def test_noalloc_rejects_shapes_beyond_its_scratch():
+    # the workspace bound is checked on the host before any HIP call
+    with pytest.raises(pa.PotError) as e:
+        pa.pot_decode_attention_noalloc(pa.make_format(0), FAKE, FAKE, None, FAKE, FAKE, 4096,
+                                        np.arange(32, dtype=np.int32) // 8, 4096, 32, 4, 4096,
+                                        FAKE)
+    assert e.value.status == pa.POT_ERR_WORKSPACE
+    assert "static scratch" in pa.pot_last_error()
+    # forced splits count against the same bound
+    dbg = pa.pot_debug()
+    dbg.force_splits = 4096
+    with pytest.raises(pa.PotError) as e:
+        pa.pot_decode_attention_noalloc(pa.make_format(0), FAKE, FAKE, None, FAKE, FAKE,
+                                        1 << 20, np.arange(32, dtype=np.int32) // 8, 16, 32, 4,
+                                        1 << 20, FAKE, dbg=dbg)
+    assert e.value.status == pa.POT_ERR_WORKSPACE
