@@ -66,12 +66,6 @@ __device__ __forceinline__ uint32_t xad_u32(uint32_t a, uint32_t b, uint32_t c) 
   asm("v_xad_u32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
   return r;
 }
-// (m & a) | (~m & b) as one v_bfi_b32
-__device__ __forceinline__ uint32_t bfi_u32(uint32_t m, uint32_t a, uint32_t b) {
-  uint32_t r;
-  asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(r) : "v"(m), "v"(a), "v"(b));
-  return r;
-}
 // max(a, b) for scores (never NaN) as v_max_f32 without operand canonicalisation
 __device__ __forceinline__ float max_f32(float a, float b) {
   return __builtin_amdgcn_fmed3f(a, b, __builtin_inff());
@@ -541,12 +535,14 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
       for (int i = 0; i < 8; ++i) {
         const uint32_t wi = w[i];
         const uint32_t x = wi & 0x77777777u;  // e per nibble
-        // each element's weight as a 4-bit two's complement nibble: 1, -1
-        // for a negative element, 0 for the zero code (e = 7, never
-        // negative): bit 0 is "e != 7", bits 1..3 copy the sign bit
-        const uint32_t s1 = wi >> 1, s2 = wi >> 2;
-        const uint32_t sw0 = bfi_u32(0x11111111u, ~(wi & s1 & s2), s2);
-        const uint32_t sw = bfi_u32(0x77777777u, bfi_u32(0x33333333u, sw0, s1), wi);
+        // e + 1 per nibble (no carry between nibbles): bit 3 is set exactly
+        // for the zero code, e = 7
+        const uint32_t y = x + 0x11111111u;
+        // per nibble, bit 3: the sign; bit 2: "not the zero code". Moved to
+        // the top of a 16-bit half and shifted arithmetically by 14 they give
+        // the element's weight: 1, -1, or 0 for the zero code (never
+        // negative)
+        const uint32_t sw = (wi & 0x88888888u) | (~(y >> 1) & 0x44444444u);
         // the mantissa bits of this code word's 8 elements, one byte per
         // plane, copied into both halves (bit n for element 8c + n in the
         // low half, bit n + 4 in the high half)
@@ -567,10 +563,10 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
         for (int k = 0; k < 4 * kCols; ++k) qq[k] = (uint32_t)qb[toff + 4 * kCols * i + k];
 #pragma unroll
         for (int n = 0; n < 4; ++n) {
+          // exponents of elements 8c + n and 8c + n + 4, one per half
           const s16x2 sh = __builtin_bit_cast(s16x2, (x >> (4 * n)) & 0x000F000Fu);
-          // the weights of elements 8c + n and 8c + n + 4, sign-extended
-          // from the top nibble of each half
-          const s16x2 sg = __builtin_bit_cast(s16x2, sw << (12 - 4 * n)) >> (short)12;
+          // the weights of elements 8c + n and 8c + n + 4
+          const s16x2 sg = __builtin_bit_cast(s16x2, sw << (12 - 4 * n)) >> (short)14;
           s16x2 mw[KP];
 #pragma unroll
           for (int bb = 0; bb < K; ++bb) {
