@@ -31,6 +31,10 @@ The line reports:
 --sweep-point B,T,k (repeatable) and --sweep-layers N restrict the sweep to
 those 22-layer points and change their layer count (one point per process for
 counter runs).
+
+--cpu-configs times only the CPU oracle, on the four single-layer
+configurations in full (every key encoded, every query head attended), on one
+thread and on every host thread; no GPU use.
 """
 from __future__ import annotations
 
@@ -117,6 +121,23 @@ def cpu_model() -> str:
     return "unknown"
 
 
+def host_threads() -> int:
+    """Host threads the oracle may use: every CPU this process may run on,
+    capped by the host's per-job share when the environment sets one
+    (OMP_NUM_THREADS; a one-GPU job's share of a shared host)."""
+    n = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+    share = os.environ.get("OMP_NUM_THREADS")
+    if share and share.isdigit() and int(share) > 0:
+        n = min(n, int(share))
+    return max(1, n)
+
+
+def host_info() -> dict:
+    return {"cpu_model": cpu_model(), "nproc": os.cpu_count(),
+            "affinity_cpus": len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity")
+            else None, "omp_num_threads": os.environ.get("OMP_NUM_THREADS")}
+
+
 def cpu_baseline(T: int, budget_s: float) -> dict:
     """The oracle (plain C) on (batch, kv-head) slices of the same workload:
     append-encode one key row, then decode attention of the G = 8 query heads
@@ -150,14 +171,72 @@ def cpu_baseline(T: int, budget_s: float) -> dict:
                     return n, el
 
     n1, e1 = run(1, budget_s / 2)
-    threads = max(1, min(16, os.cpu_count() or 1))
+    threads = host_threads()
     nt, et = run(threads, budget_s / 2)
+    info = host_info()
     return {"value": nt * G * T / et, "unit": "keys/s", "cores": threads, "kind": "oracle",
-            "value_1thread": n1 * G * T / e1,
+            "value_1thread": n1 * G * T / e1, **info,
             "sample": f"(batch, kv-head) slices of T={T}: 1 appended key + {G} query heads over "
                       f"{T} PoT-4 keys; {n1} slices in {e1:.1f} s on 1 thread, {nt} slices in "
-                      f"{et:.1f} s on {threads} threads; host CPU {cpu_model()}, "
-                      f"{os.cpu_count()} logical CPUs"}
+                      f"{et:.1f} s on {threads} threads; host CPU {info['cpu_model']}, "
+                      f"{info['nproc']} logical CPUs, {info['affinity_cpus']} available"}
+
+
+# The four single-layer configurations (name, B, T, mant_bits, hadamard,
+# query heads; one head means one kv head and no channel scale): tiny single head, TinyLlama layer at T=4096 (PoT-4), at
+# T=32768 (PoT-M1), and B=8 T=32768 with Hadamard + PoT-M4.
+CPU_CONFIGS = [("C1 tiny single head", 1, 256, 0, False, 1),
+               ("C2 TinyLlama layer", 1, 4096, 0, False, HQ),
+               ("C3 TinyLlama layer, PoT-M1", 1, 32768, 1, False, HQ),
+               ("C4 B=8, Hadamard + PoT-M4", 8, 32768, 4, True, HQ)]
+
+
+def cpu_configs() -> None:
+    """The oracle timed on each single-layer configuration in full: encode
+    every key row and run decode attention for every (batch, query head),
+    once on one thread and once split over (batch, kv head) units on every
+    host thread. One JSON line per configuration."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    import numpy as np
+
+    import oracle
+    from workloads import make_decode_inputs
+
+    threads = host_threads()
+    info = host_info()
+    for name, B, T, k, had, hq in CPU_CONFIGS:
+        hkv = 1 if hq == 1 else HKV
+        g = hq // hkv
+        d = make_decode_inputs(7, B=B, Hq=hq, Hkv=hkv, T=T, channel_scale=hq > 1)
+        units = [(b, h) for b in range(B) for h in range(hkv)]
+
+        def unit(bh):
+            b, h = bh
+            rows = d["k_bits"][b, h]
+            se, cm, sc = oracle.encode_keys(rows, mant_bits=k, hadamard=had)
+            oracle.pot_decode(d["q"][b, h * g:(h + 1) * g][None], se, cm, sc, d["v_bits"][b, h],
+                              d["t_cap"], np.zeros(g, np.int32), 1, g, 1, T, mant_bits=k,
+                              hadamard=had)
+
+        t0 = time.perf_counter()
+        for u in units:
+            unit(u)
+        t1 = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        with ThreadPoolExecutor(max_workers=threads) as ex:
+            list(ex.map(unit, units))
+        tn = time.perf_counter() - t0
+        keys = B * hq * T
+        print(json.dumps({"config": name, "B": B, "T": T, "Hq": hq, "Hkv": hkv,
+                          "mant_bits": k, "hadamard": had, "kind": "oracle",
+                          "seconds_1thread": t1, "seconds_all_threads": tn,
+                          "threads": threads, "units": len(units),
+                          "keys_scored_per_s_1thread": keys / t1,
+                          "keys_scored_per_s_all_threads": keys / tn,
+                          "rows_per_s_all_threads": B * hkv * T / tn,
+                          "work": "encode every key row, then decode attention of every "
+                                  "(batch, query head)", **info}), flush=True)
 
 
 class Layers:
@@ -451,6 +530,9 @@ def main() -> int:
                     help="with --sweep: run only this 22-layer point (repeatable)")
     ap.add_argument("--sweep-layers", type=int, default=None,
                     help="with --sweep: layers per point instead of 22")
+    ap.add_argument("--cpu-configs", action="store_true",
+                    help="only time the CPU oracle on the four single-layer configurations "
+                         "in full (one thread and all host threads); no GPU use")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run device-to-device copies of BYTES bytes (calibrates "
                          "the FETCH_SIZE / WRITE_SIZE counters against a known size)")
@@ -460,6 +542,10 @@ def main() -> int:
               "(the decode path shards over (batch, kv head) with no communication)",
               file=sys.stderr)
         return 2
+
+    if args.cpu_configs:
+        cpu_configs()
+        return 0
 
     import numpy as np
     import torch
@@ -512,7 +598,12 @@ def main() -> int:
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": read_traffic() if (B, T, k) == (64, 32768, 0) else None,
-                     "kernel": f"potattn::decode_kernel<0, 8, {k}, false, 0> (SAC, G = 8, fp16 V)",
+                     "kernel": f"potattn::decode_kernel<0, 8, {k}, false, 0> (SAC, G = 8, fp16 V: "
+                               "products by packed 16-bit shifts, signs and int32 sums by "
+                               "v_dot2_i32_i16 with weights -1/0/+1)",
+                     "note": "score cores built from shifts and adds alone (v_lshl_add_u32, "
+                             "SDWA shift + v_xad_u32) measured 0.57-0.60 of 8 TB/s in this "
+                             "kernel; the v_dot2 accumulate is the one timed here",
                      "alg_bytes_per_launch": alg, "launch_us": kern_s * 1e6,
                      "launch_us_median": float(np.median(kus)), "launch_us_best": float(kus.min()),
                      "launches_timed": int(kus.size),

@@ -219,9 +219,10 @@ pot_status pot_workspace_init(void* workspace, size_t ws_bytes, void* stream);
  *               time.
  * Steps: q is rotated (if hadamard) and quantised to int8 with step
  * Delta = amax/127; each score is the exact int32 sum of sign-flipped
- * shifts of q^ (eq. sac: q^ 2^(F-e), formed by packed 16-bit arithmetic
- * shifts of q^ 2^7 and summed with weights +-1, 0 for the zero code, by
- * v_dot2_i32_i16; PoT-Mk adds one such sum per mantissa bit plane, combined
+ * shifts of q^ (eq. sac: the products q^ 2^(F-e) are formed by packed 16-bit
+ * arithmetic shifts of q^ 2^7; the signs and the sum are applied by
+ * v_dot2_i32_i16, the dot unit's multiply-add, with weights +-1, 0 for the
+ * zero code; PoT-Mk adds one such sum per mantissa bit plane, combined
  * by shifts); x = acc * s * Delta * log2(e) * 2^-(F+k) / 8 in a fixed fp32
  * order; the running maximum is the integer M = ceil(max x)
  * (eq. logsm) so rescales are exact powers of two; weights 2^(x-M) multiply

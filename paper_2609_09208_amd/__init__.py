@@ -330,6 +330,7 @@ def alloc_value_cache_int8(B: int, Hkv: int, t_cap: int, device):
 
 
 def alloc_workspace(nbytes: int, device):
-    """Zero-initialised workspace (the split counters must start at zero)."""
+    """Workspace buffer for the decode calls (zero-filled; the kernels write
+    every word they read, so any contents would do)."""
     import torch
     return torch.zeros(max(int(nbytes), 256), dtype=torch.uint8, device=device)

@@ -15,10 +15,11 @@
 //     kv head, read through the scalar cache one code word's group at a
 //     time). v_pk_ashrrev_i16 shifts each half by its element's exponent e:
 //     q 2^7 >> e = q 2^(7 - e), exact since the low 7 bits are clear, so
-//     every product is formed by the shifter with head-room F_int = 7 >= e
-//     (eq. exact). v_dot2_i32_i16 with weights sigma in {-1, +1} (0 for the
-//     zero code) flips the signs and adds both halves into the int32 sum (a
-//     signed add; no product q 2^k goes through a multiplier). PoT-Mk (Sec.
+//     every product q 2^(7 - e) is formed by the shifter with head-room
+//     F_int = 7 >= e (eq. exact). v_dot2_i32_i16 then applies the signs and
+//     sums both halves into the int32 score: it is the dot unit's integer
+//     multiply-add, used here with weights sigma in {-1, +1} (0 for the zero
+//     code), so its multipliers only ever see -1, 0 or +1. PoT-Mk (Sec.
 //     II-D) adds one sum per mantissa bit plane b over the same shifted
 //     operands, with weight sigma where bit b of the element's mantissa is
 //     set and 0 elsewhere; the key's sum is 2^k S_lead + sum_b 2^b S_b, the
@@ -522,10 +523,10 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
       // Two elements of one head per 16-bit-pair operand (element 8c + n in
       // the low half, 8c + n + 4 in the high half). v_pk_ashrrev_i16 shifts
       // each half by its element's exponent: q 2^7 >> e = q 2^(7 - e), exact.
-      // v_dot2_i32_i16 with weights sigma = +-1 per half, and 0 for the zero
-      // code (e = 7, whose shifted operand is q), then flips the signs and
-      // adds both halves into the int32 sum (a signed add: no product q 2^k
-      // goes through a multiplier). PoT-Mk: the value is sigma (2^k + j)
+      // v_dot2_i32_i16 (the dot unit's multiply-add) with weights sigma =
+      // +-1 per half, and 0 for the zero code (e = 7, whose shifted operand
+      // is q), then applies the signs and adds both halves into the int32
+      // sum. PoT-Mk: the value is sigma (2^k + j)
       // 2^-e, so the key's sum is 2^k times the leading sum plus 2^b times
       // the sum over the elements whose mantissa j has bit b set, each over
       // the same shifted operands with weights sigma or 0.
