@@ -99,14 +99,13 @@ int split_count_for_slots(long units, long slots) {
 }
 
 // Split count when the grid would fill the GPU's resident slots with short
-// splits: a split shorter than four 256-key tiles costs more in the
-// workgroup's fixed work and in the combine than its extra parallelism gains
-// (B = 1, T = 32768: 50.6 us with 128 one-tile splits, 29.3 us with 32
-// four-tile splits, 33.5 us with 16 eight-tile splits), unless that would
-// leave fewer than 128 workgroups (half the CUs) when the keys allow more
-// (B = 1, T = 4096: 21.8 us with 16 one-tile splits, 25.5 us with 4).
-constexpr int kMinTilesPerSplit = 4;
-constexpr long kMinWorkgroups = 128;
+// splits: splits of at least two 256-key tiles, unless that leaves fewer
+// than 256 workgroups (one per CU) when the keys allow more. Measured with
+// the four-wave split combine: B = 1, T = 32768: 18.6 us with 64 two-tile
+// splits, 19.2 us with 128 one-tile splits, 22.5 us with 32 four-tile
+// splits; B = 1, T = 4096: 17.1 us with 16 one-tile splits, 17.5 us with 8.
+constexpr int kMinTilesPerSplit = 2;
+constexpr long kMinWorkgroups = 256;
 
 int split_count_short_ranges(long units, int tiles) {
   const int s_len = std::max(1, tiles / kMinTilesPerSplit);
@@ -152,10 +151,13 @@ struct WsLayout {
   size_t qbuf, part_m, part_l, part_o, total;
 };
 
+// Workspace: one slot of prepared query operands per decode workgroup
+// (B * Hkv * S slots; each workgroup writes its own and reads it back through
+// the scalar cache), then the split partials.
 WsLayout ws_layout(long B, long Hq, long Hkv, long S) {
   WsLayout w;
   w.qbuf = 0;
-  w.part_m = align_up((size_t)(B * Hkv) * query_words((int)(Hq / Hkv)) * 4, 256);
+  w.part_m = align_up((size_t)(B * Hkv * S) * query_words((int)(Hq / Hkv)) * 4, 256);
   w.part_l = w.part_m + align_up((size_t)(B * Hq * S) * 4, 256);
   w.part_o = w.part_l + align_up((size_t)(B * Hq * S) * 4, 256);
   w.total = w.part_o + align_up((size_t)(B * Hq * S) * 64 * 4, 256);

@@ -73,6 +73,12 @@ __device__ __forceinline__ float max_f32(float a, float b) {
 }
 
 
+// Waits until this wave's vector stores are acknowledged by the L2. A
+// workgroup barrier alone does not: it orders the wave's accesses for the
+// other waves' vector loads, but the scalar cache, which reads the prepared
+// query operands, fills from the L2.
+__device__ __forceinline__ void wait_stores_in_l2() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
 __device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
@@ -282,45 +288,41 @@ struct QLayout {
                                                      : (kDim / 2) * G;
 };
 
+// The new token of one (batch, kv head) sequence appended at row T - 1
+// (Sec. II-F, a cache that holds only codes): wave 0 encodes the key with the
+// row absmax scale, wave 1 stores the values (fp16, or INT8 with their
+// exponent). Only the workgroup whose key range holds row T - 1 calls it.
+template <int K>
+__device__ __forceinline__ void append_token(const DecodeArgs& a, int64_t seq, int wave) {
+  const int64_t row = seq * a.t_cap + (a.T - 1);
+  if (wave == 0)
+    encode_key_row_wave(reinterpret_cast<const __half*>(a.app_k) + seq * kDim, a.hadamard, 0,
+                        a.app_key_scale + row, a.app_codes_se + row * (kDim / 2),
+                        a.app_codes_m + row * 8 * K, a.app_tab);
+  else if (wave == 1 && a.app_v8 != nullptr)
+    store_value_token_i8_wave(a.app_v + seq * kDim, a.app_v8 + seq * a.t_cap * kDim,
+                              a.app_v_exp + seq * a.t_cap, a.T - 1);
+  else if (wave == 1)
+    store_value_token_wave(a.app_v + seq * kDim, a.app_v_cache + seq * a.t_cap * kDim, a.T - 1);
+}
+
 // Rotates (optionally) and quantises the G query vectors of one (batch, kv
-// head) and writes the operand words the decode kernel reads through the
-// scalar cache. Grid (Hkv, B), 4 waves; wave w handles heads w, w + 4. With a
-// fused append it first writes the sequence's new cache row.
-template <int MODE, int G, int K, bool DEBUG>
-__global__ __launch_bounds__(kBlock) void prep_queries_kernel(const DecodeArgs a) {
+// head) and writes the operand words and per-head score factors that the
+// score loop reads through the scalar cache, into qb (this workgroup's own
+// slot of the workspace). Called by all four waves of the workgroup; wave w
+// handles heads w, w + 4. taps: also write the q^ and Delta debug taps.
+template <int MODE, int G, int K>
+__device__ __forceinline__ void prepare_queries(const DecodeArgs& a, int kvh, int b,
+                                                int32_t* __restrict__ qb, bool taps) {
   using QL = QLayout<MODE, G, K>;
-  __shared__ int32_t qh[G * kDim];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int kvh = blockIdx.x, b = blockIdx.y;
-  const int64_t seq = (int64_t)b * a.Hkv + kvh;
-  int32_t* qb = a.qbuf + seq * a.qstride;
+  const int lane = lane_id(), wave = threadIdx.x >> 6;
   float* cb = reinterpret_cast<float*>(qb + QL::kWords);
-  // this wave's query elements, loaded before the append so that their
-  // latency overlaps it
   constexpr int kHeadsPerWave = (G + kWaves - 1) / kWaves;
   float qin[kHeadsPerWave];
 #pragma unroll
   for (int i = 0; i < kHeadsPerWave; ++i) {
     const int h = wave + kWaves * i;
     qin[i] = h < G ? a.q[((int64_t)b * a.Hq + a.q_of_kv[kvh * G + h]) * kDim + lane] : 0.0f;
-  }
-  if constexpr (MODE == kScorePot || MODE == kScoreDs4a) {
-    // fused append of this sequence's new token at row T - 1: wave 0 encodes
-    // the key (row absmax scale), wave 1 stores the values (fp16, or INT8
-    // with their exponent)
-    if (a.app_k != nullptr) {
-      const int64_t row = seq * a.t_cap + (a.T - 1);
-      if (wave == 0)
-        encode_key_row_wave(reinterpret_cast<const __half*>(a.app_k) + seq * kDim, a.hadamard, 0,
-                            a.app_key_scale + row, a.app_codes_se + row * (kDim / 2),
-                            a.app_codes_m + row * 8 * K, a.app_tab);
-      else if (wave == 1 && a.app_v8 != nullptr)
-        store_value_token_i8_wave(a.app_v + seq * kDim, a.app_v8 + seq * a.t_cap * kDim,
-                                  a.app_v_exp + seq * a.t_cap, a.T - 1);
-      else if (wave == 1)
-        store_value_token_wave(a.app_v + seq * kDim, a.app_v_cache + seq * a.t_cap * kDim,
-                               a.T - 1);
-    }
   }
 #pragma unroll
   for (int i = 0; i < kHeadsPerWave; ++i) {
@@ -337,8 +339,15 @@ __global__ __launch_bounds__(kBlock) void prep_queries_kernel(const DecodeArgs a
       if (a.hadamard) qv = (float)(wave_fwht64((double)qv) * 0.125);
       float step;
       const int qi = wave_quantize_int8(qv, &step);
-      qh[h * kDim + lane] = qi;
       if constexpr (MODE == kScorePot) {
+        // word ((c * 4 + n) * G + h) holds, for elements 8c + n (low half)
+        // and 8c + n + 4 (high half), q 2^7 of head h: signed 16-bit
+        // operands in [-16256, 16256] with 7 clear low bits, so an
+        // arithmetic right shift by e <= 7 is exact
+        const uint32_t up = (uint32_t)__shfl_down(qi, 4, 64);
+        if ((lane & 4) == 0)
+          qb[((lane >> 3) * 4 + (lane & 3)) * G + h] =
+              (int32_t)(((uint32_t)(qi * 128) & 0xFFFFu) | ((up * 128u) << 16));
         if (lane == 0)
           cb[h] = __fmul_rn(__fmul_rn(step, log2e_f32()),
                             __builtin_amdgcn_ldexpf(1.0f, -(a.frac_bits + K + 3)));
@@ -359,24 +368,10 @@ __global__ __launch_bounds__(kBlock) void prep_queries_kernel(const DecodeArgs a
         if ((lane & 3) == 0) qb[(lane >> 2) * G + h] = (int32_t)word;
         if (lane == 0) cb[h] = __fmul_rn(__fmul_rn(step, log2e_f32()), 0.125f);
       }
-      if constexpr (DEBUG) {
+      if (taps) {
         if (a.dbg_qhat) a.dbg_qhat[bq * kDim + lane] = (int8_t)qi;
         if (a.dbg_delta && lane == 0) a.dbg_delta[bq] = step;
       }
-    }
-  }
-  if constexpr (MODE == kScorePot) {
-    __syncthreads();
-    // word ((c * 4 + n) * G + h) holds, for elements 8c + n (low half) and
-    // 8c + n + 4 (high half), q 2^7 of head h: signed 16-bit operands in
-    // [-16256, 16256] with 7 clear low bits, so an arithmetic right shift by
-    // e <= 7 is exact
-    for (int i = tid; i < 32 * G; i += kBlock) {
-      const int h = i % G, cn = i / G, n = cn & 3, c = cn >> 2;
-      const int m = 8 * c + n;
-      const uint32_t lo = (uint32_t)(qh[h * kDim + m] * 128) & 0xFFFFu;
-      const uint32_t hi = (uint32_t)(qh[h * kDim + m + 4] * 128) << 16;
-      qb[i] = (int32_t)(lo | hi);
     }
   }
 }
@@ -413,8 +408,11 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
   const int64_t seq = (int64_t)b * a.Hkv + kvh;
   const int64_t row0 = seq * a.t_cap;
   const int8_t* eseq = V8 ? a.v_exp + row0 : nullptr;
-  // query operands and score factors: uniform, read-only here -> scalar loads
-  const int32_t* __restrict__ qb = qbuf + seq * a.qstride;
+  // This workgroup's own slot of query operands and score factors: written
+  // by the prologue below, then only read, through the scalar cache (which
+  // starts each dispatch empty; no other workgroup touches the slot).
+  const int64_t slot = seq * a.n_splits + split;
+  const int32_t* __restrict__ qb = qbuf + slot * a.qstride;
   const float* __restrict__ cb = reinterpret_cast<const float*>(qb + QL::kWords);
 
   // ---- per-wave streaming over 64-key tiles ------------------------------------
@@ -424,27 +422,17 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
   const int row = lane & 15, grp = lane >> 4, hrow = row & 7, part = row >> 3;
   const bool hvalid = hrow < G;
 
-  // INT8 values: the reference exponent g_ref = min g over this workgroup's
-  // keys (Sec. II-E eq. av). Weights are formed as p 2^(g_ref - g_j) <= p, so
-  // they stay in fp16 range for any g, and the sums are scaled by 2^-g_ref at
-  // the end (fp32).
-  int gref = 0;
-  if constexpr (V8) {
-    int gmin = INT_MAX;
-    for (int t = t_begin + 8 * tid; t < t_end; t += 8 * kBlock) {
-      const uint2 w = *reinterpret_cast<const uint2*>(eseq + t);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int gi = (int)(int8_t)(((i < 4) ? w.x : w.y) >> (8 * (i & 3)));
-        gmin = (t + i < t_end) ? min(gmin, gi) : gmin;
-      }
+  // The sequence's new token (fused append) is written before any of this
+  // workgroup's loads: only the workgroup whose range holds row T - 1 reads
+  // that row.
+  if constexpr (MODE == kScorePot || MODE == kScoreDs4a) {
+    if (a.app_k != nullptr && split == a.n_splits - 1) {  // uniform per workgroup
+      append_token<K>(a, seq, wave);
+      wait_stores_in_l2();
+      __syncthreads();
     }
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) gmin = min(gmin, __shfl_xor(gmin, o, 64));
-    if (lane == 0) sm.gm[wave] = gmin;
-    __syncthreads();
-    gref = min(min(sm.gm[0], sm.gm[1]), min(sm.gm[2], sm.gm[3]));
   }
+  int gref = 0;
   float lsum = 0.0f;  // INT8 values: this lane's sum of the unscaled weights
 
   float4v acc[5];
@@ -486,6 +474,30 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
   int j = wave;
   const int j_last = n_tiles - 1;
   if (j < n_tiles) load_keys_tile(j, kr[0]);
+
+  // Query preparation into this workgroup's slot while the first codes load;
+  // with INT8 values also the reference exponent g_ref = min g over this
+  // workgroup's keys (Sec. II-E eq. av): weights are formed as p 2^(g_ref -
+  // g_j) <= p, so they stay in fp16 range for any g, and the sums are scaled
+  // by 2^-g_ref at the end (fp32). One barrier then publishes both.
+  prepare_queries<MODE, G, K>(a, kvh, b, a.qbuf + slot * a.qstride, DEBUG && split == 0);
+  if constexpr (V8) {
+    int gmin = INT_MAX;
+    for (int t = t_begin + 8 * tid; t < t_end; t += 8 * kBlock) {
+      const uint2 w = *reinterpret_cast<const uint2*>(eseq + t);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int gi = (int)(int8_t)(((i < 4) ? w.x : w.y) >> (8 * (i & 3)));
+        gmin = (t + i < t_end) ? min(gmin, gi) : gmin;
+      }
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) gmin = min(gmin, __shfl_xor(gmin, o, 64));
+    if (lane == 0) sm.gm[wave] = gmin;
+  }
+  wait_stores_in_l2();
+  __syncthreads();
+  if constexpr (V8) gref = min(min(sm.gm[0], sm.gm[1]), min(sm.gm[2], sm.gm[3]));
 
   // PoT scoring is long enough to cover the latency of value loads issued at
   // the start of the tile; the short INT8 / fp16 scoring is not, so those
@@ -951,27 +963,54 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
 
 // Merges the key splits of one (batch, query head): M = max_s M_s and
 // O = sum_s 2^(M_s - M) o_s / sum_s 2^(M_s - M) l_s with exact power-of-two
-// weights (Sec. II-E). Grid B * Hq, one thread per output dimension.
+// weights (Sec. II-E). Grid B * Hq, 4 waves: the maximum is a block
+// reduction over the splits; wave w then sums splits w, w + 4, ... with one
+// lane per output dimension (the loads of a wave's splits are independent,
+// so their latencies overlap), and the four waves' sums meet in LDS.
+constexpr int kCombineWaves = 4;
 template <bool DEBUG>
-__global__ __launch_bounds__(64) void combine_kernel(const DecodeArgs a) {
+__global__ __launch_bounds__(64 * kCombineWaves) void combine_kernel(const DecodeArgs a) {
+  __shared__ float so[kCombineWaves][kDim];
+  __shared__ float sl[kCombineWaves];
+  __shared__ int smax[kCombineWaves];
   const int64_t bq = blockIdx.x;
-  const int d = threadIdx.x;
+  const int tid = threadIdx.x, d = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int Sn = a.n_splits;
   const int32_t* __restrict__ pm = a.part_m + bq * Sn;
   const float* __restrict__ pl = a.part_l + bq * Sn;
   const float* __restrict__ po = a.part_o + bq * Sn * kDim;
   int M = INT_MIN;
-  for (int s = 0; s < Sn; ++s) M = max(M, pm[s]);
+  for (int s = tid; s < Sn; s += 64 * kCombineWaves) M = max(M, pm[s]);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) M = max(M, __shfl_xor(M, o, 64));
+  if (d == 0) smax[w] = M;
+  __syncthreads();
+  M = smax[0];
+#pragma unroll
+  for (int i = 1; i < kCombineWaves; ++i) M = max(M, smax[i]);
   float L = 0.0f, O = 0.0f;
-#pragma unroll 4
-  for (int s = 0; s < Sn; ++s) {
+#pragma unroll 8
+  for (int s = w; s < Sn; s += kCombineWaves) {
     const float f = __builtin_amdgcn_ldexpf(1.0f, pm[s] - M);
     L = fmaf(f, pl[s], L);
     O = fmaf(f, po[s * kDim + d], O);
   }
-  a.out[bq * kDim + d] = O / L;
-  if constexpr (DEBUG) {
-    if (d == 0 && a.dbg_m_final) a.dbg_m_final[bq] = M;
+  so[w][d] = O;
+  if (d == 0) sl[w] = L;
+  __syncthreads();
+  if (w == 0) {
+    O = so[0][d];
+    L = sl[0];
+#pragma unroll
+    for (int i = 1; i < kCombineWaves; ++i) {
+      O += so[i][d];
+      L += sl[i];
+    }
+    a.out[bq * kDim + d] = O / L;
+    if constexpr (DEBUG) {
+      if (d == 0 && a.dbg_m_final) a.dbg_m_final[bq] = M;
+    }
   }
 }
 
@@ -981,10 +1020,7 @@ static hipError_t launch_t(const DecodeArgs& a, hipStream_t stream, hipEvent_t e
   if constexpr (VF != 0 && MODE != kScorePot && MODE != kScoreDs4a) {
     return hipErrorInvalidValue;
   } else {
-  hipLaunchKernelGGL((prep_queries_kernel<MODE, G, K, DEBUG>), dim3((uint32_t)a.Hkv, (uint32_t)a.B),
-                     dim3(kBlock), 0, stream, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  hipError_t e = hipSuccess;
   if (ev_begin != nullptr && (e = hipEventRecord(ev_begin, stream)) != hipSuccess) return e;
   const dim3 grid((uint32_t)a.n_splits, (uint32_t)a.Hkv, (uint32_t)a.B);
   hipLaunchKernelGGL((decode_kernel<MODE, G, K, DEBUG, VF>), grid, dim3(kBlock), 0, stream, a,
@@ -992,8 +1028,8 @@ static hipError_t launch_t(const DecodeArgs& a, hipStream_t stream, hipEvent_t e
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (ev_end != nullptr && (e = hipEventRecord(ev_end, stream)) != hipSuccess) return e;
   if (a.n_splits == 1) return hipSuccess;
-  hipLaunchKernelGGL((combine_kernel<DEBUG>), dim3((uint32_t)(a.B * a.Hq)), dim3(64), 0, stream,
-                     a);
+  hipLaunchKernelGGL((combine_kernel<DEBUG>), dim3((uint32_t)(a.B * a.Hq)),
+                     dim3(64 * kCombineWaves), 0, stream, a);
   return hipGetLastError();
   }
 }

@@ -66,8 +66,9 @@ struct DecodeArgs {
   const int8_t* v_exp;       // one exponent g per row: value v^ 2^-g
   float* out;
   // workspace
-  int32_t* qbuf;             // [B*Hkv][qstride]: prepared query operands per kv head
-  int32_t qstride;           // 32-bit words per kv head in qbuf
+  int32_t* qbuf;             // [B*Hkv*n_splits][qstride]: prepared query operands, one
+                             // slot per decode workgroup (written and read by it)
+  int32_t qstride;           // 32-bit words per slot in qbuf
   int32_t* part_m;           // [B*Hq*S]
   float* part_l;             // [B*Hq*S]
   float* part_o;             // [B*Hq*S*64]
@@ -79,7 +80,8 @@ struct DecodeArgs {
   int32_t* dbg_m_split;
   // fused append (PoT only; app_k NULL: none): the new token of every
   // (batch, kv head) sequence is encoded into cache row T - 1 and its values
-  // stored there by the query-preparation kernel, before the decode kernel runs
+  // stored there by the decode workgroup whose key range holds that row,
+  // before it loads any key
   const uint16_t* app_k;     // fp16 [B*Hkv][64]
   const uint16_t* app_v;     // fp16 [B*Hkv][64]
   uint8_t* app_codes_se;     // the cache arrays, written at row T - 1 only

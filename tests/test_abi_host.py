@@ -52,10 +52,11 @@ def test_workspace_sizes():
     # sized for the most splits the planner can pick: 2048 resident slots / 256
     # (batch, kv head) pairs = 8 splits
     per = 64 * 32 * 8                       # partials (m, l, o[64]) per (b, q head, split)
-    # prepared query words per kv head (G = 8): 32 operand words and one
-    # score factor per head, rounded up to 64 words
+    # prepared query words per decode workgroup (one slot per (batch, kv
+    # head, split); G = 8): 32 operand words and one score factor per head,
+    # rounded up to 64 words
     qwords = -(-(32 + 1) * 8 // 64) * 64
-    need = per * (64 + 2) * 4 + 64 * 4 * qwords * 4
+    need = per * (64 + 2) * 4 + 64 * 4 * 8 * qwords * 4
     assert need <= w < need + 4 * 256
     assert pa.pot_decode_workspace_bytes(0, 32, 4, 10) == 0
     assert pa.pot_decode_workspace_bytes(1, 32, 4, 0) == 0
