@@ -963,11 +963,12 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
 
 // Merges the key splits of one (batch, query head): M = max_s M_s and
 // O = sum_s 2^(M_s - M) o_s / sum_s 2^(M_s - M) l_s with exact power-of-two
-// weights (Sec. II-E). Grid B * Hq, 4 waves: the maximum is a block
-// reduction over the splits; wave w then sums splits w, w + 4, ... with one
-// lane per output dimension (the loads of a wave's splits are independent,
-// so their latencies overlap), and the four waves' sums meet in LDS.
+// weights (Sec. II-E). Grid B * Hq, 4 waves; wave w takes splits w, w + 4,
+// ... with one lane per output dimension, and the four waves meet in LDS.
+// Up to 64 splits, every load of a wave is issued before the first wait (one
+// memory latency for the whole merge); more splits go through a loop.
 constexpr int kCombineWaves = 4;
+constexpr int kCombineBatch = 16;  // splits per wave in the single-batch path
 template <bool DEBUG>
 __global__ __launch_bounds__(64 * kCombineWaves) void combine_kernel(const DecodeArgs a) {
   __shared__ float so[kCombineWaves][kDim];
@@ -980,21 +981,52 @@ __global__ __launch_bounds__(64 * kCombineWaves) void combine_kernel(const Decod
   const int32_t* __restrict__ pm = a.part_m + bq * Sn;
   const float* __restrict__ pl = a.part_l + bq * Sn;
   const float* __restrict__ po = a.part_o + bq * Sn * kDim;
-  int M = INT_MIN;
-  for (int s = tid; s < Sn; s += 64 * kCombineWaves) M = max(M, pm[s]);
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) M = max(M, __shfl_xor(M, o, 64));
-  if (d == 0) smax[w] = M;
-  __syncthreads();
-  M = smax[0];
-#pragma unroll
-  for (int i = 1; i < kCombineWaves; ++i) M = max(M, smax[i]);
   float L = 0.0f, O = 0.0f;
+  int M;
+  if (Sn <= kCombineWaves * kCombineBatch) {  // uniform
+    // lane i (< 16) holds M_s and l_s of split s = w + 4 i; every lane holds
+    // o_s[d] of all of them. Splits past the last read the last one
+    // (unconditional loads, so all are in flight together) and are dropped.
+    const int li = min(d, kCombineBatch - 1);
+    const int s_l = w + kCombineWaves * li;
+    const bool valid = d < kCombineBatch && s_l < Sn;
+    const int m_l = pm[min(s_l, Sn - 1)];
+    const float l_l = pl[min(s_l, Sn - 1)];
+    float ov[kCombineBatch];
+#pragma unroll
+    for (int i = 0; i < kCombineBatch; ++i)
+      ov[i] = po[min(w + kCombineWaves * i, Sn - 1) * kDim + d];
+    int mw = valid ? m_l : INT_MIN;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) mw = max(mw, __shfl_xor(mw, o, 64));
+    if (d == 0) smax[w] = mw;
+    __syncthreads();
+    M = max(max(smax[0], smax[1]), max(smax[2], smax[3]));
+    const float f_l = valid ? __builtin_amdgcn_ldexpf(1.0f, m_l - M) : 0.0f;
+    float fl = f_l * l_l;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) fl += __shfl_xor(fl, o, 64);
+    L = fl;
+#pragma unroll
+    for (int i = 0; i < kCombineBatch; ++i) {
+      const float f = __builtin_bit_cast(
+          float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, f_l), i));
+      O = fmaf(f, ov[i], O);
+    }
+  } else {
+    M = INT_MIN;
+    for (int s = tid; s < Sn; s += 64 * kCombineWaves) M = max(M, pm[s]);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) M = max(M, __shfl_xor(M, o, 64));
+    if (d == 0) smax[w] = M;
+    __syncthreads();
+    M = max(max(smax[0], smax[1]), max(smax[2], smax[3]));
 #pragma unroll 8
-  for (int s = w; s < Sn; s += kCombineWaves) {
-    const float f = __builtin_amdgcn_ldexpf(1.0f, pm[s] - M);
-    L = fmaf(f, pl[s], L);
-    O = fmaf(f, po[s * kDim + d], O);
+    for (int s = w; s < Sn; s += kCombineWaves) {
+      const float f = __builtin_amdgcn_ldexpf(1.0f, pm[s] - M);
+      L = fmaf(f, pl[s], L);
+      O = fmaf(f, po[s * kDim + d], O);
+    }
   }
   so[w][d] = O;
   if (d == 0) sl[w] = L;
