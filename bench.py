@@ -393,6 +393,29 @@ def timed_calls(fn, n_layers, reps=10, warm=2):
     return s.elapsed_time(e) / (reps * n_layers) * 1e3
 
 
+def bulk_encode(pa, lay, dev):
+    """The prefill-side bulk key encoder (pot_encode_keys, row scales from the
+    rows) over one layer's whole key cache, B * Hkv * T fp16 rows, rotating
+    over the layers kept with their fp16 keys."""
+    import torch
+    cl = [c for c in lay.layers if "k16" in c]
+    B, T, k = lay.B, lay.T, lay.k
+    n = B * HKV * T
+    out = pa.alloc_pot_cache(B, HKV, T, k, dev)
+    us = timed_calls(lambda i: pa.pot_encode_keys(lay.fmt, cl[i]["k16"], n, 1, 0,
+                                                  out["key_scale"], out["codes_se"],
+                                                  out["codes_m"]), len(cl), reps=10, warm=2)
+    # bit-identical to the cache encoded when the layer was built
+    same = bool(torch.equal(out["codes_se"], cl[-1]["codes_se"]) and
+                torch.equal(out["key_scale"], cl[-1]["key_scale"]))
+    per_row = 2 * D + D // 2 + 4 + 8 * k  # fp16 row in; codes, planes, scale out
+    gbs = n * per_row / (us * 1e-6) / 1e9
+    return {"rows": n, "us_per_call": us, "alg_bytes_per_row": per_row, "achieved_gbs": gbs,
+            "frac": gbs / HBM_PEAK_GBS, "same_codes_as_cache": same,
+            "kernel": f"potattn::encode_pot_kernel<{k}, false>",
+            "timing": f"mean of 10 passes over {len(cl)} layers, HIP events around the passes"}
+
+
 def comparators(pa, lay, dev):
     """fp16 and INT8 kernels and the PoT kernel on the same caches, rotating
     over the layers kept with their fp16 keys."""
@@ -625,6 +648,7 @@ def main() -> int:
                        "note": "the same step captured once as a HIP graph and replayed"}
     if not args.no_compare:
         result["comparators"] = comparators(pa, lay, dev)
+        result["bulk_encode"] = bulk_encode(pa, lay, dev)
     if args.cpu_budget > 0:
         result["cpu_baseline"] = cpu_baseline(T, args.cpu_budget)
     print(json.dumps(result), flush=True)

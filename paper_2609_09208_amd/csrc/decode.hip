@@ -296,7 +296,7 @@ template <int K>
 __device__ __forceinline__ void append_token(const DecodeArgs& a, int64_t seq, int wave) {
   const int64_t row = seq * a.t_cap + (a.T - 1);
   if (wave == 0)
-    encode_key_row_wave(reinterpret_cast<const __half*>(a.app_k) + seq * kDim, a.hadamard, 0,
+    encode_key_row_wave<K>(reinterpret_cast<const __half*>(a.app_k) + seq * kDim, a.hadamard, 0,
                         a.app_key_scale + row, a.app_codes_se + row * (kDim / 2),
                         a.app_codes_m + row * 8 * K, a.app_tab);
   else if (wave == 1 && a.app_v8 != nullptr)

@@ -61,37 +61,59 @@ __device__ __forceinline__ int wave_quantize_int8(float x, float* step) {
   return (int)r;
 }
 
-// Log-nearest PoT-Mk code of one element. Returns the nibble (neg<<3 | e, or
-// 7 for zero) and the mantissa j.
-__device__ __forceinline__ int classify(float x, float s, const EncodeTables& tab, int* j_out) {
-  *j_out = 0;
-  if (!(s > 0.0f) || x == 0.0f || x != x) return kZeroField;
-  const float u = fabsf(x) / s;  // one correctly rounded division
-  if (!(u > tab.zero_cut)) return kZeroField;
-  const int n = 1 << tab.mant_bits;
+// The correctly rounded quotient a / s from r = RN(1 / s): q = RN(a r) is
+// within one ulp of a / s, the residual a - q s is exact in one FMA, and
+// RN(q + residual * r) is the correctly rounded quotient (Markstein's
+// correction step; r must be the correctly rounded reciprocal, finite and
+// non-zero). An infinite q (a infinite, or past the largest float) is the
+// quotient's rounding already; the residual would be inf - inf there.
+__device__ __forceinline__ float div_by_recip(float a, float s, float r) {
+  const float q = a * r;
+  const float c = __builtin_fmaf(__builtin_fmaf(-q, s, a), r, q);
+  return (q < __builtin_inff()) ? c : q;
+}
+
+// Log-nearest PoT-Mk code of one element, mantissa width K (Sec. II-A, eq.
+// pot; Sec. II-D, eq. mant), from u = RN(|x| / s) (a zero or NaN x gives a
+// ratio at or below the zero cut, or NaN); s_bad: s is not positive. Branch-
+// free. Returns the nibble (neg<<3 | e, or 7 for zero) and the mantissa j.
+template <int K>
+__device__ __forceinline__ int code_from_ratio(float u, bool neg, bool s_bad,
+                                               const EncodeTables& tab, int* j_out) {
+  constexpr int n = 1 << K;
+  const bool zero = s_bad || !(u > tab.zero_cut);  // also a NaN ratio
   const uint32_t ub = __float_as_uint(u);
-  const int e2 = (int)((ub >> 23) & 0xFF) - 127;         // u > 2^-7: normal
+  const int e2 = (int)(ub >> 23) - 127;  // u > 2^-7 (normal) where it matters
   const float m = __uint_as_float((ub & 0x007FFFFFu) | 0x3F800000u);  // [1, 2)
-  int c = 0;
-#pragma unroll
-  for (int i = 0; i < 16; ++i) c += (i < n && m > tab.cut[i]) ? 1 : 0;
-  int e, j;
-  if (e2 >= 0) {  // u >= 1: the top binade, saturating at its largest value
-    e = 0;
-    j = (e2 > 0) ? n - 1 : min(c, n - 1);
-  } else if (c == n) {  // rounds up to the next binade's first value
-    e = -e2 - 1;
-    j = 0;
+  if constexpr (K == 0) {
+    // above the cut m rounds up into the next binade; u >= 1 saturates at
+    // e = 0; below 2^-E (above the zero cut) the smallest magnitude
+    const int c = (m > tab.cut[0]) ? 1 : 0;
+    const int e = min(max(-e2 - c, 0), kExpMax);
+    *j_out = 0;
+    return zero ? kZeroField : ((neg ? 8 : 0) | e);
   } else {
-    e = -e2;
-    j = c;
+    int c = 0;
+#pragma unroll
+    for (int i = 0; i < n; ++i) c += (m > tab.cut[i]) ? 1 : 0;
+    // c == n rounds up to the next binade's first value; u >= 1 is the top
+    // binade, saturating at its largest value; below 2^-E (above the zero
+    // cut) the smallest magnitude
+    int e = (c == n) ? -e2 - 1 : -e2;
+    int j = (c == n) ? 0 : c;
+    e = (e2 >= 0) ? 0 : e;
+    j = (e2 > 0) ? n - 1 : ((e2 == 0) ? min(c, n - 1) : j);
+    j = (e > kExpMax) ? 0 : j;
+    e = min(e, kExpMax);
+    *j_out = zero ? 0 : j;
+    return zero ? kZeroField : ((neg ? 8 : 0) | e);
   }
-  if (e > kExpMax) {  // between the zero cut and 2^-E: the smallest magnitude
-    e = kExpMax;
-    j = 0;
-  }
-  *j_out = j;
-  return ((x < 0.0f) ? 8 : 0) | e;
+}
+
+// The same from x and the row scale s (one correctly rounded division).
+template <int K>
+__device__ __forceinline__ int classify(float x, float s, const EncodeTables& tab, int* j_out) {
+  return code_from_ratio<K>(fabsf(x) / s, x < 0.0f, !(s > 0.0f), tab, j_out);
 }
 
 // Encodes one 64-element fp16 key row with the calling wave, one element per
@@ -100,6 +122,7 @@ __device__ __forceinline__ int classify(float x, float s, const EncodeTables& ta
 // the log-nearest code of every element, sign/exponent nibbles packed by lane
 // shuffles (element m at bit 4*(m%8) of dword m/8 of se_out) and mantissa
 // bit-planes by ballots (bit m of the 64-bit plane b of m_out is bit b of j_m).
+template <int K>
 __device__ __forceinline__ void encode_key_row_wave(const __half* __restrict__ k_row,
                                                     int hadamard, int scale_mode,
                                                     float* __restrict__ scale,
@@ -117,13 +140,14 @@ __device__ __forceinline__ void encode_key_row_wave(const __half* __restrict__ k
     s = *scale;
   }
   int j;
-  const int nib = classify(x, s, tab, &j);
+  const int nib = classify<K>(x, s, tab, &j);
   uint32_t w = (uint32_t)nib << (4 * (lane & 7));
   w |= __shfl_xor(w, 1, 64);
   w |= __shfl_xor(w, 2, 64);
   w |= __shfl_xor(w, 4, 64);
   if ((lane & 7) == 0) reinterpret_cast<uint32_t*>(se_out)[lane >> 3] = w;
-  for (int b = 0; b < tab.mant_bits; ++b) {
+#pragma unroll
+  for (int b = 0; b < K; ++b) {
     const unsigned long long plane = __ballot((j >> b) & 1);
     if (lane == 0) reinterpret_cast<unsigned long long*>(m_out)[b] = plane;
   }

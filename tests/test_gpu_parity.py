@@ -34,6 +34,61 @@ def test_encode_every_fp16_pattern(k):
             assert np.array_equal(g[1], o[1]), (k, s)
 
 
+def _f32(bits):
+    return np.array(bits, np.uint32).view(np.float32)
+
+
+# Scales at the edges of the one-reciprocal path: all-ones mantissas (where a
+# Newton step from the hardware reciprocal can land on a tie), the ends of the
+# normal-reciprocal range [2^-126, 2^126] and one ulp past them, subnormal,
+# largest finite, infinite, NaN and negative scales.
+_EDGE_SCALES = _f32([0x3FFFFFFF, 0x3F7FFFFF, 0x4B7FFFFF, 0x37FFFFFF, 0x00FFFFFF, 0x7E7FFFFF,
+                     0x7E800000, 0x7E800001, 0x00800000, 0x007FFFFF, 0x00000001, 0x7F7FFFFF,
+                     0x7F800000, 0x7FC00000, 0xBF800000])
+
+
+@pytest.mark.parametrize("k", [0, 1, 4])
+def test_encode_every_fp16_pattern_edge_scales(k):
+    rows = _all_fp16_rows()
+    for s in _EDGE_SCALES:
+        sc = np.full(1024, s, np.float32)
+        g = gpu_encode(rows, k, key_scale=sc)
+        o = oracle.encode_keys(rows, mant_bits=k, key_scale=sc)
+        assert np.array_equal(g[0], o[0]), (k, hex(int(np.float32(s).view(np.uint32))))
+        if k:
+            assert np.array_equal(g[1], o[1]), (k, s)
+
+
+@pytest.mark.parametrize("k", [0, 2])
+def test_encode_every_fp16_pattern_random_scales(k):
+    # one log-uniform scale per row: many distinct reciprocals on the fast path
+    rng = np.random.default_rng(11 + k)
+    rows = _all_fp16_rows()[rng.permutation(1024)]
+    sc = np.exp2(rng.uniform(-30.0, 20.0, 1024)).astype(np.float32)
+    sc[::7] = (sc[::7].view(np.uint32) | np.uint32(0x7FFFFF)).view(np.float32)
+    g = gpu_encode(rows, k, key_scale=sc)
+    o = oracle.encode_keys(rows, mant_bits=k, key_scale=sc)
+    assert np.array_equal(g[0], o[0])
+    if k:
+        assert np.array_equal(g[1], o[1])
+
+
+@pytest.mark.parametrize("k,had", [(0, False), (0, True), (1, False), (4, True)])
+def test_encode_absmax_every_fp16_pattern(k, had):
+    # row scales from the rows themselves, over every fp16 pattern: in order
+    # (rows of only NaNs, a row holding infinity and NaNs, rows of subnormals)
+    # and shuffled (NaN and infinity mixed into ordinary rows)
+    rng = np.random.default_rng(23)
+    flat = _all_fp16_rows().reshape(-1)
+    for rows in (flat.reshape(1024, 64), flat[rng.permutation(flat.size)].reshape(1024, 64)):
+        g = gpu_encode(rows, k, had)
+        o = oracle.encode_keys(rows, mant_bits=k, hadamard=had)
+        assert np.array_equal(g[0], o[0])
+        if k:
+            assert np.array_equal(g[1], o[1])
+        assert np.array_equal(g[2].view(np.uint32), o[2].view(np.uint32))
+
+
 @pytest.mark.parametrize("k,had", [(0, False), (1, False), (4, False), (0, True),
                                    (1, True), (4, True)])
 def test_encode_absmax_rows(k, had):
