@@ -387,6 +387,24 @@ pot_status pot_ds4a_decode_attention(const pot_format* fmt, const float* q,
                                      void* workspace, size_t ws_bytes,
                                      pot_debug* dbg, void* stream);
 
+/* Decode attention over a PoT or PoT-Mk cache with the codes decoded to
+ * integer weights and scored on the dot unit (a multiply path beside the
+ * shift-accumulate one, Sec. III, eq. ds4a and eq. mant): PoT-4 as
+ * pot_ds4a_decode_attention (bytes sigma 2^(6-e), v_dot4_i32_i8); PoT-Mk as
+ * 16-bit weights sigma (2^k + j) 2^(7-e) (0 for the zero code), at most
+ * 31 * 128, with v_dot2_i32_i16 over q^ for two elements per head, one dot
+ * per head and element pair whatever k. The int32 scores, integer maxima and
+ * outputs equal pot_decode_attention's (same scores tap convention, 2^-(F+k)
+ * for k > 0). Arguments, layout, workspace, taps and errors as
+ * pot_decode_attention. */
+pot_status pot_dot_decode_attention(const pot_format* fmt, const float* q,
+                                    const uint8_t* codes_se, const uint8_t* codes_m,
+                                    const float* key_scale, const uint16_t* v_cache,
+                                    int64_t t_cap, const int32_t* kv_head_of_q, int32_t B,
+                                    int32_t Hq, int32_t Hkv, int32_t T, float* out,
+                                    void* workspace, size_t ws_bytes, pot_debug* dbg,
+                                    void* stream);
+
 /* Decode attention on an unquantised fp16 cache (the FP16 baseline of
  * Sec. IV): q is rounded to fp16, scores accumulate in fp32.
  *  k_fp16 [rows][d] fp16 row-major keys; v_cache as above. */

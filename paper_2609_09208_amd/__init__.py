@@ -88,6 +88,8 @@ def _load_library():
                                                i32, i32, P, dbg_p, P]),
         "pot_ds4a_decode_attention": (i32, [fmt_p, P, P, P, P, i64, P, i32, i32, i32, i32, P, P,
                                             S, dbg_p, P]),
+        "pot_dot_decode_attention": (i32, [fmt_p, P, P, P, P, P, i64, P, i32, i32, i32, i32,
+                                           P, P, S, dbg_p, P]),
         "pot_int8_encode_keys": (i32, [P, i64, i64, i32, P, P, P]),
         "pot_int8_decode_attention": (i32, [P, P, P, P, i64, P, i32, i32, i32,
                                             i32, i32, P, P, S, dbg_p, P]),
@@ -268,6 +270,18 @@ def pot_ds4a_decode_attention(fmt: pot_format, q, codes_se, key_scale, v_fp16, t
     _check(_lib.pot_ds4a_decode_attention(
         ctypes.byref(fmt), _ptr(q), _ptr(codes_se), _ptr(key_scale), _ptr(v_fp16),
         int(t_cap), hp, B, Hq, Hkv, T, _ptr(out), _ptr(workspace), nbytes,
+        ctypes.byref(dbg) if dbg is not None else None, _stream(stream)))
+
+
+def pot_dot_decode_attention(fmt: pot_format, q, codes_se, codes_m, key_scale, v_fp16,
+                             t_cap: int, kv_head_of_q, B: int, Hq: int, Hkv: int, T: int, out,
+                             workspace, ws_bytes=None, dbg: pot_debug | None = None,
+                             stream=None) -> None:
+    _, hp = _heads(kv_head_of_q)
+    nbytes = workspace.numel() * workspace.element_size() if ws_bytes is None else ws_bytes
+    _check(_lib.pot_dot_decode_attention(
+        ctypes.byref(fmt), _ptr(q), _ptr(codes_se), _ptr(codes_m), _ptr(key_scale),
+        _ptr(v_fp16), int(t_cap), hp, B, Hq, Hkv, T, _ptr(out), _ptr(workspace), nbytes,
         ctypes.byref(dbg) if dbg is not None else None, _stream(stream)))
 
 

@@ -18,7 +18,7 @@ LIB = os.path.join(PKG, "libpotattn.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
-    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
+    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
     "-ffp-contract=off", "-fno-gpu-flush-denormals-to-zero",
     "-fhip-fp32-correctly-rounded-divide-sqrt",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
@@ -28,24 +28,43 @@ FLAGS = [
 
 def sources():
     csrc = os.path.join(PKG, "csrc")
-    return sorted(glob.glob(os.path.join(csrc, "*.hip"))) + [os.path.join(csrc, "api.cpp")]
+    return sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.cpp")))
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every HIP source into libpotattn.so (always recompiles)."""
-    out_tmp = LIB + ".tmp"
-    cmd = [HIPCC, *FLAGS, "-I", os.path.join(ROOT, "include"),
-           "-I", os.path.join(PKG, "csrc"), "-o", out_tmp, *sources()]
-    if verbose:
-        print(" ".join(cmd), flush=True)
+def _compile(src: str, obj: str) -> tuple[int, str]:
+    cmd = [HIPCC, *FLAGS, "-c", "-I", os.path.join(ROOT, "include"),
+           "-I", os.path.join(PKG, "csrc"), "-o", obj, src]
     res = subprocess.run(cmd, capture_output=True, text=True)
-    errs = [ln for ln in res.stderr.splitlines()
-            if "packed-fp32-ops" not in ln and ln.strip()]
+    return res.returncode, res.stderr
+
+
+def build(verbose: bool = False, jobs: int | None = None) -> str:
+    """Compile every source (in parallel, one object each) and link
+    libpotattn.so (always recompiles)."""
+    from concurrent.futures import ThreadPoolExecutor
+    srcs = sources()
+    objdir = os.path.join(PKG, "_build")
+    os.makedirs(objdir, exist_ok=True)
+    objs = [os.path.join(objdir, os.path.basename(s) + ".o") for s in srcs]
+    jobs = jobs or max(1, min(len(srcs), os.cpu_count() or 1, 16))
+    with ThreadPoolExecutor(jobs) as ex:
+        results = list(ex.map(_compile, srcs, objs))
+    failed = False
+    for src, (rc, err) in zip(srcs, results):
+        errs = [ln for ln in err.splitlines() if "packed-fp32-ops" not in ln and ln.strip()]
+        if rc != 0:
+            failed = True
+            sys.stderr.write(f"--- {os.path.basename(src)}\n{err}")
+        elif verbose and errs:
+            sys.stderr.write("\n".join(errs) + "\n")
+    if failed:
+        raise RuntimeError("hipcc failed building libpotattn.so")
+    out_tmp = LIB + ".tmp"
+    link = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", out_tmp, *objs]
+    res = subprocess.run(link, capture_output=True, text=True)
     if res.returncode != 0:
         sys.stderr.write(res.stderr)
-        raise RuntimeError("hipcc failed building libpotattn.so")
-    if verbose and errs:
-        sys.stderr.write("\n".join(errs) + "\n")
+        raise RuntimeError("linking libpotattn.so failed")
     os.replace(out_tmp, LIB)
     return LIB
 

@@ -225,7 +225,7 @@ pot_status decode_common(int mode, int mant_bits, DecodeArgs& a, const int32_t* 
   if (force > 0) {
     p = plan_from_count(T, force);
   } else {
-    const int mbits = mode == kScorePot ? mant_bits : 0;
+    const int mbits = (mode == kScorePot || mode == kScoreDs4a) ? mant_bits : 0;
     const int S = split_count_for_slots((long)B * Hkv, device_slots(mode, G, mbits, vf));
     const int tiles = (T + kTile - 1) / kTile;
     const int s_short = split_count_short_ranges((long)B * Hkv, tiles);
@@ -566,6 +566,33 @@ pot_status pot_ds4a_decode_attention(const pot_format* fmt, const float* q,
   a.hadamard = fmt->hadamard;
   return decode_common(kScoreDs4a, 0, a, kv_head_of_q, B, Hq, Hkv, T, t_cap, workspace, ws_bytes,
                        dbg, stream);
+}
+
+pot_status pot_dot_decode_attention(const pot_format* fmt, const float* q,
+                                    const uint8_t* codes_se, const uint8_t* codes_m,
+                                    const float* key_scale, const uint16_t* v_cache,
+                                    int64_t t_cap, const int32_t* kv_head_of_q, int32_t B,
+                                    int32_t Hq, int32_t Hkv, int32_t T, float* out,
+                                    void* workspace, size_t ws_bytes, pot_debug* dbg,
+                                    void* stream) {
+  pot_status st = check_format(fmt);
+  if (st != POT_OK) return st;
+  if (!codes_se || !key_scale) return fail(POT_ERR_INVALID_ARG, "codes_se or key_scale is NULL");
+  if ((fmt->mant_bits > 0) != (codes_m != nullptr))
+    return fail(POT_ERR_INVALID_ARG, "codes_m must be non-NULL exactly when mant_bits > 0");
+  if (!aligned(codes_se, 16) || !aligned(key_scale, 4) || (codes_m && !aligned(codes_m, 8)))
+    return fail(POT_ERR_INVALID_ARG, "misaligned codes_se / key_scale / codes_m");
+  DecodeArgs a{};
+  a.q = q;
+  a.codes_se = codes_se;
+  a.codes_m = codes_m;
+  a.key_scale = key_scale;
+  a.v = v_cache;
+  a.out = out;
+  a.frac_bits = fmt->frac_bits;
+  a.hadamard = fmt->hadamard;
+  return decode_common(kScoreDs4a, fmt->mant_bits, a, kv_head_of_q, B, Hq, Hkv, T, t_cap,
+                       workspace, ws_bytes, dbg, stream);
 }
 
 pot_status pot_int8_encode_keys(const uint16_t* k_fp16, int64_t n_rows, int64_t out_row_stride,

@@ -23,7 +23,11 @@
 //     II-D) adds one sum per mantissa bit plane b over the same shifted
 //     operands, with weight sigma where bit b of the element's mantissa is
 //     set and 0 elsewhere; the key's sum is 2^k S_lead + sum_b 2^b S_b, the
-//     per-bit shifts of eq. sac regrouped by plane.
+//     per-bit shifts of eq. sac regrouped by plane. The decoded-code engines
+//     (a multiply path) instead decode each code once per key into dot-unit
+//     weights shared by all G heads: PoT-4 into int8 bytes sigma 2^(6 - e)
+//     for v_dot4_i32_i8, PoT-Mk into 16-bit sigma (2^k + j) 2^(7 - e) for
+//     v_dot2_i32_i16; the int32 sums equal the shift-accumulate ones.
 //  2. x = fl32(fl32(float(acc) * s) * c), c = fl32(fl32(Delta * log2 e) *
 //     2^-(F+k+3)) in this order; x is staged transposed in wave-private LDS.
 //  3. Integer running maximum M = max(M, ceil(max x)) per head (eq. logsm);
@@ -39,6 +43,11 @@
 // 2^(M_s - M) weights. (A last-workgroup merge inside this kernel would need
 // an agent-scope release/acquire per workgroup, which on a multi-XCD part
 // writes back and invalidates the XCD's L2 each time and serialises.)
+// (Kernel templates; the instantiations live in decode_pot*.hip,
+// decode_dot.hip and decode_cmp.hip, one translation unit per score mode and
+// value format.)
+#pragma once
+
 #include <hip/hip_fp16.h>
 
 #include <climits>
@@ -140,6 +149,7 @@ struct KeyRegs<kScorePot, K> {
 template <int K>
 struct KeyRegs<kScoreDs4a, K> {
   uint4 c0, c1;
+  uint2 pl[K > 0 ? K : 1];
   float s;
 };
 template <int K>
@@ -192,7 +202,7 @@ __device__ __forceinline__ void load_keys_buf(const Streams& st, int t0, int lan
   const u32x4v c1 = __builtin_amdgcn_raw_buffer_load_b128(rc, lane * 32 + 16, 0, kAuxNt);
   r.c0 = make_uint4(c0.x, c0.y, c0.z, c0.w);
   r.c1 = make_uint4(c1.x, c1.y, c1.z, c1.w);
-  if constexpr (MODE == kScorePot) {
+  if constexpr (MODE == kScorePot || MODE == kScoreDs4a) {
     if constexpr (K > 0) {
       const BufRsrc rp = tile_rsrc(st.planes, t0, st.t_end, 8 * K);
 #pragma unroll
@@ -277,13 +287,14 @@ __device__ __forceinline__ void mask_values(int t0, int t_end, int lane, ValRegs
 // ---- prepared query operands (workspace, one block per kv head) -------------
 // PoT-4 and PoT-Mk: [(c * 4 + n) * G + h] = q 2^7 of elements 8c + n and
 // 8c + n + 4 as signed 16-bit halves;
+// PoT-Mk decoded to weights: the same words with q itself;
 // INT8: [i * G + h] four int8 per word;
 // byte decode: [(2c + o) * G + h] four int8 (elements 8c + o + 2t, t = 0..3);
 // fp16: [i * G + h] two fp16 per word. The G per-head score factors follow.
 template <int MODE, int G, int K>
 struct QLayout {
   static constexpr int kCols = G;                              // one operand column per head
-  static constexpr int kWords = MODE == kScorePot ? 32 * kCols
+  static constexpr int kWords = (MODE == kScorePot || (MODE == kScoreDs4a && K > 0)) ? 32 * kCols
                                 : (MODE == kScoreInt8 || MODE == kScoreDs4a) ? (kDim / 4) * G
                                                      : (kDim / 2) * G;
 };
@@ -339,15 +350,17 @@ __device__ __forceinline__ void prepare_queries(const DecodeArgs& a, int kvh, in
       if (a.hadamard) qv = (float)(wave_fwht64((double)qv) * 0.125);
       float step;
       const int qi = wave_quantize_int8(qv, &step);
-      if constexpr (MODE == kScorePot) {
+      if constexpr (MODE == kScorePot || (MODE == kScoreDs4a && K > 0)) {
         // word ((c * 4 + n) * G + h) holds, for elements 8c + n (low half)
         // and 8c + n + 4 (high half), q 2^7 of head h: signed 16-bit
         // operands in [-16256, 16256] with 7 clear low bits, so an
-        // arithmetic right shift by e <= 7 is exact
+        // arithmetic right shift by e <= 7 is exact. The decoded-weight
+        // path takes q itself (its weights carry the 2^(7 - e)).
+        constexpr int kMul = MODE == kScorePot ? 128 : 1;
         const uint32_t up = (uint32_t)__shfl_down(qi, 4, 64);
         if ((lane & 4) == 0)
           qb[((lane >> 3) * 4 + (lane & 3)) * G + h] =
-              (int32_t)(((uint32_t)(qi * 128) & 0xFFFFu) | ((up * 128u) << 16));
+              (int32_t)(((uint32_t)(qi * kMul) & 0xFFFFu) | ((up * (uint32_t)kMul) << 16));
         if (lane == 0)
           cb[h] = __fmul_rn(__fmul_rn(step, log2e_f32()),
                             __builtin_amdgcn_ldexpf(1.0f, -(a.frac_bits + K + 3)));
@@ -502,7 +515,7 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
   // PoT scoring is long enough to cover the latency of value loads issued at
   // the start of the tile; the short INT8 / fp16 scoring is not, so those
   // prefetch the values of this wave's next tile as well.
-  constexpr bool kPrefetchV = MODE != kScorePot;
+  constexpr bool kPrefetchV = !(MODE == kScorePot || (MODE == kScoreDs4a && K > 0));
   ValRegs<V8> vr[kPrefetchV ? 2 : 1];
   if constexpr (kPrefetchV) {
     if (j < n_tiles) load_values_buf<V8>(st, t_begin + kWTile * j, lane, vr[0]);
@@ -630,6 +643,86 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
 #pragma unroll
           for (int bb = 0; bb < K; ++bb) t += (uint32_t)accm[bb][h] << bb;
           accv[h] = (int32_t)t;
+        }
+      }
+      if (a.frac_bits != kFInt) {  // uniform: rescale to head-room F exactly
+#pragma unroll
+        for (int h = 0; h < G; ++h)
+          accv[h] = a.frac_bits > kFInt
+                        ? (int32_t)((uint32_t)accv[h] << (a.frac_bits - kFInt))
+                        : (accv[h] >> (kFInt - a.frac_bits));
+      }
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        const int32_t v = accv[h];
+        xs[h] = __fmul_rn(__fmul_rn((float)v, ks.s), cb[h]);
+        if constexpr (DEBUG) {
+          if (a.dbg_scores && kvalid)
+            a.dbg_scores[((int64_t)b * a.Hq + a.q_of_kv[kvh * G + h]) * a.T + t] = v;
+        }
+      }
+    } else if constexpr (MODE == kScoreDs4a && K > 0) {
+      // PoT-Mk codes decoded to 16-bit integer weights (a multiply path):
+      // element m's weight is sigma (2^k + j) 2^(7 - e), 0 for the zero code,
+      // at most 31 * 128 in magnitude; v_dot2_i32_i16 accumulates q^ times
+      // the weights of two elements per head. The sum is exactly 2^k times
+      // the key's sum of eq. sac at head-room 7 (eq. mant), the integer the
+      // shift-accumulate path forms from its planes, with one dot per head
+      // and element pair for any k.
+      const uint32_t w[8] = {ks.c0.x, ks.c0.y, ks.c0.z, ks.c0.w,
+                             ks.c1.x, ks.c1.y, ks.c1.z, ks.c1.w};
+      int32_t accv[G];
+      // the mantissas regrouped per element pair n: byte i of jw[n][hw]
+      // holds j of element 8(4 hw + i) + n in bits 0..3 and of element
+      // 8(4 hw + i) + n + 4 in bits 4..7 (bit m of plane byte i is bit b of
+      // the mantissa of element 8i + m)
+      uint32_t jw[4][2];
+#pragma unroll
+      for (int n = 0; n < 4; ++n)
+#pragma unroll
+        for (int hw = 0; hw < 2; ++hw) {
+          uint32_t jacc = 0;
+#pragma unroll
+          for (int bb = 0; bb < K; ++bb) {
+            const uint32_t pw = hw ? ks.pl[bb].y : ks.pl[bb].x;
+            const uint32_t t = (bb <= n) ? (pw >> (n - bb)) : (pw << (bb - n));
+            jacc |= t & (0x11111111u << bb);
+          }
+          jw[n][hw] = jacc;
+        }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const uint32_t wi = w[i];
+        const uint32_t x = wi & 0x77777777u;
+        const uint32_t y = x + 0x11111111u;
+        // per nibble, bit 3: the sign; bit 2: "not the zero code" (as in
+        // the shift-accumulate path); ~wi holds 7 - e in each nibble's low
+        // three bits
+        const uint32_t sw = (wi & 0x88888888u) | (~(y >> 1) & 0x44444444u);
+        const uint32_t nx = ~wi;
+        int toff = 0;
+        asm("" : "+s"(toff) : "s"(jt));
+        uint32_t qq[4 * kCols];
+#pragma unroll
+        for (int k = 0; k < 4 * kCols; ++k) qq[k] = (uint32_t)qb[toff + 4 * kCols * i + k];
+#pragma unroll
+        for (int n = 0; n < 4; ++n) {
+          // weights sigma 2^(7 - e) (0 for the zero code) of elements 8i + n
+          // and 8i + n + 4, then times 2^k + j
+          const s16x2 sg = __builtin_bit_cast(s16x2, sw << (12 - 4 * n)) >> (short)14;
+          const s16x2 sh7 = __builtin_bit_cast(s16x2, (nx >> (4 * n)) & 0x00070007u);
+          const u16x2 sgs = __builtin_bit_cast(u16x2, (s16x2)(sg << sh7));
+          const uint32_t jb = __builtin_amdgcn_perm(jw[n][i >> 2], jw[n][i >> 2],
+                                                    (uint32_t)(i & 3) * 0x00010001u | 0x0C000C00u);
+          const u16x2 j4 = __builtin_bit_cast(u16x2, jb) >> u16x2{0, 4};
+          const u16x2 jn = (j4 & u16x2{15, 15}) | u16x2{1 << K, 1 << K};
+          const s16x2 wt = __builtin_bit_cast(s16x2, (u16x2)(jn * sgs));
+#pragma unroll
+          for (int h = 0; h < G; ++h) {
+            const s16x2 qv = __builtin_bit_cast(s16x2, qq[kCols * n + h]);
+            accv[h] = (i == 0 && n == 0) ? __builtin_amdgcn_sdot2(qv, wt, 0, true)
+                                         : __builtin_amdgcn_sdot2(qv, wt, accv[h], false);
+          }
         }
       }
       if (a.frac_bits != kFInt) {  // uniform: rescale to head-room F exactly
@@ -1076,43 +1169,10 @@ static int occupancy_t() {
   return n;
 }
 
-template <int VF>
-static int occupancy_v(int mode, int G, int mant_bits) {
-  auto by_k = [&](auto g_tag) -> int {
-    constexpr int GG = decltype(g_tag)::value;
-    if (mode == kScoreDs4a) return occupancy_t<kScoreDs4a, GG, 0, VF>();
-    if constexpr (VF == 0) {
-      if (mode == kScoreInt8) return occupancy_t<kScoreInt8, GG, 0, 0>();
-      if (mode == kScoreFp16) return occupancy_t<kScoreFp16, GG, 0, 0>();
-    }
-    switch (mant_bits) {
-      case 0: return occupancy_t<kScorePot, GG, 0, VF>();
-      case 1: return occupancy_t<kScorePot, GG, 1, VF>();
-      case 2: return occupancy_t<kScorePot, GG, 2, VF>();
-      case 3: return occupancy_t<kScorePot, GG, 3, VF>();
-      default: return occupancy_t<kScorePot, GG, 4, VF>();
-    }
-  };
-  switch (G) {
-    case 1: return by_k(std::integral_constant<int, 1>{});
-    case 2: return by_k(std::integral_constant<int, 2>{});
-    case 4: return by_k(std::integral_constant<int, 4>{});
-    default: return by_k(std::integral_constant<int, 8>{});
-  }
-}
-
-int decode_occupancy(int mode, int G, int mant_bits, int vf) {
-  switch (vf) {
-    case 1: return occupancy_v<1>(mode, G, mant_bits);
-    case 2: return occupancy_v<2>(mode, G, mant_bits);
-    default: return occupancy_v<0>(mode, G, mant_bits);
-  }
-}
-
 template <int MODE, int G, bool DEBUG, int VF>
 static hipError_t launch_k(int mant_bits, const DecodeArgs& a, hipStream_t stream, hipEvent_t e0,
                            hipEvent_t e1) {
-  if constexpr (MODE != kScorePot) {
+  if constexpr (!(MODE == kScorePot || (MODE == kScoreDs4a && VF == 0))) {
     return launch_t<MODE, G, 0, DEBUG, VF>(a, stream, e0, e1);
   } else {
     switch (mant_bits) {
@@ -1138,37 +1198,40 @@ static hipError_t launch_g(int G, int mant_bits, const DecodeArgs& a, hipStream_
   }
 }
 
-template <int VF>
-static hipError_t launch_v(int mode, int G, int mant_bits, bool debug, const DecodeArgs& a,
-                           hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
-  switch (mode) {
-    case kScorePot:
-      return debug ? launch_g<kScorePot, true, VF>(G, mant_bits, a, stream, e0, e1)
-                   : launch_g<kScorePot, false, VF>(G, mant_bits, a, stream, e0, e1);
-    case kScoreDs4a:
-      return debug ? launch_g<kScoreDs4a, true, VF>(G, 0, a, stream, e0, e1)
-                   : launch_g<kScoreDs4a, false, VF>(G, 0, a, stream, e0, e1);
-    case kScoreInt8:
-      if constexpr (VF != 0) return hipErrorInvalidValue;
-      else
-        return debug ? launch_g<kScoreInt8, true, 0>(G, 0, a, stream, e0, e1)
-                     : launch_g<kScoreInt8, false, 0>(G, 0, a, stream, e0, e1);
-    case kScoreFp16:
-      if constexpr (VF != 0) return hipErrorInvalidValue;
-      else return launch_g<kScoreFp16, false, 0>(G, 0, a, stream, e0, e1);
-    default:
-      return hipErrorInvalidValue;
-  }
+// One score mode and value format: every head-group size and mantissa width
+// the mode supports (the instantiations live in one translation unit per
+// mode / format, declared in pot_launch.hpp).
+template <int MODE, int VF>
+hipError_t launch_mode_vf(int G, int mant_bits, bool debug, const DecodeArgs& a,
+                          hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
+  if constexpr (MODE == kScoreFp16)
+    return launch_g<MODE, false, VF>(G, mant_bits, a, stream, e0, e1);
+  else
+    return debug ? launch_g<MODE, true, VF>(G, mant_bits, a, stream, e0, e1)
+                 : launch_g<MODE, false, VF>(G, mant_bits, a, stream, e0, e1);
 }
 
-hipError_t launch_decode(int mode, int G, int mant_bits, bool debug, int vf,
-                         const DecodeArgs& a, hipStream_t stream, hipEvent_t ev_begin,
-                         hipEvent_t ev_end) {
-  switch (vf) {
-    case 0: return launch_v<0>(mode, G, mant_bits, debug, a, stream, ev_begin, ev_end);
-    case 1: return launch_v<1>(mode, G, mant_bits, debug, a, stream, ev_begin, ev_end);
-    case 2: return launch_v<2>(mode, G, mant_bits, debug, a, stream, ev_begin, ev_end);
-    default: return hipErrorInvalidValue;
+template <int MODE, int VF>
+int occupancy_mode_vf(int G, int mant_bits) {
+  auto by_k = [&](auto g_tag) -> int {
+    constexpr int GG = decltype(g_tag)::value;
+    if constexpr (MODE == kScorePot || (MODE == kScoreDs4a && VF == 0)) {
+      switch (mant_bits) {
+        case 0: return occupancy_t<MODE, GG, 0, VF>();
+        case 1: return occupancy_t<MODE, GG, 1, VF>();
+        case 2: return occupancy_t<MODE, GG, 2, VF>();
+        case 3: return occupancy_t<MODE, GG, 3, VF>();
+        default: return occupancy_t<MODE, GG, 4, VF>();
+      }
+    } else {
+      return occupancy_t<MODE, GG, 0, VF>();
+    }
+  };
+  switch (G) {
+    case 1: return by_k(std::integral_constant<int, 1>{});
+    case 2: return by_k(std::integral_constant<int, 2>{});
+    case 4: return by_k(std::integral_constant<int, 4>{});
+    default: return by_k(std::integral_constant<int, 8>{});
   }
 }
 

@@ -1,0 +1,10 @@
+// Decode kernels: shift-accumulate scores, INT8 values (softmax weights).
+#include "decode_kernel.hpp"
+
+namespace potattn {
+
+template hipError_t launch_mode_vf<kScorePot, 1>(int, int, bool, const DecodeArgs&, hipStream_t,
+                                                 hipEvent_t, hipEvent_t);
+template int occupancy_mode_vf<kScorePot, 1>(int, int);
+
+}  // namespace potattn

@@ -122,4 +122,12 @@ hipError_t launch_decode(int mode, int G, int mant_bits, bool debug, int vf,
                          const DecodeArgs& a, hipStream_t stream, hipEvent_t ev_begin = nullptr,
                          hipEvent_t ev_end = nullptr);
 
+// The launch and occupancy query of one score mode and value format; each
+// mode's kernels are instantiated in a translation unit of their own.
+template <int MODE, int VF>
+hipError_t launch_mode_vf(int G, int mant_bits, bool debug, const DecodeArgs& a,
+                          hipStream_t stream, hipEvent_t e0, hipEvent_t e1);
+template <int MODE, int VF>
+int occupancy_mode_vf(int G, int mant_bits);
+
 }  // namespace potattn

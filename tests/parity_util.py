@@ -51,8 +51,9 @@ def gpu_pot_decode(d, codes_se, codes_m, key_scale, mant_bits=0, frac_bits=7,
                    hadamard=False, taps=True, force_splits=0, engine="sac"):
     """d: workloads.make_decode_inputs dict; cache arrays are host numpy in the
     row layout. engine "sac" runs pot_decode_attention (shift-accumulate),
-    "ds4a" pot_ds4a_decode_attention (byte decode + v_dot4). Returns dict of
-    numpy results (taps when requested)."""
+    "ds4a" pot_ds4a_decode_attention (byte decode + v_dot4), "dot"
+    pot_dot_decode_attention (codes decoded to dot-unit weights, any k).
+    Returns dict of numpy results (taps when requested)."""
     B, Hq, Hkv, T, t_cap = d["B"], d["Hq"], d["Hkv"], d["T"], d["t_cap"]
     fmt = pa.make_format(mant_bits, frac_bits, hadamard)
     q = to_dev(d["q"])
@@ -80,6 +81,9 @@ def gpu_pot_decode(d, codes_se, codes_m, key_scale, mant_bits=0, frac_bits=7,
     if engine == "sac":
         pa.pot_decode_attention(fmt, q, se, cm, sc, v, t_cap, d["kv_head_of_q"], B,
                                 Hq, Hkv, T, out, ws, dbg=dbg)
+    elif engine == "dot":
+        pa.pot_dot_decode_attention(fmt, q, se, cm, sc, v, t_cap, d["kv_head_of_q"], B,
+                                    Hq, Hkv, T, out, ws, dbg=dbg)
     else:
         assert engine == "ds4a" and cm is None
         pa.pot_ds4a_decode_attention(fmt, q, se, sc, v, t_cap, d["kv_head_of_q"], B,

@@ -13,7 +13,7 @@ stream, and checks at ragged T = t_cap (the tightest legal cache) that:
 * every performed access lies inside the sequence's rows [0, t_cap);
 * a multi-byte load is either wholly in range or wholly out;
 * every key below the range's end is read (none is dropped by the window).
-The formulas mirror those of decode.hip (load_keys_buf, load_values_buf).
+The formulas mirror those of decode_kernel.hpp (load_keys_buf, load_values_buf).
 """
 import pytest
 

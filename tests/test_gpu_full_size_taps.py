@@ -3,7 +3,8 @@
 B = 64, T = 32768, PoT-4 (the headline shape) and B = 8, T = 32768 with
 Hadamard + PoT-M4: the planner's key splits, through both decode entry points
 (pot_decode_attention and the benchmark's pot_append_decode_attention, which
-appends the token at T - 1 first). Each call runs twice on the same inputs:
+appends the token at T - 1 first); the decoded-weight entry point
+pot_dot_decode_attention at Hadamard + PoT-M4 (B = 8) and PoT-M1 (B = 64). Each call runs twice on the same inputs:
 plain (the timed kernel) and with the score taps on (the instrumented build
 of the same kernel source, same split plan). Checked:
 * the two outputs are bit-identical;
@@ -27,11 +28,16 @@ HQ, HKV = 32, 4
 G = HQ // HKV
 
 
-def _run(fmt, d, cache, v, append, dbg):
+def _run(fmt, d, cache, v, append, dbg, engine="sac"):
     B, T = d["B"], d["T"]
     out = torch.empty((B, HQ, 64), dtype=torch.float32, device=DEV)
     ws = pa.alloc_workspace(pa.pot_decode_workspace_bytes(B, HQ, HKV, T), DEV)
-    if append:
+    if engine == "dot":
+        assert not append
+        pa.pot_dot_decode_attention(fmt, d["q"], cache["codes_se"], cache["codes_m"],
+                                    cache["key_scale"], v, T, d["kv_head_of_q"], B, HQ, HKV,
+                                    T, out, ws, dbg=dbg)
+    elif append:
         pa.pot_append_decode_attention(fmt, d["q"], d["k_new"], d["v_new"], cache["codes_se"],
                                        cache["codes_m"], cache["key_scale"], v, T,
                                        d["kv_head_of_q"], B, HQ, HKV, T, out, ws, dbg=dbg)
@@ -42,9 +48,9 @@ def _run(fmt, d, cache, v, append, dbg):
     return out
 
 
-def _check(B, T, mant_bits, hadamard, append, samples, seed):
-    print(f"full-size taps B={B} T={T} k={mant_bits} had={hadamard} append={append}",
-          flush=True)
+def _check(B, T, mant_bits, hadamard, append, samples, seed, engine="sac"):
+    print(f"full-size taps B={B} T={T} k={mant_bits} had={hadamard} append={append} "
+          f"engine={engine}", flush=True)
     d = make_decode_inputs_device(seed, B, HQ, HKV, T, DEV)
     fmt = pa.make_format(mant_bits, 7, hadamard)
     rows = B * HKV * T
@@ -71,7 +77,7 @@ def _check(B, T, mant_bits, hadamard, append, samples, seed):
     # the plain call, as timed; the planner's split length comes back in dbg
     cache, v = fresh_cache()
     plan = pa.pot_debug()
-    out_plain = _run(fmt, d, cache, v, append, plan)
+    out_plain = _run(fmt, d, cache, v, append, plan, engine)
     torch.cuda.synchronize()
     n_splits, split_len = plan.n_splits, plan.split_len
     del cache, v
@@ -85,7 +91,7 @@ def _check(B, T, mant_bits, hadamard, append, samples, seed):
     dbg = pa.pot_debug()
     for name, t in taps.items():
         setattr(dbg, name, t.data_ptr())
-    out_taps = _run(fmt, d, cache, v, append, dbg)
+    out_taps = _run(fmt, d, cache, v, append, dbg, engine)
     torch.cuda.synchronize()
     assert (dbg.n_splits, dbg.split_len) == (n_splits, split_len)
     assert torch.equal(out_plain.view(torch.int32), out_taps.view(torch.int32)), \
@@ -131,3 +137,12 @@ def test_full_size_b64_t32768_pot4_taps(append):
 @pytest.mark.parametrize("append", [False, True])
 def test_full_size_b8_t32768_hadamard_potm4_taps(append):
     _check(8, 32768, 4, True, append, [(0, 2), (7, 3)], 50 + append)
+
+
+# the decoded-weight engine (pot_dot_decode_attention) at the PoT-Mk shapes
+def test_full_size_b8_t32768_hadamard_potm4_dot_taps():
+    _check(8, 32768, 4, True, False, [(1, 0), (6, 3)], 52, engine="dot")
+
+
+def test_full_size_b64_t32768_potm1_dot_taps():
+    _check(64, 32768, 1, False, False, [(0, 1), (40, 2), (63, 0)], 53, engine="dot")
