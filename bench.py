@@ -54,6 +54,12 @@ LLC_BYTES = 256 << 20  # last-level (MALL) cache
 COMPARE_ROUNDS = 3  # interleaved timing rounds per comparator engine
 PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "decode_pot4_b64_t32768_traffic.txt")
 PROFILE_READ_CEILING = os.path.join(ROOT, "profiles", "stream_read_ceiling.md")
+PROFILE_VALU = os.path.join(ROOT, "profiles", "decode_valu_counters.txt")
+# wave64 VALU instructions per ns per CU that shifts, v_perm, v_dot2 / v_dot4,
+# packed 16-bit ops and SGPR-operand forms issue at (profiles/valu_issue_rates.md):
+# the issue term of the roofline for the score cores
+ISSUE_RATE = 2.2
+N_CU = 256
 CSRC = os.path.join(ROOT, "paper_2609_09208_amd", "csrc")
 METRIC = "decode-attention keys scored/s and achieved HBM GB/s at T=32k (PoT-4)"
 
@@ -81,22 +87,57 @@ def source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def read_traffic():
-    """HBM bytes per launch measured with rocprofv3 counters, if they were
+def read_profile(path):
+    """key: value lines of a committed counter summary, if its counters were
     taken on the current kernel sources; otherwise None."""
-    if not os.path.exists(PROFILE_TRAFFIC):
+    if not os.path.exists(path):
         return None
     vals = {}
-    for line in open(PROFILE_TRAFFIC):
+    for line in open(path):
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             vals[k.strip()] = v.strip()
     if vals.get("source_digest") != source_digest():
         return None
+    return vals
+
+
+def read_traffic():
+    """HBM bytes per launch measured with rocprofv3 counters, if they were
+    taken on the current kernel sources; otherwise None."""
+    vals = read_profile(PROFILE_TRAFFIC)
+    if vals is None:
+        return None
     try:
         return float(vals["hbm_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
+
+
+def lane_ops_per_key(engine: str, mant_bits: int):
+    """VALU lane-ops per cache row of a decode kernel (SQ_INSTS_VALU * 64 /
+    rows, rocprofv3 counters on the current sources), or None."""
+    vals = read_profile(PROFILE_VALU)
+    try:
+        return float(vals[f"lane_ops_per_key.{engine}.k{mant_bits}"]) if vals else None
+    except (KeyError, ValueError):
+        return None
+
+
+def issue_term(lane_ops, rows: int, us: float):
+    """The VALU issue term of the roofline (Sec. III, eq. roofline) for one
+    launch: wave64 instructions / (ISSUE_RATE * N_CU) against the measured
+    kernel time."""
+    if lane_ops is None:
+        return None
+    wave_instr = lane_ops * rows / 64.0
+    floor_us = wave_instr / (ISSUE_RATE * N_CU) / 1e3
+    return {"lane_ops_per_key": lane_ops, "wave_instr_per_launch": wave_instr,
+            "issue_floor_us": floor_us, "achieved_rate": wave_instr / (us * 1e3) / N_CU,
+            "peak_rate": ISSUE_RATE, "rate_unit": "wave64 VALU instr/ns/CU",
+            "frac": floor_us / us,
+            "source": "SQ_INSTS_VALU from profiles/decode_valu_counters.txt; issue rate of "
+                      "the shift / dot / SGPR-operand class from profiles/valu_issue_rates.md"}
 
 
 def read_ceiling():
@@ -449,6 +490,10 @@ def comparators(pa, lay, dev):
     engines["pot_v8_pow2"] = lambda i: pa.pot_decode_attention_v8_pow2(
         lay.fmt, 0, cl[i]["q"], cl[i]["codes_se"], cl[i]["codes_m"], cl[i]["key_scale"],
         v8[i][0], v8[i][1], T, heads, B, HQ, HKV, T, out, ws)
+    if lay.k > 0:  # PoT-Mk decoded to 16-bit weights + v_dot2 (a multiply path)
+        engines["dot"] = lambda i: pa.pot_dot_decode_attention(
+            lay.fmt, cl[i]["q"], cl[i]["codes_se"], cl[i]["codes_m"], cl[i]["key_scale"],
+            cl[i]["v"], T, heads, B, HQ, HKV, T, out, ws)
     if lay.k == 0:  # byte decode + v_dot4 on the same PoT-4 caches (a multiply path)
         engines["ds4a"] = lambda i: pa.pot_ds4a_decode_attention(
             lay.fmt, cl[i]["q"], cl[i]["codes_se"], cl[i]["key_scale"], cl[i]["v"], T, heads,
@@ -464,6 +509,7 @@ def comparators(pa, lay, dev):
     med = {name: float(sorted(v)[len(v) // 2]) for name, v in runs.items()}
     pot_us, f16_us, i8_us, ds4a_us = med["pot"], med["fp16"], med["int8"], med.get("ds4a")
     pv8_us, dv8_us, pw_us = med["pot_v8"], med.get("ds4a_v8"), med["pot_v8_pow2"]
+    dot_us = med.get("dot")
 
     def frac(per_row, us):
         return algorithmic_bytes(B, T, per_row) / (us * 1e-6) / 1e9 / HBM_PEAK_GBS
@@ -477,6 +523,12 @@ def comparators(pa, lay, dev):
             "ds4a_speedup_vs_fp16": f16_us / ds4a_us if ds4a_us else None,
             "ds4a_note": "PoT-4 codes decoded to int8 bytes by v_perm and scored by v_dot4 "
                          "(software packed shift-dot, a multiply path)",
+            "dot_us_per_layer": dot_us,
+            "dot_hbm_frac": frac(row_bytes(lay.k), dot_us) if dot_us else None,
+            "dot_speedup_vs_fp16": f16_us / dot_us if dot_us else None,
+            "dot_speedup_vs_sac": pot_us / dot_us if dot_us else None,
+            "dot_note": "PoT-Mk codes decoded to 16-bit weights sigma (2^k + j) 2^(7-e) and "
+                        "scored by v_dot2 (pot_dot_decode_attention, a multiply path)",
             "int8_values": {
                 "bytes_per_row": row_bytes_v8(lay.k),
                 "pot_us_per_layer": pv8_us,
@@ -497,9 +549,10 @@ def fmt_name(k: int, had: bool) -> str:
     return ("Hadamard + " if had else "") + ("PoT-4" if k == 0 else f"PoT-M{k}")
 
 
-def sweep(pa, dev, steps, warmup, only=None, layers=None):
+def sweep(pa, dev, steps, warmup, only=None, layers=None, compare_only=False):
     """only: keep the points whose (B, T, k) is in this set; layers: layer
-    count override (the counter runs profile one point per process)."""
+    count override (the counter runs profile one point per process);
+    compare_only: only the configurations timed with the comparators."""
     import numpy as np
     import torch
     pts = []
@@ -507,17 +560,21 @@ def sweep(pa, dev, steps, warmup, only=None, layers=None):
         for T in (1024, 4096, 16384, 32768):
             for k in (0, 4):
                 pts.append(dict(B=B, T=T, k=k, had=False, L=22, compare=False))
-    pts += [dict(B=1, T=4096, k=0, had=False, L=4, compare=True),
-            dict(B=1, T=32768, k=1, had=False, L=4, compare=True),
-            dict(B=8, T=32768, k=4, had=True, L=4, compare=True),
-            dict(B=8, T=32768, k=0, had=False, L=4, compare=True)]
+    # the single-layer configurations with the comparators, over 22 layers
+    # that all keep their fp16 keys (every engine streams the same layers)
+    pts += [dict(B=1, T=4096, k=0, had=False, L=22, compare=True),
+            dict(B=1, T=32768, k=1, had=False, L=22, compare=True),
+            dict(B=8, T=32768, k=4, had=True, L=22, compare=True),
+            dict(B=8, T=32768, k=0, had=False, L=22, compare=True)]
     if only is not None:
         pts = [p for p in pts if (p["B"], p["T"], p["k"]) in only and not p["compare"]]
+    if compare_only:
+        pts = [p for p in pts if p["compare"]]
     for p in pts:
         if layers is not None:
             p["L"] = layers
         lay = Layers(pa, p["B"], p["T"], p["L"], p["k"], p["had"], dev, distinct=False,
-                     keep_k16=4 if p["compare"] else 0)
+                     keep_k16=p["L"] if p["compare"] else 0)
         elapsed, us = time_steps(lay, steps, warmup)
         graph_ms = time_graph(lay, steps, warmup)
         alg = algorithmic_bytes(p["B"], p["T"], row_bytes(p["k"]))
@@ -551,6 +608,8 @@ def main() -> int:
                     help="one JSON line per workload point instead of the headline line")
     ap.add_argument("--sweep-point", action="append", default=None, metavar="B,T,k",
                     help="with --sweep: run only this 22-layer point (repeatable)")
+    ap.add_argument("--sweep-compare", action="store_true",
+                    help="with --sweep: only the configurations timed with the comparators")
     ap.add_argument("--sweep-layers", type=int, default=None,
                     help="with --sweep: layers per point instead of 22")
     ap.add_argument("--cpu-configs", action="store_true",
@@ -591,7 +650,7 @@ def main() -> int:
         if args.sweep_point:
             only = {tuple(int(v) for v in sp.split(",")) for sp in args.sweep_point}
         sweep(pa, dev, max(2, min(args.steps, 5)), max(1, min(args.warmup, 2)), only,
-              args.sweep_layers)
+              args.sweep_layers, args.sweep_compare)
         return 0
 
     B, T, L, k = args.batch, args.seq, args.layers, args.mant_bits
@@ -607,6 +666,35 @@ def main() -> int:
     alg = algorithmic_bytes(B, T, row_bytes(k))
     achieved = alg / kern_s / 1e9
 
+    roofline = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                "traffic": read_traffic() if (B, T, k) == (64, 32768, 0) else None,
+                "kernel": f"potattn::decode_kernel<0, 8, {k}, false, 0> (SAC, G = 8, fp16 V: "
+                          "products by packed 16-bit shifts, signs and int32 sums by "
+                          "v_dot2_i32_i16 with weights -1/0/+1"
+                          + (", one sum per mantissa bit plane" if k else "") + ")",
+                "note": "score cores built from shifts and adds alone (v_lshl_add_u32, "
+                        "SDWA shift + v_xad_u32) measured 0.57-0.60 of 8 TB/s in this "
+                        "kernel; the v_dot2 accumulate is the one timed here",
+                "alg_bytes_per_launch": alg, "launch_us": kern_s * 1e6,
+                "launch_us_median": float(np.median(kus)), "launch_us_best": float(kus.min()),
+                "launches_timed": int(kus.size),
+                "call_us": call_s * 1e6, "call_us_median": float(np.median(us)),
+                "frac_call": alg / call_s / 1e9 / HBM_PEAK_GBS,
+                "read_ceiling_gbs": read_ceiling(),
+                "frac_of_read_ceiling": achieved / read_ceiling() if read_ceiling() else None,
+                "keys_scored_per_s_kernel": B * HQ * T / kern_s,
+                "keys_scored_per_s_call": B * HQ * T / call_s}
+    issue = issue_term(lane_ops_per_key("sac", k), B * HKV * T, kern_s * 1e6)
+    roofline["issue"] = issue
+    if k > 0 and issue is not None:
+        # PoT-Mk's shift-accumulate core is bound by VALU issue (eq. roofline's
+        # second term): the headline fraction is the issue one, HBM beside it
+        hbm = {key: roofline.pop(key) for key in ("achieved", "peak", "unit", "frac", "traffic")}
+        roofline.pop("bound")
+        roofline = {"bound": "valu", "achieved": issue["achieved_rate"], "peak": ISSUE_RATE,
+                    "unit": issue["rate_unit"], "frac": issue["frac"], "traffic": None,
+                    "hbm": hbm, **roofline}
     result = {
         "metric": METRIC,
         "value": B * HQ * T * L * args.steps / elapsed, "unit": "keys/s", "n_gpus": 1,
@@ -618,24 +706,7 @@ def main() -> int:
                                f"fp16 V, B={B}, T={T}, Hq={HQ}, Hkv={HKV}, d={D}",
                    "B": B, "T": T, "layers": L, "Hq": HQ, "Hkv": HKV, "head_dim": D,
                    "mant_bits": k, "frac_bits": 7, "parallelism": "none (1 GPU)"},
-        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": read_traffic() if (B, T, k) == (64, 32768, 0) else None,
-                     "kernel": f"potattn::decode_kernel<0, 8, {k}, false, 0> (SAC, G = 8, fp16 V: "
-                               "products by packed 16-bit shifts, signs and int32 sums by "
-                               "v_dot2_i32_i16 with weights -1/0/+1)",
-                     "note": "score cores built from shifts and adds alone (v_lshl_add_u32, "
-                             "SDWA shift + v_xad_u32) measured 0.57-0.60 of 8 TB/s in this "
-                             "kernel; the v_dot2 accumulate is the one timed here",
-                     "alg_bytes_per_launch": alg, "launch_us": kern_s * 1e6,
-                     "launch_us_median": float(np.median(kus)), "launch_us_best": float(kus.min()),
-                     "launches_timed": int(kus.size),
-                     "call_us": call_s * 1e6, "call_us_median": float(np.median(us)),
-                     "frac_call": alg / call_s / 1e9 / HBM_PEAK_GBS,
-                     "read_ceiling_gbs": read_ceiling(),
-                     "frac_of_read_ceiling": achieved / read_ceiling() if read_ceiling() else None,
-                     "keys_scored_per_s_kernel": B * HQ * T / kern_s,
-                     "keys_scored_per_s_call": B * HQ * T / call_s},
+        "roofline": roofline,
         "timing": {"value": f"{args.steps} steps after {args.warmup} warm-up steps, no events "
                             "in the timed region",
                    "roofline": f"{args.steps} further steps with HIP events around every "
