@@ -338,9 +338,11 @@ pot_status pot_append_decode_attention_v8(const pot_format* fmt, int32_t engine,
  * Errors: as pot_decode_attention; a shape whose workspace bound
  * (pot_decode_workspace_bytes, or pot_decode_workspace_bytes_for_splits with
  * dbg->force_splits) exceeds POT_NOALLOC_SCRATCH_BYTES -> POT_ERR_WORKSPACE,
- * checked on the host before any HIP call. At the TinyLlama shape (Hq = 32,
- * Hkv = 4) that bound is about 2.5 MB at B = 64 and grows by 264 bytes per
- * query head and key split.
+ * checked on the host before any HIP call. The bound covers the largest split
+ * count the planner may choose: 264 bytes per query head and key split (the
+ * split partials) plus one prepared-query slot per kv head and key split
+ * (1280 bytes at G = 8). At the TinyLlama shape (Hq = 32, Hkv = 4) it is
+ * about 7 MB for B >= 8 and 1.7 MB at B = 1.
  * Every call on one GPU shares that GPU's scratch, which keeps the previous
  * call's contents (the kernels write every word they read, so nothing needs
  * clearing): calls that overlap in time on one GPU race and must not be made. */
