@@ -317,30 +317,46 @@ __device__ __forceinline__ void append_token(const DecodeArgs& a, int64_t seq, i
     store_value_token_wave(a.app_v + seq * kDim, a.app_v_cache + seq * a.t_cap * kDim, a.T - 1);
 }
 
+// The query elements of the heads this wave prepares (wave w: heads w,
+// w + 4), one per lane; loaded first thing so that their latency overlaps
+// the rest of the prologue.
+template <int G>
+struct QueryIn {
+  static constexpr int kHeadsPerWave = (G + kWaves - 1) / kWaves;
+  float v[kHeadsPerWave];
+};
+template <int G>
+__device__ __forceinline__ QueryIn<G> load_queries(const DecodeArgs& a, int kvh, int b) {
+  const int lane = lane_id(), wave = threadIdx.x >> 6;
+  QueryIn<G> qin;
+#pragma unroll
+  for (int i = 0; i < QueryIn<G>::kHeadsPerWave; ++i) {
+    const int h = wave + kWaves * i;
+    qin.v[i] = h < G ? a.q[((int64_t)b * a.Hq + a.q_of_kv[kvh * G + h]) * kDim + lane] : 0.0f;
+  }
+  return qin;
+}
+
 // Rotates (optionally) and quantises the G query vectors of one (batch, kv
 // head) and writes the operand words and per-head score factors that the
 // score loop reads through the scalar cache, into qb (this workgroup's own
 // slot of the workspace). Called by all four waves of the workgroup; wave w
-// handles heads w, w + 4. taps: also write the q^ and Delta debug taps.
+// handles heads w, w + 4, whose elements qin holds. taps: also write the q^
+// and Delta debug taps.
 template <int MODE, int G, int K>
 __device__ __forceinline__ void prepare_queries(const DecodeArgs& a, int kvh, int b,
-                                                int32_t* __restrict__ qb, bool taps) {
+                                                int32_t* __restrict__ qb, bool taps,
+                                                const QueryIn<G>& qin) {
   using QL = QLayout<MODE, G, K>;
   const int lane = lane_id(), wave = threadIdx.x >> 6;
   float* cb = reinterpret_cast<float*>(qb + QL::kWords);
-  constexpr int kHeadsPerWave = (G + kWaves - 1) / kWaves;
-  float qin[kHeadsPerWave];
-#pragma unroll
-  for (int i = 0; i < kHeadsPerWave; ++i) {
-    const int h = wave + kWaves * i;
-    qin[i] = h < G ? a.q[((int64_t)b * a.Hq + a.q_of_kv[kvh * G + h]) * kDim + lane] : 0.0f;
-  }
+  constexpr int kHeadsPerWave = QueryIn<G>::kHeadsPerWave;
 #pragma unroll
   for (int i = 0; i < kHeadsPerWave; ++i) {
     const int h = wave + kWaves * i;
     if (h >= G) break;
     const int64_t bq = (int64_t)b * a.Hq + a.q_of_kv[kvh * G + h];
-    float qv = qin[i];
+    float qv = qin.v[i];
     if constexpr (MODE == kScoreFp16) {
       const uint32_t bits = __half_as_ushort(__float2half_rn(qv));
       const uint32_t other = __shfl_xor(bits, 1, 64);
@@ -435,9 +451,10 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
   const int row = lane & 15, grp = lane >> 4, hrow = row & 7, part = row >> 3;
   const bool hvalid = hrow < G;
 
+  const QueryIn<G> qin = load_queries<G>(a, kvh, b);
   // The sequence's new token (fused append) is written before any of this
-  // workgroup's loads: only the workgroup whose range holds row T - 1 reads
-  // that row.
+  // workgroup's cache loads: only the workgroup whose range holds row T - 1
+  // reads that row.
   if constexpr (MODE == kScorePot || MODE == kScoreDs4a) {
     if (a.app_k != nullptr && split == a.n_splits - 1) {  // uniform per workgroup
       append_token<K>(a, seq, wave);
@@ -493,7 +510,7 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
   // workgroup's keys (Sec. II-E eq. av): weights are formed as p 2^(g_ref -
   // g_j) <= p, so they stay in fp16 range for any g, and the sums are scaled
   // by 2^-g_ref at the end (fp32). One barrier then publishes both.
-  prepare_queries<MODE, G, K>(a, kvh, b, a.qbuf + slot * a.qstride, DEBUG && split == 0);
+  prepare_queries<MODE, G, K>(a, kvh, b, a.qbuf + slot * a.qstride, DEBUG && split == 0, qin);
   if constexpr (V8) {
     int gmin = INT_MAX;
     for (int t = t_begin + 8 * tid; t < t_end; t += 8 * kBlock) {
