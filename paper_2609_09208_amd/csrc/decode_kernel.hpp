@@ -528,6 +528,14 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
   wait_stores_in_l2();
   __syncthreads();
   if constexpr (V8) gref = min(min(sm.gm[0], sm.gm[1]), min(sm.gm[2], sm.gm[3]));
+  // Fill the scalar cache with the slot's lines now, all at once (one load
+  // per 64-byte line), instead of one miss per code word in the first tile.
+  {
+    uint32_t warm = 0;
+#pragma unroll
+    for (int l = 0; l < (QL::kWords + G + 15) / 16; ++l) warm ^= (uint32_t)qb[16 * l];
+    asm volatile("" ::"s"(warm));
+  }
 
   // PoT scoring is long enough to cover the latency of value loads issued at
   // the start of the tile; the short INT8 / fp16 scoring is not, so those
