@@ -135,6 +135,52 @@ __device__ __forceinline__ uint32_t pot4_word(const float (&c)[8], uint32_t sgn,
   return (w ^ 0x77777777u) | (sgn & (w + 0x77777777u) & 0x88888888u);
 }
 
+// PoT-Mk code word and mantissa-plane bytes of 8 elements from their clamped
+// half ratios v_i = min(RN(|x_i| / (2 s)), 1) (0 for NaN): ratios up to 2 on
+// the unit interval, so that caller scales with |x| / s in [1, 2) still see
+// their mantissa. With v = (1 + M 2^-23) 2^(E-127) and Mc the mantissa of the
+// largest cut point (the one between the binade's top value and the next
+// binade), F = E + [M > Mc] - 119 (bits + 2^23 - 1 - Mc - (119 << 23), shifted)
+// gives the exponent field 7 - clamp(F, 1, 7) for a ratio above the zero cut
+// (F >= 8: the top value; F <= 0: the smallest magnitude), 7 for the zero
+// code. The mantissa is the number of cut points below m = 1 + M 2^-23 modulo
+// 2^k: with t = floor(m 2^k) = 2^k + j0, m lies above the cut between grid
+// points j0 and j0 + 1, RD(sqrt(t (t + 1)) / 2^k), exactly when (m 2^k)^2 >
+// t (t + 1) (the root is irrational), which one fused multiply-add decides
+// by its sign. Saturated ratios take j = 2^k - 1, the smallest magnitude and
+// the zero code j = 0. Returns the code word (signs as in pot4_word) and
+// writes the K plane bytes (bit i of plane b: bit b of element i's j).
+template <int K>
+__device__ __forceinline__ uint32_t potmk_word(const float (&v)[8], uint32_t sgn, uint32_t cmk,
+                                               uint32_t zc_half, uint32_t (&planes)[K]) {
+  constexpr uint32_t n = 1u << K;
+  uint32_t w = 0, jw = 0;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const uint32_t vb = __float_as_uint(v[i]);
+    const int f1 = (int)(vb + cmk) >> 23;
+    const uint32_t g = (vb > zc_half) ? (uint32_t)min(max(f1, 1), 7) : 0u;
+    w |= g << (4 * i);
+    const float mn = __uint_as_float((vb & 0x007FFFFFu) | ((127u + K) << 23));  // m 2^k
+    const uint32_t j0 = (vb >> (23 - K)) & (n - 1);
+    const float t = truncf(mn);                  // 2^k + j0
+    const float p = __builtin_fmaf(t, t, t);     // t (t + 1) <= 992, exact
+    const uint32_t above = (__builtin_fmaf(mn, mn, -p) > 0.0f) ? 1u : 0u;
+    uint32_t j = (j0 + above) & (n - 1);
+    j = (f1 > 7) ? n - 1 : j;
+    j = (f1 < 1) ? 0u : j;  // also every zero code
+    jw |= j << (4 * i);
+  }
+#pragma unroll
+  for (int b = 0; b < K; ++b) {  // bits 4i + b of jw to bit i
+    uint32_t x = (jw >> b) & 0x11111111u;
+    x = (x | (x >> 3)) & 0x03030303u;
+    x = (x | (x >> 6)) & 0x000F000Fu;
+    planes[b] = (x | (x >> 12)) & 0xFFu;
+  }
+  return (w ^ 0x77777777u) | (sgn & (w + 0x77777777u) & 0x88888888u);
+}
+
 template <int K, bool HAD>
 __global__ __launch_bounds__(kBlock) void encode_pot_kernel(
     const __half* __restrict__ k, int64_t n_rows, int64_t out_stride, int scale_mode,
@@ -144,9 +190,12 @@ __global__ __launch_bounds__(kBlock) void encode_pot_kernel(
   const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const uint32_t groups = (uint32_t)((n_rows + 7) / 8);
   const uint32_t stride = gridDim.x * (kBlock / 64);
-  // K = 0: bits-to-G offset of pot4_word (Mc from the fp32 cut point)
+  // K = 0: bits-to-G offset of pot4_word (Mc from the fp32 cut point); K > 0:
+  // the offset of potmk_word (the largest cut point) and half the zero cut
   const uint32_t cst =
-      0x007FFFFFu - (__float_as_uint(tab.cut[0]) & 0x007FFFFFu) - (120u << 23);
+      K == 0 ? 0x007FFFFFu - (__float_as_uint(tab.cut[0]) & 0x007FFFFFu) - (120u << 23)
+             : 0x007FFFFFu - (__float_as_uint(tab.cut[(1 << K) - 1]) & 0x007FFFFFu) - (119u << 23);
+  const uint32_t zc_half = __float_as_uint(tab.zero_cut) - (1u << 23);
   // lane parts of the addresses; a group's bases are uniform
   const uint32_t in_off = (uint32_t)(rl * kDim * 2 + 16 * g);
   const int64_t out_row = (int64_t)rl * out_stride;
@@ -204,65 +253,53 @@ __global__ __launch_bounds__(kBlock) void encode_pot_kernel(
     } else {
       s = valid ? key_scale[orow] : 0.0f;
     }
-    // u = RN(|x| / s) per element from one correctly rounded reciprocal per
-    // row; other scales (zero, negative, NaN, infinite, or too small or too
-    // large for a normal reciprocal) divide instead
-    const bool fast = recip_in_range(s);
-    const float r = recip_rn(s);
-    uint32_t word = 0;
-    uint32_t plane[K > 0 ? K : 1] = {};
-    if constexpr (K == 0) {
-      // c = min(u, 1) (u >= 1 saturates anyway), NaN -> 0 (zero code). The
-      // quotient q = RN(|x| r) is clamped too: min(q, 1) is still within an
-      // ulp of a quotient below 1, any q >= 1 gives c >= 1, and an infinite
-      // or NaN q (infinite or NaN x) cannot poison the residual.
-      float c[8];
-      if (fast) {
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const float a = fabsf(x[i]);
-          const float q = clamp01(a * r);
-          c[i] = clamp01(__builtin_fmaf(__builtin_fmaf(-q, s, a), r, q));
-        }
-      } else {
-#pragma unroll
-        for (int i = 0; i < 8; ++i) c[i] = (s > 0.0f) ? clamp01(fabsf(x[i]) / s) : 0.0f;
-      }
-      uint32_t sa, sb;  // sign bytes 0x00 / 0xFF of elements 0..3 and 4..7
-      if constexpr (HAD) {
-        const uint32_t xb[8] = {__float_as_uint(x[0]), __float_as_uint(x[1]),
-                                __float_as_uint(x[2]), __float_as_uint(x[3]),
-                                __float_as_uint(x[4]), __float_as_uint(x[5]),
-                                __float_as_uint(x[6]), __float_as_uint(x[7])};
-        // selector 9 / 11: bit 31 of the low / high source, 12: zero byte
-        sa = __builtin_amdgcn_perm(xb[1], xb[0], 0x0C0C0B09u) |
-             __builtin_amdgcn_perm(xb[3], xb[2], 0x0B090C0Cu);
-        sb = __builtin_amdgcn_perm(xb[5], xb[4], 0x0C0C0B09u) |
-             __builtin_amdgcn_perm(xb[7], xb[6], 0x0B090C0Cu);
-      } else {
-        // selectors 8..11: bits 15, 31 of the low and of the high source,
-        // the sign bits of the four halves
-        sa = __builtin_amdgcn_perm(w4[1], w4[0], 0x0B0A0908u);
-        sb = __builtin_amdgcn_perm(w4[3], w4[2], 0x0B0A0908u);
-      }
-      word = pot4_word(c, sign_nibbles(sa, sb), cst);
-    } else {
-      float u[8];
-      if (fast) {
-#pragma unroll
-        for (int i = 0; i < 8; ++i) u[i] = div_by_recip(fabsf(x[i]), s, r);
-      } else {
-#pragma unroll
-        for (int i = 0; i < 8; ++i) u[i] = fabsf(x[i]) / s;
-      }
-      const bool s_bad = !(s > 0.0f);
+    // The clamped ratio c = min(RN(|x| / ss), 1) per element (ss = s for
+    // PoT-4, 2 s for PoT-Mk), NaN -> 0 (zero code), from one correctly
+    // rounded reciprocal per row; other scales (zero, negative, NaN,
+    // infinite, or too small or too large for a normal reciprocal) divide
+    // instead. The quotient q = RN(|x| r) is clamped too: min(q, 1) is still
+    // within an ulp of a quotient below 1, any q >= 1 gives c >= 1, and an
+    // infinite or NaN q (infinite or NaN x) cannot poison the residual.
+    const float ss = K == 0 ? s : 2.0f * s;
+    const bool fast = recip_in_range(ss);
+    const float r = recip_rn(ss);
+    float c[8];
+    if (fast) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        int j;
-        word |= (uint32_t)code_from_ratio<K>(u[i], x[i] < 0.0f, s_bad, tab, &j) << (4 * i);
-#pragma unroll
-        for (int b = 0; b < K; ++b) plane[b] |= (uint32_t)((j >> b) & 1) << i;
+        const float a = fabsf(x[i]);
+        const float q = clamp01(a * r);
+        c[i] = clamp01(__builtin_fmaf(__builtin_fmaf(-q, ss, a), r, q));
       }
+    } else {
+      // (|x| / 2) / s rounds as |x| / (2 s) and stays finite-safe for huge s
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        c[i] = (s > 0.0f) ? clamp01((K == 0 ? fabsf(x[i]) : fabsf(x[i]) * 0.5f) / s) : 0.0f;
+    }
+    uint32_t sa, sb;  // sign bytes 0x00 / 0xFF of elements 0..3 and 4..7
+    if constexpr (HAD) {
+      const uint32_t xb[8] = {__float_as_uint(x[0]), __float_as_uint(x[1]),
+                              __float_as_uint(x[2]), __float_as_uint(x[3]),
+                              __float_as_uint(x[4]), __float_as_uint(x[5]),
+                              __float_as_uint(x[6]), __float_as_uint(x[7])};
+      // selector 9 / 11: bit 31 of the low / high source, 12: zero byte
+      sa = __builtin_amdgcn_perm(xb[1], xb[0], 0x0C0C0B09u) |
+           __builtin_amdgcn_perm(xb[3], xb[2], 0x0B090C0Cu);
+      sb = __builtin_amdgcn_perm(xb[5], xb[4], 0x0C0C0B09u) |
+           __builtin_amdgcn_perm(xb[7], xb[6], 0x0B090C0Cu);
+    } else {
+      // selectors 8..11: bits 15, 31 of the low and of the high source,
+      // the sign bits of the four halves
+      sa = __builtin_amdgcn_perm(w4[1], w4[0], 0x0B0A0908u);
+      sb = __builtin_amdgcn_perm(w4[3], w4[2], 0x0B0A0908u);
+    }
+    uint32_t word;
+    uint32_t plane[K > 0 ? K : 1];
+    if constexpr (K == 0) {
+      word = pot4_word(c, sign_nibbles(sa, sb), cst);
+    } else {
+      word = potmk_word<K>(c, sign_nibbles(sa, sb), cst, zc_half, plane);
     }
     if (valid) {
       const int64_t urow = row0 * out_stride;  // uniform part of orow

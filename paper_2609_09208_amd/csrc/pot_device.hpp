@@ -61,18 +61,6 @@ __device__ __forceinline__ int wave_quantize_int8(float x, float* step) {
   return (int)r;
 }
 
-// The correctly rounded quotient a / s from r = RN(1 / s): q = RN(a r) is
-// within one ulp of a / s, the residual a - q s is exact in one FMA, and
-// RN(q + residual * r) is the correctly rounded quotient (Markstein's
-// correction step; r must be the correctly rounded reciprocal, finite and
-// non-zero). An infinite q (a infinite, or past the largest float) is the
-// quotient's rounding already; the residual would be inf - inf there.
-__device__ __forceinline__ float div_by_recip(float a, float s, float r) {
-  const float q = a * r;
-  const float c = __builtin_fmaf(__builtin_fmaf(-q, s, a), r, q);
-  return (q < __builtin_inff()) ? c : q;
-}
-
 // Log-nearest PoT-Mk code of one element, mantissa width K (Sec. II-A, eq.
 // pot; Sec. II-D, eq. mant), from u = RN(|x| / s) (a zero or NaN x gives a
 // ratio at or below the zero cut, or NaN); s_bad: s is not positive. Branch-
