@@ -417,12 +417,25 @@ struct alignas(16) DecodeSmem {
 
 // VF: value format, 0 fp16 values, 1 INT8 values, 2 INT8 values with the
 // power-of-two weights of eq. logsm.
+// Resident waves per SIMD the register allocation must allow (1: no
+// constraint). The decoded-weight PoT-Mk path and the one- and two-plane
+// shift-accumulate paths would otherwise take a few registers more than four
+// waves leave (three per SIMD); held to four they keep every value in
+// registers, without spills (measured faster at every shape). The three-
+// and four-plane paths run at two or three waves, where a tighter budget
+// measured slower at B = 8.
+template <int MODE, int K>
+constexpr int kMinWaves = ((MODE == kScoreDs4a && K > 0) || (MODE == kScorePot && (K == 1 || K == 2)))
+                              ? 4
+                              : 1;
+
 template <int MODE, int G, int K, bool DEBUG, int VF>
 // qbuf is passed on its own as a restrict parameter: the prepared query
 // operands are never written here, which lets the compiler read them through
 // the scalar cache even in the debug variants that store score taps.
-__global__ __launch_bounds__(kBlock) void decode_kernel(const DecodeArgs a,
-                                                        const int32_t* __restrict__ qbuf) {
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
+    kMinWaves<MODE, K>))) void decode_kernel(const DecodeArgs a,
+                                                               const int32_t* __restrict__ qbuf) {
   using QL = QLayout<MODE, G, K>;
   __shared__ DecodeSmem sm;
   constexpr bool V8 = VF != 0;
