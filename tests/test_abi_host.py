@@ -187,6 +187,28 @@ def test_ds4a_rejects_bad_arguments():
     assert D(*args(pa.make_format(), se=FAKE + 4)) == pa.POT_ERR_INVALID_ARG
 
 
+def test_dot_rejects_bad_arguments():
+    hm = (np.arange(32, dtype=np.int32) // 8)
+    hp = hm.ctypes.data_as(ctypes.c_void_p)
+    D = pa._lib.pot_dot_decode_attention
+
+    def args(fmt=None, se=FAKE, cm=None, sc=FAKE, T=4096, t_cap=4096, ws=1 << 30):
+        fmt = fmt if fmt is not None else pa.make_format()
+        return (ctypes.byref(fmt), FAKE, se, cm, sc, FAKE, t_cap, hp, 1, 32, 4, T, FAKE, FAKE,
+                ws, None, None)
+    assert D(*args(se=None)) == pa.POT_ERR_INVALID_ARG
+    assert D(*args(sc=None)) == pa.POT_ERR_INVALID_ARG
+    assert D(*args(se=FAKE + 4)) == pa.POT_ERR_INVALID_ARG
+    assert D(*args(fmt=pa.make_format(mant_bits=4))) == pa.POT_ERR_INVALID_ARG  # planes NULL
+    assert D(*args(cm=FAKE)) == pa.POT_ERR_INVALID_ARG  # planes given for PoT-4
+    assert D(*args(fmt=pa.make_format(mant_bits=2), cm=FAKE + 4)) == pa.POT_ERR_INVALID_ARG
+    assert D(*args(fmt=pa.make_format(mant_bits=5), cm=FAKE)) == pa.POT_ERR_UNSUPPORTED
+    assert D(*args(fmt=pa.make_format(frac_bits=5))) == pa.POT_ERR_INVALID_ARG
+    assert D(*args(T=0)) == pa.POT_ERR_INVALID_ARG
+    assert D(*args(T=4097)) == pa.POT_ERR_INVALID_ARG  # beyond t_cap
+    assert D(*args(ws=16)) == pa.POT_ERR_WORKSPACE
+
+
 def test_append_rejects_bad_arguments():
     hm = (np.arange(32, dtype=np.int32) // 8)
     hp = hm.ctypes.data_as(ctypes.c_void_p)

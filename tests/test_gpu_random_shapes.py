@@ -7,8 +7,9 @@ against the oracle: codes, scales, q^, Delta, int32 scores and integer maxima
 bit-exact, O within 2e-3. The cases are fixed by their seeds, so the test is
 deterministic; together they cover combinations that the hand-written cases
 do not. A second set draws the same shapes over the INT8 value cache, with
-softmax or power-of-two weights and either score engine, and a third the
-fused append of the new token.
+softmax or power-of-two weights and either score engine, a third the fused
+append of the new token, and a fourth the decoded-code entry point
+(pot_dot_decode_attention) at every mantissa width.
 """
 import numpy as np
 import pytest
@@ -44,6 +45,19 @@ def test_random_shape(seed):
     err, g = assert_pot_parity(d, mant_bits=c["k"], frac_bits=c["F"], hadamard=c["hadamard"],
                                force_splits=c["splits"], engine=c["engine"])
     print(f"seed {seed} {c} splits={g['n_splits']} O err {err:.2e}")
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_random_shape_dot_engine(seed):
+    # the decoded-code entry point over the same kind of draws, every k
+    c = _case(100 + seed)
+    k = int(np.random.default_rng(9300 + seed).integers(0, 5))
+    d = make_decode_inputs(7100 + seed, B=c["B"], Hq=c["G"] * c["Hkv"], Hkv=c["Hkv"],
+                           T=c["T"], t_cap=c["t_cap"])
+    err, g = assert_pot_parity(d, mant_bits=k, frac_bits=c["F"], hadamard=c["hadamard"],
+                               force_splits=c["splits"], engine="dot")
+    shape = {key: c[key] for key in ("G", "Hkv", "B", "T", "t_cap", "hadamard", "F", "splits")}
+    print(f"seed {seed} {shape} k={k} dot splits={g['n_splits']} O err {err:.2e}")
 
 
 def _case_v8(seed):
