@@ -25,10 +25,31 @@ __device__ __forceinline__ float log2e_f32() { return __uint_as_float(0x3FB8AA3B
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 
+// One DPP lane move inside each row of 16 lanes (bound_ctrl: every source
+// lane exists for the patterns used here).
+template <int kCtrl>
+__device__ __forceinline__ float dpp_move(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), kCtrl,
+                                                            0xF, 0xF, true));
+}
+
+// Maximum over the wave (fmaxf: NaN ignored unless every lane is NaN), with
+// register-to-register moves only: neighbour and pair swaps, the mirror
+// inside each half row and each row (DPP), then the swaps of rows 0-1 / 2-3
+// and of the two halves (v_permlane16_swap, v_permlane32_swap). A maximum
+// does not care which lane of the other group it meets.
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
+  constexpr int kQuadSwap1 = 0xB1, kQuadSwap2 = 0x4E, kRowHalfMirror = 0x141, kRowMirror = 0x140;
+  v = fmaxf(v, dpp_move<kQuadSwap1>(v));
+  v = fmaxf(v, dpp_move<kQuadSwap2>(v));
+  v = fmaxf(v, dpp_move<kRowHalfMirror>(v));
+  v = fmaxf(v, dpp_move<kRowMirror>(v));
+  const auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v),
+                                                    false, false);
+  v = fmaxf(__uint_as_float(r16[0]), __uint_as_float(r16[1]));
+  const auto r32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v),
+                                                    false, false);
+  return fmaxf(__uint_as_float(r32[0]), __uint_as_float(r32[1]));
 }
 
 // Radix-2 Walsh-Hadamard butterfly over one 64-vector held one element per
