@@ -73,6 +73,22 @@ def test_encode_every_fp16_pattern_random_scales(k):
         assert np.array_equal(g[1], o[1])
 
 
+@pytest.mark.parametrize("k", [0, 1, 4])
+def test_encode_hadamard_with_caller_scales(k):
+    # the rotation followed by caller scales (scale mode 1): one log-uniform
+    # scale per row, every fp16 pattern, shuffled into rows; ratios of the
+    # rotated elements span [0, 2) and beyond
+    rng = np.random.default_rng(31 + k)
+    flat = _all_fp16_rows().reshape(-1)
+    rows = flat[rng.permutation(flat.size)].reshape(1024, 64)
+    sc = np.exp2(rng.uniform(-12.0, 16.0, 1024)).astype(np.float32)
+    g = gpu_encode(rows, k, True, key_scale=sc)
+    o = oracle.encode_keys(rows, mant_bits=k, hadamard=True, key_scale=sc)
+    assert np.array_equal(g[0], o[0])
+    if k:
+        assert np.array_equal(g[1], o[1])
+
+
 @pytest.mark.parametrize("k,had", [(0, False), (0, True), (1, False), (4, True)])
 def test_encode_absmax_every_fp16_pattern(k, had):
     # row scales from the rows themselves, over every fp16 pattern: in order
