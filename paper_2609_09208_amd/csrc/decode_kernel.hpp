@@ -62,6 +62,71 @@ typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 typedef short s16x2 __attribute__((ext_vector_type(2)));
 typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+
+// Shift-accumulate of one element pair for G heads (G = 2, 4 or 8): each
+// head's uniform word q[h] (operands q 2^7 of elements 8c + n and 8c + n + 4)
+// is shifted right arithmetically per half by the low four bits of the
+// matching half of sh, and the result is added into the head's int32 sum
+// a[h] by v_dot2_i32_i16 with the pair's weights w (1, -1 or 0 per half); the
+// first pair of a key starts the sums from 0. v_pk_ashrrev_i16 reads only
+// those four bits, so the caller need not clear the bits above them (a C++
+// vector shift needs every amount below 16 and so costs a mask). Heads go two
+// at a time, both shifts before both sums, so each v_dot2 reads a result
+// written two instructions earlier; one block for all G heads leaves the
+// compiler no boundary between them at which to add wait states.
+#define POT_SAC_SH(t, h) "v_pk_ashrrev_i16 %" #t ", %[sh], %[q" #h "]\n\t"
+#define POT_SAC_D0(h, t) "v_dot2_i32_i16 %[a" #h "], %" #t ", %[w], 0\n\t"
+#define POT_SAC_DC(h, t) "v_dot2c_i32_i16 %[a" #h "], %" #t ", %[w]\n\t"
+#define POT_SAC_2(D, x, y) POT_SAC_SH(0, x) POT_SAC_SH(1, y) D(x, 0) D(y, 1)
+template <int G, bool kFirst>
+__device__ __forceinline__ void sac_heads(int32_t* a, const uint32_t* q, uint32_t sh, uint32_t w) {
+  static_assert(G == 2 || G == 4 || G == 8, "two, four or eight heads");
+  uint32_t t0, t1;
+  if constexpr (G == 2) {
+    if constexpr (kFirst)
+      asm(POT_SAC_2(POT_SAC_D0, 0, 1)
+          : "=&v"(t0), "=&v"(t1), [a0] "=&v"(a[0]), [a1] "=&v"(a[1])
+          : [sh] "v"(sh), [w] "v"(w), [q0] "s"(q[0]), [q1] "s"(q[1]));
+    else
+      asm(POT_SAC_2(POT_SAC_DC, 0, 1)
+          : "=&v"(t0), "=&v"(t1), [a0] "+v"(a[0]), [a1] "+v"(a[1])
+          : [sh] "v"(sh), [w] "v"(w), [q0] "s"(q[0]), [q1] "s"(q[1]));
+  } else if constexpr (G == 4) {
+    if constexpr (kFirst)
+      asm(POT_SAC_2(POT_SAC_D0, 0, 1) POT_SAC_2(POT_SAC_D0, 2, 3)
+          : "=&v"(t0), "=&v"(t1), [a0] "=&v"(a[0]), [a1] "=&v"(a[1]), [a2] "=&v"(a[2]),
+            [a3] "=&v"(a[3])
+          : [sh] "v"(sh), [w] "v"(w), [q0] "s"(q[0]), [q1] "s"(q[1]), [q2] "s"(q[2]),
+            [q3] "s"(q[3]));
+    else
+      asm(POT_SAC_2(POT_SAC_DC, 0, 1) POT_SAC_2(POT_SAC_DC, 2, 3)
+          : "=&v"(t0), "=&v"(t1), [a0] "+v"(a[0]), [a1] "+v"(a[1]), [a2] "+v"(a[2]),
+            [a3] "+v"(a[3])
+          : [sh] "v"(sh), [w] "v"(w), [q0] "s"(q[0]), [q1] "s"(q[1]), [q2] "s"(q[2]),
+            [q3] "s"(q[3]));
+  } else {
+    if constexpr (kFirst)
+      asm(POT_SAC_2(POT_SAC_D0, 0, 1) POT_SAC_2(POT_SAC_D0, 2, 3)
+              POT_SAC_2(POT_SAC_D0, 4, 5) POT_SAC_2(POT_SAC_D0, 6, 7)
+          : "=&v"(t0), "=&v"(t1), [a0] "=&v"(a[0]), [a1] "=&v"(a[1]), [a2] "=&v"(a[2]),
+            [a3] "=&v"(a[3]), [a4] "=&v"(a[4]), [a5] "=&v"(a[5]), [a6] "=&v"(a[6]),
+            [a7] "=&v"(a[7])
+          : [sh] "v"(sh), [w] "v"(w), [q0] "s"(q[0]), [q1] "s"(q[1]), [q2] "s"(q[2]),
+            [q3] "s"(q[3]), [q4] "s"(q[4]), [q5] "s"(q[5]), [q6] "s"(q[6]), [q7] "s"(q[7]));
+    else
+      asm(POT_SAC_2(POT_SAC_DC, 0, 1) POT_SAC_2(POT_SAC_DC, 2, 3)
+              POT_SAC_2(POT_SAC_DC, 4, 5) POT_SAC_2(POT_SAC_DC, 6, 7)
+          : "=&v"(t0), "=&v"(t1), [a0] "+v"(a[0]), [a1] "+v"(a[1]), [a2] "+v"(a[2]),
+            [a3] "+v"(a[3]), [a4] "+v"(a[4]), [a5] "+v"(a[5]), [a6] "+v"(a[6]),
+            [a7] "+v"(a[7])
+          : [sh] "v"(sh), [w] "v"(w), [q0] "s"(q[0]), [q1] "s"(q[1]), [q2] "s"(q[2]),
+            [q3] "s"(q[3]), [q4] "s"(q[4]), [q5] "s"(q[5]), [q6] "s"(q[6]), [q7] "s"(q[7]));
+  }
+}
+#undef POT_SAC_2
+#undef POT_SAC_DC
+#undef POT_SAC_D0
+#undef POT_SAC_SH
 typedef float float4v __attribute__((ext_vector_type(4)));
 
 constexpr int kWaves = kBlock / 64;
@@ -595,6 +660,23 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
       // the same shifted operands with weights sigma or 0.
       constexpr int KP = K > 0 ? K : 1;
       int32_t accm[KP][G];
+      // With k = 0 and G > 1 the shifts and sums are one assembly block per
+      // element pair (sac_heads), and the operands arrive in chunks of two
+      // pairs (2 G words): chunk c + 1 is requested once chunk c is in
+      // registers, so every scalar load has a chunk's work to land in (a
+      // wait on scalar loads covers all of them, as they may return in any
+      // order). A zero offset that depends on the tile keeps the compiler
+      // from hoisting the loads out of the loop, where 32 G words would not
+      // fit in scalar registers.
+      constexpr bool kRaw = K == 0 && G > 1;
+      uint32_t qc[2][2 * kCols];
+      auto load_chunk = [&](int c) {
+        int toff = 0;
+        asm("" : "+s"(toff) : "s"(jt));
+#pragma unroll
+        for (int k = 0; k < 2 * kCols; ++k) qc[c & 1][k] = (uint32_t)qb[toff + 2 * kCols * c + k];
+      };
+      if constexpr (kRaw) load_chunk(0);
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         const uint32_t wi = w[i];
@@ -620,15 +702,30 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
         // zero offset that depends on the tile keeps the compiler from
         // hoisting all 32 G words out of the loop, where they would not fit
         // in scalar registers and would spill into vector lanes)
-        int toff = 0;
-        asm("" : "+s"(toff) : "s"(jt));
         uint32_t qq[4 * kCols];
+        if constexpr (!kRaw) {
+          int toff = 0;
+          asm("" : "+s"(toff) : "s"(jt));
 #pragma unroll
-        for (int k = 0; k < 4 * kCols; ++k) qq[k] = (uint32_t)qb[toff + 4 * kCols * i + k];
+          for (int k = 0; k < 4 * kCols; ++k) qq[k] = (uint32_t)qb[toff + 4 * kCols * i + k];
+        }
 #pragma unroll
         for (int n = 0; n < 4; ++n) {
-          // exponents of elements 8c + n and 8c + n + 4, one per half
-          const s16x2 sh = __builtin_bit_cast(s16x2, (x >> (4 * n)) & 0x000F000Fu);
+          const int c = 2 * i + (n >> 1);  // operand chunk (kRaw)
+          if constexpr (kRaw) {
+            if ((n & 1) == 0) {
+              asm volatile("" ::"s"(qc[c & 1][0]), "s"(qc[c & 1][2 * kCols - 1]));
+              __builtin_amdgcn_sched_barrier(0);
+              if (c + 1 < 16) load_chunk(c + 1);
+              __builtin_amdgcn_sched_barrier(0);
+            }
+          }
+          // exponents of elements 8c + n and 8c + n + 4, one per half (with
+          // G > 1 and k = 0 only their low four bits are read, see
+          // sac_heads, and the bits above them are left in place)
+          constexpr bool kRaw = K == 0 && G > 1;
+          const uint32_t shr = x >> (4 * n);
+          const s16x2 sh = __builtin_bit_cast(s16x2, kRaw ? shr : shr & 0x000F000Fu);
           // the weights of elements 8c + n and 8c + n + 4
           const s16x2 sg = __builtin_bit_cast(s16x2, sw << (12 - 4 * n)) >> (short)14;
           s16x2 mw[KP];
@@ -661,6 +758,17 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
           // before nearly every v_dot2).
 #pragma unroll
           for (int h = 0; h < G; h += 2) {
+            if constexpr (kRaw) {
+              if (h == 0) {
+                const uint32_t wsg = __builtin_bit_cast(uint32_t, sg);
+                const uint32_t* qp = &qc[c & 1][kCols * (n & 1)];
+                if (i == 0 && n == 0)
+                  sac_heads<G, true>(accv, qp, shr, wsg);
+                else
+                  sac_heads<G, false>(accv, qp, shr, wsg);
+              }
+              continue;
+            }
             const s16x2 pv0 = __builtin_bit_cast(s16x2, qq[kCols * n + h]) >> sh;
             if constexpr (G > 1) {
               const s16x2 pv1 = __builtin_bit_cast(s16x2, qq[kCols * n + h + 1]) >> sh;
