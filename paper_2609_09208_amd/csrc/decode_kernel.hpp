@@ -123,6 +123,51 @@ __device__ __forceinline__ void sac_heads(int32_t* a, const uint32_t* q, uint32_
             [q3] "s"(q[3]), [q4] "s"(q[4]), [q5] "s"(q[5]), [q6] "s"(q[6]), [q7] "s"(q[7]));
   }
 }
+// The same for one mantissa bit plane (k = 1): each shifted operand also goes
+// into the head's plane sum c[h] with the plane weights m (sigma where the
+// element's mantissa bit is set, else 0).
+#define POT_SAC1_D0(h, t)                                 \
+  "v_dot2_i32_i16 %[a" #h "], %" #t ", %[w], 0\n\t" \
+  "v_dot2_i32_i16 %[c" #h "], %" #t ", %[m], 0\n\t"
+#define POT_SAC1_DC(h, t)                              \
+  "v_dot2c_i32_i16 %[a" #h "], %" #t ", %[w]\n\t" \
+  "v_dot2c_i32_i16 %[c" #h "], %" #t ", %[m]\n\t"
+template <int G, bool kFirst>
+__device__ __forceinline__ void sac_heads_m1(int32_t* a, int32_t* c, const uint32_t* q, uint32_t sh,
+                                             uint32_t w, uint32_t m) {
+  static_assert(G == 2 || G == 4 || G == 8, "two, four or eight heads");
+  uint32_t t0, t1;
+  if constexpr (G == 2) {
+    if constexpr (kFirst)
+      asm(POT_SAC_2(POT_SAC1_D0, 0, 1)
+          : "=&v"(t0), "=&v"(t1), [a0] "=&v"(a[0]), [a1] "=&v"(a[1]), [c0] "=&v"(c[0]), [c1] "=&v"(c[1])
+          : [sh] "v"(sh), [w] "v"(w), [m] "v"(m), [q0] "s"(q[0]), [q1] "s"(q[1]));
+    else
+      asm(POT_SAC_2(POT_SAC1_DC, 0, 1)
+          : "=&v"(t0), "=&v"(t1), [a0] "+v"(a[0]), [a1] "+v"(a[1]), [c0] "+v"(c[0]), [c1] "+v"(c[1])
+          : [sh] "v"(sh), [w] "v"(w), [m] "v"(m), [q0] "s"(q[0]), [q1] "s"(q[1]));
+  } else if constexpr (G == 4) {
+    if constexpr (kFirst)
+      asm(POT_SAC_2(POT_SAC1_D0, 0, 1) POT_SAC_2(POT_SAC1_D0, 2, 3)
+          : "=&v"(t0), "=&v"(t1), [a0] "=&v"(a[0]), [a1] "=&v"(a[1]), [a2] "=&v"(a[2]), [a3] "=&v"(a[3]), [c0] "=&v"(c[0]), [c1] "=&v"(c[1]), [c2] "=&v"(c[2]), [c3] "=&v"(c[3])
+          : [sh] "v"(sh), [w] "v"(w), [m] "v"(m), [q0] "s"(q[0]), [q1] "s"(q[1]), [q2] "s"(q[2]), [q3] "s"(q[3]));
+    else
+      asm(POT_SAC_2(POT_SAC1_DC, 0, 1) POT_SAC_2(POT_SAC1_DC, 2, 3)
+          : "=&v"(t0), "=&v"(t1), [a0] "+v"(a[0]), [a1] "+v"(a[1]), [a2] "+v"(a[2]), [a3] "+v"(a[3]), [c0] "+v"(c[0]), [c1] "+v"(c[1]), [c2] "+v"(c[2]), [c3] "+v"(c[3])
+          : [sh] "v"(sh), [w] "v"(w), [m] "v"(m), [q0] "s"(q[0]), [q1] "s"(q[1]), [q2] "s"(q[2]), [q3] "s"(q[3]));
+  } else if constexpr (G == 8) {
+    if constexpr (kFirst)
+      asm(POT_SAC_2(POT_SAC1_D0, 0, 1) POT_SAC_2(POT_SAC1_D0, 2, 3) POT_SAC_2(POT_SAC1_D0, 4, 5) POT_SAC_2(POT_SAC1_D0, 6, 7)
+          : "=&v"(t0), "=&v"(t1), [a0] "=&v"(a[0]), [a1] "=&v"(a[1]), [a2] "=&v"(a[2]), [a3] "=&v"(a[3]), [a4] "=&v"(a[4]), [a5] "=&v"(a[5]), [a6] "=&v"(a[6]), [a7] "=&v"(a[7]), [c0] "=&v"(c[0]), [c1] "=&v"(c[1]), [c2] "=&v"(c[2]), [c3] "=&v"(c[3]), [c4] "=&v"(c[4]), [c5] "=&v"(c[5]), [c6] "=&v"(c[6]), [c7] "=&v"(c[7])
+          : [sh] "v"(sh), [w] "v"(w), [m] "v"(m), [q0] "s"(q[0]), [q1] "s"(q[1]), [q2] "s"(q[2]), [q3] "s"(q[3]), [q4] "s"(q[4]), [q5] "s"(q[5]), [q6] "s"(q[6]), [q7] "s"(q[7]));
+    else
+      asm(POT_SAC_2(POT_SAC1_DC, 0, 1) POT_SAC_2(POT_SAC1_DC, 2, 3) POT_SAC_2(POT_SAC1_DC, 4, 5) POT_SAC_2(POT_SAC1_DC, 6, 7)
+          : "=&v"(t0), "=&v"(t1), [a0] "+v"(a[0]), [a1] "+v"(a[1]), [a2] "+v"(a[2]), [a3] "+v"(a[3]), [a4] "+v"(a[4]), [a5] "+v"(a[5]), [a6] "+v"(a[6]), [a7] "+v"(a[7]), [c0] "+v"(c[0]), [c1] "+v"(c[1]), [c2] "+v"(c[2]), [c3] "+v"(c[3]), [c4] "+v"(c[4]), [c5] "+v"(c[5]), [c6] "+v"(c[6]), [c7] "+v"(c[7])
+          : [sh] "v"(sh), [w] "v"(w), [m] "v"(m), [q0] "s"(q[0]), [q1] "s"(q[1]), [q2] "s"(q[2]), [q3] "s"(q[3]), [q4] "s"(q[4]), [q5] "s"(q[5]), [q6] "s"(q[6]), [q7] "s"(q[7]));
+  }
+}
+#undef POT_SAC1_DC
+#undef POT_SAC1_D0
 #undef POT_SAC_2
 #undef POT_SAC_DC
 #undef POT_SAC_D0
@@ -668,7 +713,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
       // order). A zero offset that depends on the tile keeps the compiler
       // from hoisting the loads out of the loop, where 32 G words would not
       // fit in scalar registers.
-      constexpr bool kRaw = K == 0 && G > 1;
+      constexpr bool kRaw = K <= 1 && G > 1;
       uint32_t qc[2][2 * kCols];
       auto load_chunk = [&](int c) {
         int toff = 0;
@@ -721,9 +766,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
             }
           }
           // exponents of elements 8c + n and 8c + n + 4, one per half (with
-          // G > 1 and k = 0 only their low four bits are read, see
+          // G > 1 and k <= 1 only their low four bits are read, see
           // sac_heads, and the bits above them are left in place)
-          constexpr bool kRaw = K == 0 && G > 1;
           const uint32_t shr = x >> (4 * n);
           const s16x2 sh = __builtin_bit_cast(s16x2, kRaw ? shr : shr & 0x000F000Fu);
           // the weights of elements 8c + n and 8c + n + 4
@@ -762,10 +806,18 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
               if (h == 0) {
                 const uint32_t wsg = __builtin_bit_cast(uint32_t, sg);
                 const uint32_t* qp = &qc[c & 1][kCols * (n & 1)];
-                if (i == 0 && n == 0)
-                  sac_heads<G, true>(accv, qp, shr, wsg);
-                else
-                  sac_heads<G, false>(accv, qp, shr, wsg);
+                if constexpr (K == 0) {
+                  if (i == 0 && n == 0)
+                    sac_heads<G, true>(accv, qp, shr, wsg);
+                  else
+                    sac_heads<G, false>(accv, qp, shr, wsg);
+                } else {
+                  const uint32_t wm = __builtin_bit_cast(uint32_t, mw[0]);
+                  if (i == 0 && n == 0)
+                    sac_heads_m1<G, true>(accv, accm[0], qp, shr, wsg, wm);
+                  else
+                    sac_heads_m1<G, false>(accv, accm[0], qp, shr, wsg, wm);
+                }
               }
               continue;
             }
