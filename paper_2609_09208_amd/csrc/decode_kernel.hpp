@@ -12,8 +12,10 @@
 //  1. Scores, one key per lane (Sec. II-B eq. sac). PoT-4: the key's 32 code
 //     bytes arrive as two 16-byte loads. Each query operand holds two
 //     elements of one head as signed 16-bit halves, q 2^7 (prepared once per
-//     kv head, read through the scalar cache one code word's group at a
-//     time). v_pk_ashrrev_i16 shifts each half by its element's exponent e:
+//     kv head, read through the scalar cache in chunks of two element pairs,
+//     each requested while the previous one is used). v_pk_ashrrev_i16
+//     (inline assembly, which reads the exponent nibbles in place) shifts
+//     each half by its element's exponent e:
 //     q 2^7 >> e = q 2^(7 - e), exact since the low 7 bits are clear, so
 //     every product q 2^(7 - e) is formed by the shifter with head-room
 //     F_int = 7 >= e (eq. exact). v_dot2_i32_i16 then applies the signs and
@@ -168,6 +170,110 @@ __device__ __forceinline__ void sac_heads_m1(int32_t* a, int32_t* c, const uint3
 }
 #undef POT_SAC1_DC
 #undef POT_SAC1_D0
+// The same for k = 2, 3 or 4 mantissa bit planes, H = 2 or 4 heads per block
+// (the operand count of one statement is limited): plane b's sum of head h is
+// c[b][h0 + h], with the plane weights m[b].
+#define POT_DOT0(acc, t, wt) "v_dot2_i32_i16 %[" acc "], %" #t ", %[" wt "], 0\n\t"
+#define POT_DOTC(acc, t, wt) "v_dot2c_i32_i16 %[" acc "], %" #t ", %[" wt "]\n\t"
+#define POT_HEAD_K2(D, h, t) D("a" #h, t, "w") D("c0" #h, t, "m0") D("c1" #h, t, "m1")
+#define POT_HEAD_K3(D, h, t) POT_HEAD_K2(D, h, t) D("c2" #h, t, "m2")
+#define POT_HEAD_K4(D, h, t) POT_HEAD_K3(D, h, t) D("c3" #h, t, "m3")
+#define POT_PAIR(HK, D, x, y) POT_SAC_SH(0, x) POT_SAC_SH(1, y) HK(D, x, 0) HK(D, y, 1)
+template <int H, int K, int G, bool kFirst>
+__device__ __forceinline__ void sac_heads_mk(int32_t* a, int32_t (*c)[G], int h0, const uint32_t* q,
+                                             uint32_t sh, uint32_t w, const uint32_t* m) {
+  static_assert((H == 2 && K >= 2 && K <= 4) || (H == 4 && (K == 2 || K == 3)),
+                "two heads with two to four planes, or four heads with two or three");
+  uint32_t t0, t1;
+  if constexpr (H == 2 && K == 2 && kFirst) {
+    asm(POT_PAIR(POT_HEAD_K2, POT_DOT0, 0, 1)
+        : "=&v"(t0), "=&v"(t1), [a0] "=&v"(a[h0 + 0]), [a1] "=&v"(a[h0 + 1]),
+          [c00] "=&v"(c[0][h0 + 0]), [c01] "=&v"(c[0][h0 + 1]), [c10] "=&v"(c[1][h0 + 0]),
+          [c11] "=&v"(c[1][h0 + 1])
+        : [sh] "v"(sh), [w] "v"(w), [m0] "v"(m[0]), [m1] "v"(m[1]), [q0] "s"(q[0]),
+          [q1] "s"(q[1]));
+  } else if constexpr (H == 2 && K == 2 && !kFirst) {
+    asm(POT_PAIR(POT_HEAD_K2, POT_DOTC, 0, 1)
+        : "=&v"(t0), "=&v"(t1), [a0] "+v"(a[h0 + 0]), [a1] "+v"(a[h0 + 1]),
+          [c00] "+v"(c[0][h0 + 0]), [c01] "+v"(c[0][h0 + 1]), [c10] "+v"(c[1][h0 + 0]),
+          [c11] "+v"(c[1][h0 + 1])
+        : [sh] "v"(sh), [w] "v"(w), [m0] "v"(m[0]), [m1] "v"(m[1]), [q0] "s"(q[0]),
+          [q1] "s"(q[1]));
+  } else if constexpr (H == 2 && K == 3 && kFirst) {
+    asm(POT_PAIR(POT_HEAD_K3, POT_DOT0, 0, 1)
+        : "=&v"(t0), "=&v"(t1), [a0] "=&v"(a[h0 + 0]), [a1] "=&v"(a[h0 + 1]),
+          [c00] "=&v"(c[0][h0 + 0]), [c01] "=&v"(c[0][h0 + 1]), [c10] "=&v"(c[1][h0 + 0]),
+          [c11] "=&v"(c[1][h0 + 1]), [c20] "=&v"(c[2][h0 + 0]), [c21] "=&v"(c[2][h0 + 1])
+        : [sh] "v"(sh), [w] "v"(w), [m0] "v"(m[0]), [m1] "v"(m[1]), [m2] "v"(m[2]),
+          [q0] "s"(q[0]), [q1] "s"(q[1]));
+  } else if constexpr (H == 2 && K == 3 && !kFirst) {
+    asm(POT_PAIR(POT_HEAD_K3, POT_DOTC, 0, 1)
+        : "=&v"(t0), "=&v"(t1), [a0] "+v"(a[h0 + 0]), [a1] "+v"(a[h0 + 1]),
+          [c00] "+v"(c[0][h0 + 0]), [c01] "+v"(c[0][h0 + 1]), [c10] "+v"(c[1][h0 + 0]),
+          [c11] "+v"(c[1][h0 + 1]), [c20] "+v"(c[2][h0 + 0]), [c21] "+v"(c[2][h0 + 1])
+        : [sh] "v"(sh), [w] "v"(w), [m0] "v"(m[0]), [m1] "v"(m[1]), [m2] "v"(m[2]),
+          [q0] "s"(q[0]), [q1] "s"(q[1]));
+  } else if constexpr (H == 2 && K == 4 && kFirst) {
+    asm(POT_PAIR(POT_HEAD_K4, POT_DOT0, 0, 1)
+        : "=&v"(t0), "=&v"(t1), [a0] "=&v"(a[h0 + 0]), [a1] "=&v"(a[h0 + 1]),
+          [c00] "=&v"(c[0][h0 + 0]), [c01] "=&v"(c[0][h0 + 1]), [c10] "=&v"(c[1][h0 + 0]),
+          [c11] "=&v"(c[1][h0 + 1]), [c20] "=&v"(c[2][h0 + 0]), [c21] "=&v"(c[2][h0 + 1]),
+          [c30] "=&v"(c[3][h0 + 0]), [c31] "=&v"(c[3][h0 + 1])
+        : [sh] "v"(sh), [w] "v"(w), [m0] "v"(m[0]), [m1] "v"(m[1]), [m2] "v"(m[2]),
+          [m3] "v"(m[3]), [q0] "s"(q[0]), [q1] "s"(q[1]));
+  } else if constexpr (H == 2 && K == 4 && !kFirst) {
+    asm(POT_PAIR(POT_HEAD_K4, POT_DOTC, 0, 1)
+        : "=&v"(t0), "=&v"(t1), [a0] "+v"(a[h0 + 0]), [a1] "+v"(a[h0 + 1]),
+          [c00] "+v"(c[0][h0 + 0]), [c01] "+v"(c[0][h0 + 1]), [c10] "+v"(c[1][h0 + 0]),
+          [c11] "+v"(c[1][h0 + 1]), [c20] "+v"(c[2][h0 + 0]), [c21] "+v"(c[2][h0 + 1]),
+          [c30] "+v"(c[3][h0 + 0]), [c31] "+v"(c[3][h0 + 1])
+        : [sh] "v"(sh), [w] "v"(w), [m0] "v"(m[0]), [m1] "v"(m[1]), [m2] "v"(m[2]),
+          [m3] "v"(m[3]), [q0] "s"(q[0]), [q1] "s"(q[1]));
+  } else if constexpr (H == 4 && K == 2 && kFirst) {
+    asm(POT_PAIR(POT_HEAD_K2, POT_DOT0, 0, 1) POT_PAIR(POT_HEAD_K2, POT_DOT0, 2, 3)
+        : "=&v"(t0), "=&v"(t1), [a0] "=&v"(a[h0 + 0]), [a1] "=&v"(a[h0 + 1]),
+          [a2] "=&v"(a[h0 + 2]), [a3] "=&v"(a[h0 + 3]), [c00] "=&v"(c[0][h0 + 0]),
+          [c01] "=&v"(c[0][h0 + 1]), [c02] "=&v"(c[0][h0 + 2]), [c03] "=&v"(c[0][h0 + 3]),
+          [c10] "=&v"(c[1][h0 + 0]), [c11] "=&v"(c[1][h0 + 1]), [c12] "=&v"(c[1][h0 + 2]),
+          [c13] "=&v"(c[1][h0 + 3])
+        : [sh] "v"(sh), [w] "v"(w), [m0] "v"(m[0]), [m1] "v"(m[1]), [q0] "s"(q[0]),
+          [q1] "s"(q[1]), [q2] "s"(q[2]), [q3] "s"(q[3]));
+  } else if constexpr (H == 4 && K == 2 && !kFirst) {
+    asm(POT_PAIR(POT_HEAD_K2, POT_DOTC, 0, 1) POT_PAIR(POT_HEAD_K2, POT_DOTC, 2, 3)
+        : "=&v"(t0), "=&v"(t1), [a0] "+v"(a[h0 + 0]), [a1] "+v"(a[h0 + 1]), [a2] "+v"(a[h0 + 2]),
+          [a3] "+v"(a[h0 + 3]), [c00] "+v"(c[0][h0 + 0]), [c01] "+v"(c[0][h0 + 1]),
+          [c02] "+v"(c[0][h0 + 2]), [c03] "+v"(c[0][h0 + 3]), [c10] "+v"(c[1][h0 + 0]),
+          [c11] "+v"(c[1][h0 + 1]), [c12] "+v"(c[1][h0 + 2]), [c13] "+v"(c[1][h0 + 3])
+        : [sh] "v"(sh), [w] "v"(w), [m0] "v"(m[0]), [m1] "v"(m[1]), [q0] "s"(q[0]),
+          [q1] "s"(q[1]), [q2] "s"(q[2]), [q3] "s"(q[3]));
+  } else if constexpr (H == 4 && K == 3 && kFirst) {
+    asm(POT_PAIR(POT_HEAD_K3, POT_DOT0, 0, 1) POT_PAIR(POT_HEAD_K3, POT_DOT0, 2, 3)
+        : "=&v"(t0), "=&v"(t1), [a0] "=&v"(a[h0 + 0]), [a1] "=&v"(a[h0 + 1]),
+          [a2] "=&v"(a[h0 + 2]), [a3] "=&v"(a[h0 + 3]), [c00] "=&v"(c[0][h0 + 0]),
+          [c01] "=&v"(c[0][h0 + 1]), [c02] "=&v"(c[0][h0 + 2]), [c03] "=&v"(c[0][h0 + 3]),
+          [c10] "=&v"(c[1][h0 + 0]), [c11] "=&v"(c[1][h0 + 1]), [c12] "=&v"(c[1][h0 + 2]),
+          [c13] "=&v"(c[1][h0 + 3]), [c20] "=&v"(c[2][h0 + 0]), [c21] "=&v"(c[2][h0 + 1]),
+          [c22] "=&v"(c[2][h0 + 2]), [c23] "=&v"(c[2][h0 + 3])
+        : [sh] "v"(sh), [w] "v"(w), [m0] "v"(m[0]), [m1] "v"(m[1]), [m2] "v"(m[2]),
+          [q0] "s"(q[0]), [q1] "s"(q[1]), [q2] "s"(q[2]), [q3] "s"(q[3]));
+  } else if constexpr (H == 4 && K == 3 && !kFirst) {
+    asm(POT_PAIR(POT_HEAD_K3, POT_DOTC, 0, 1) POT_PAIR(POT_HEAD_K3, POT_DOTC, 2, 3)
+        : "=&v"(t0), "=&v"(t1), [a0] "+v"(a[h0 + 0]), [a1] "+v"(a[h0 + 1]), [a2] "+v"(a[h0 + 2]),
+          [a3] "+v"(a[h0 + 3]), [c00] "+v"(c[0][h0 + 0]), [c01] "+v"(c[0][h0 + 1]),
+          [c02] "+v"(c[0][h0 + 2]), [c03] "+v"(c[0][h0 + 3]), [c10] "+v"(c[1][h0 + 0]),
+          [c11] "+v"(c[1][h0 + 1]), [c12] "+v"(c[1][h0 + 2]), [c13] "+v"(c[1][h0 + 3]),
+          [c20] "+v"(c[2][h0 + 0]), [c21] "+v"(c[2][h0 + 1]), [c22] "+v"(c[2][h0 + 2]),
+          [c23] "+v"(c[2][h0 + 3])
+        : [sh] "v"(sh), [w] "v"(w), [m0] "v"(m[0]), [m1] "v"(m[1]), [m2] "v"(m[2]),
+          [q0] "s"(q[0]), [q1] "s"(q[1]), [q2] "s"(q[2]), [q3] "s"(q[3]));
+  }
+}
+#undef POT_PAIR
+#undef POT_HEAD_K4
+#undef POT_HEAD_K3
+#undef POT_HEAD_K2
+#undef POT_DOTC
+#undef POT_DOT0
 #undef POT_SAC_2
 #undef POT_SAC_DC
 #undef POT_SAC_D0
@@ -705,15 +811,15 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
       // the same shifted operands with weights sigma or 0.
       constexpr int KP = K > 0 ? K : 1;
       int32_t accm[KP][G];
-      // With k = 0 and G > 1 the shifts and sums are one assembly block per
-      // element pair (sac_heads), and the operands arrive in chunks of two
-      // pairs (2 G words): chunk c + 1 is requested once chunk c is in
-      // registers, so every scalar load has a chunk's work to land in (a
-      // wait on scalar loads covers all of them, as they may return in any
+      // With G > 1 the shifts and sums are assembly blocks per element pair
+      // (sac_heads, sac_heads_m1, sac_heads_mk), and the operands arrive in
+      // chunks of two pairs (2 G words): chunk c + 1 is requested once chunk
+      // c is in registers, so every scalar load has a chunk's work to land in
+      // (a wait on scalar loads covers all of them, as they may return in any
       // order). A zero offset that depends on the tile keeps the compiler
       // from hoisting the loads out of the loop, where 32 G words would not
       // fit in scalar registers.
-      constexpr bool kRaw = K <= 1 && G > 1;
+      constexpr bool kRaw = G > 1;
       uint32_t qc[2][2 * kCols];
       auto load_chunk = [&](int c) {
         int toff = 0;
@@ -743,10 +849,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
           const uint32_t pw = (i < 4) ? ks.pl[bb].x : ks.pl[bb].y;
           pb[bb] = __builtin_amdgcn_perm(pw, pw, (uint32_t)(i & 3) * 0x00010001u | 0x0C000C00u);
         }
-        // this code word's operands, read as one scalar group per tile (a
-        // zero offset that depends on the tile keeps the compiler from
-        // hoisting all 32 G words out of the loop, where they would not fit
-        // in scalar registers and would spill into vector lanes)
+        // one head: this code word's four operand words, read as one scalar
+        // group per tile (the zero offset as for the chunks)
         uint32_t qq[4 * kCols];
         if constexpr (!kRaw) {
           int toff = 0;
@@ -765,11 +869,10 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
               __builtin_amdgcn_sched_barrier(0);
             }
           }
-          // exponents of elements 8c + n and 8c + n + 4, one per half (with
-          // G > 1 and k <= 1 only their low four bits are read, see
-          // sac_heads, and the bits above them are left in place)
+          // exponents of elements 8c + n and 8c + n + 4, one per half (the
+          // shifts in sac_heads* read only the low four bits of each half, so
+          // the bits above them stay; the one-head C++ path masks them)
           const uint32_t shr = x >> (4 * n);
-          const s16x2 sh = __builtin_bit_cast(s16x2, kRaw ? shr : shr & 0x000F000Fu);
           // the weights of elements 8c + n and 8c + n + 4
           const s16x2 sg = __builtin_bit_cast(s16x2, sw << (12 - 4 * n)) >> (short)14;
           s16x2 mw[KP];
@@ -782,55 +885,46 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
                 __builtin_bit_cast(s16x2, __builtin_bit_cast(u16x2, pb[bb]) << amt) >> (short)15;
             mw[bb] = bit & sg;
           }
-          // the first pair starts each sum from the constant 0; with clamp
-          // set (|sum| <= 2 * 16256, never reached) the compiler emits the
-          // three-operand form instead of zeroing the accumulator first
-          auto accumulate = [&](int h, s16x2 pv) {
-            accv[h] = (i == 0 && n == 0) ? __builtin_amdgcn_sdot2(pv, sg, 0, true)
-                                         : __builtin_amdgcn_sdot2(pv, sg, accv[h], false);
+          const bool first = i == 0 && n == 0;  // the first pair starts every sum from 0
+          if constexpr (kRaw) {
+            const uint32_t wsg = __builtin_bit_cast(uint32_t, sg);
+            const uint32_t* qp = &qc[c & 1][kCols * (n & 1)];
+            if constexpr (K == 0) {
+              if (first)
+                sac_heads<G, true>(accv, qp, shr, wsg);
+              else
+                sac_heads<G, false>(accv, qp, shr, wsg);
+            } else if constexpr (K == 1) {
+              const uint32_t wm = __builtin_bit_cast(uint32_t, mw[0]);
+              if (first)
+                sac_heads_m1<G, true>(accv, accm[0], qp, shr, wsg, wm);
+              else
+                sac_heads_m1<G, false>(accv, accm[0], qp, shr, wsg, wm);
+            } else {
+              constexpr int H = (K == 4 || G == 2) ? 2 : 4;
+              uint32_t wm[K];
+#pragma unroll
+              for (int bb = 0; bb < K; ++bb) wm[bb] = __builtin_bit_cast(uint32_t, mw[bb]);
+#pragma unroll
+              for (int h0 = 0; h0 < G; h0 += H) {
+                if (first)
+                  sac_heads_mk<H, K, G, true>(accv, accm, h0, qp + h0, shr, wsg, wm);
+                else
+                  sac_heads_mk<H, K, G, false>(accv, accm, h0, qp + h0, shr, wsg, wm);
+              }
+            }
+          } else {
+            // one head: the same sums in C++ (with clamp set, |sum| <= 2 *
+            // 16256 is never reached, the compiler emits the three-operand
+            // form for the first pair instead of zeroing the sum first)
+            const s16x2 pv = __builtin_bit_cast(s16x2, qq[n]) >>
+                             __builtin_bit_cast(s16x2, shr & 0x000F000Fu);
+            accv[0] = first ? __builtin_amdgcn_sdot2(pv, sg, 0, true)
+                            : __builtin_amdgcn_sdot2(pv, sg, accv[0], false);
 #pragma unroll
             for (int bb = 0; bb < K; ++bb)
-              accm[bb][h] = (i == 0 && n == 0)
-                                ? __builtin_amdgcn_sdot2(pv, mw[bb], 0, true)
-                                : __builtin_amdgcn_sdot2(pv, mw[bb], accm[bb][h], false);
-          };
-          // Two heads at a time: both shifts, then both heads' sums. The
-          // scheduling barriers keep this order, so the shifted operands
-          // alternate between two registers and no v_dot2 reads a register
-          // that the instruction just before it wrote while the v_dot2 before
-          // that read it (with one register the compiler puts a wait state
-          // before nearly every v_dot2).
-#pragma unroll
-          for (int h = 0; h < G; h += 2) {
-            if constexpr (kRaw) {
-              if (h == 0) {
-                const uint32_t wsg = __builtin_bit_cast(uint32_t, sg);
-                const uint32_t* qp = &qc[c & 1][kCols * (n & 1)];
-                if constexpr (K == 0) {
-                  if (i == 0 && n == 0)
-                    sac_heads<G, true>(accv, qp, shr, wsg);
-                  else
-                    sac_heads<G, false>(accv, qp, shr, wsg);
-                } else {
-                  const uint32_t wm = __builtin_bit_cast(uint32_t, mw[0]);
-                  if (i == 0 && n == 0)
-                    sac_heads_m1<G, true>(accv, accm[0], qp, shr, wsg, wm);
-                  else
-                    sac_heads_m1<G, false>(accv, accm[0], qp, shr, wsg, wm);
-                }
-              }
-              continue;
-            }
-            const s16x2 pv0 = __builtin_bit_cast(s16x2, qq[kCols * n + h]) >> sh;
-            if constexpr (G > 1) {
-              const s16x2 pv1 = __builtin_bit_cast(s16x2, qq[kCols * n + h + 1]) >> sh;
-              __builtin_amdgcn_sched_barrier(0);
-              accumulate(h, pv0);
-              accumulate(h + 1, pv1);
-              __builtin_amdgcn_sched_barrier(0);
-            } else {
-              accumulate(h, pv0);
-            }
+              accm[bb][0] = first ? __builtin_amdgcn_sdot2(pv, mw[bb], 0, true)
+                                  : __builtin_amdgcn_sdot2(pv, mw[bb], accm[bb][0], false);
           }
         }
       }
