@@ -795,6 +795,27 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
     const bool kvalid = t < t_end;
     float xs[G];
     // ---- 1. scores (lane = key) ----
+    // Query operands of the shift paths (two element pairs of every head per
+    // chunk, 2 G words; 16 chunks per key): chunk c + 1 is requested
+    // once chunk c is in registers, so every scalar load has a chunk's work to
+    // land in (a wait on scalar loads covers all of them, as they may return
+    // in any order). A zero offset that depends on the tile keeps the
+    // compiler from hoisting the loads out of the loop, where 32 G words
+    // would not fit in scalar registers.
+    uint32_t qc[2][2 * kCols];
+    auto load_chunk = [&](int c) {
+      int toff = 0;
+      asm("" : "+s"(toff) : "s"(jt));
+#pragma unroll
+      for (int k = 0; k < 2 * kCols; ++k) qc[c & 1][k] = (uint32_t)qb[toff + 2 * kCols * c + k];
+    };
+    // wait for chunk c, then request chunk c + 1
+    auto next_chunk = [&](int c) {
+      asm volatile("" ::"s"(qc[c & 1][0]), "s"(qc[c & 1][2 * kCols - 1]));
+      __builtin_amdgcn_sched_barrier(0);
+      if (c + 1 < 16) load_chunk(c + 1);
+      __builtin_amdgcn_sched_barrier(0);
+    };
     if constexpr (MODE == kScorePot) {
       const uint32_t w[8] = {ks.c0.x, ks.c0.y, ks.c0.z, ks.c0.w,
                              ks.c1.x, ks.c1.y, ks.c1.z, ks.c1.w};
@@ -812,21 +833,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
       constexpr int KP = K > 0 ? K : 1;
       int32_t accm[KP][G];
       // With G > 1 the shifts and sums are assembly blocks per element pair
-      // (sac_heads, sac_heads_m1, sac_heads_mk), and the operands arrive in
-      // chunks of two pairs (2 G words): chunk c + 1 is requested once chunk
-      // c is in registers, so every scalar load has a chunk's work to land in
-      // (a wait on scalar loads covers all of them, as they may return in any
-      // order). A zero offset that depends on the tile keeps the compiler
-      // from hoisting the loads out of the loop, where 32 G words would not
-      // fit in scalar registers.
+      // (sac_heads, sac_heads_m1, sac_heads_mk) over operand chunks (above).
       constexpr bool kRaw = G > 1;
-      uint32_t qc[2][2 * kCols];
-      auto load_chunk = [&](int c) {
-        int toff = 0;
-        asm("" : "+s"(toff) : "s"(jt));
-#pragma unroll
-        for (int k = 0; k < 2 * kCols; ++k) qc[c & 1][k] = (uint32_t)qb[toff + 2 * kCols * c + k];
-      };
       if constexpr (kRaw) load_chunk(0);
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
@@ -862,12 +870,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
         for (int n = 0; n < 4; ++n) {
           const int c = 2 * i + (n >> 1);  // operand chunk (kRaw)
           if constexpr (kRaw) {
-            if ((n & 1) == 0) {
-              asm volatile("" ::"s"(qc[c & 1][0]), "s"(qc[c & 1][2 * kCols - 1]));
-              __builtin_amdgcn_sched_barrier(0);
-              if (c + 1 < 16) load_chunk(c + 1);
-              __builtin_amdgcn_sched_barrier(0);
-            }
+            if ((n & 1) == 0) next_chunk(c);
           }
           // exponents of elements 8c + n and 8c + n + 4, one per half (the
           // shifts in sac_heads* read only the low four bits of each half, so
@@ -992,6 +995,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
         // three bits
         const uint32_t sw = (wi & 0x88888888u) | (~(y >> 1) & 0x44444444u);
         const uint32_t nx = ~wi;
+        // this code word's operands as one scalar group (one wait per code
+        // word: the chunked loads of the shift paths measured slower here)
         int toff = 0;
         asm("" : "+s"(toff) : "s"(jt));
         uint32_t qq[4 * kCols];
