@@ -112,6 +112,16 @@ typedef struct pot_format {
  *               the split combine), so that kernel can be timed alone. They
  *               do not select the instrumented build. A failed record returns
  *               POT_ERR_HIP.
+ *  force_wg_waves (in) 0: the planner picks the decode workgroup size; 4:
+ *               four-wave workgroups, each wave taking every fourth 64-key
+ *               tile of its split; or the wave count of the CU-wide variant
+ *               of the shift-accumulate kernels over fp16 values (16 at
+ *               k <= 2, 12 at k = 3 and 4): one workgroup per CU whose
+ *               waves claim the split's tiles from a counter in LDS. Other
+ *               values return POT_ERR_INVALID_ARG. Scores and maxima do not
+ *               depend on it; O does to fp32 rounding (with claimed tiles the
+ *               order of the sums varies from call to call).
+ *  wg_waves     (out) the waves per workgroup used (written on the host)
  */
 typedef struct pot_debug {
   int8_t* qhat;
@@ -124,6 +134,8 @@ typedef struct pot_debug {
   int32_t split_len;
   void* decode_begin;
   void* decode_end;
+  int32_t force_wg_waves;
+  int32_t wg_waves;
 } pot_debug;
 
 /* Static string for a status code. Never NULL. */

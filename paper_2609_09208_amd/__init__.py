@@ -42,7 +42,8 @@ class pot_debug(ctypes.Structure):
                 ("scores", ctypes.c_void_p), ("m_final", ctypes.c_void_p),
                 ("m_split", ctypes.c_void_p), ("force_splits", ctypes.c_int32),
                 ("n_splits", ctypes.c_int32), ("split_len", ctypes.c_int32),
-                ("decode_begin", ctypes.c_void_p), ("decode_end", ctypes.c_void_p)]
+                ("decode_begin", ctypes.c_void_p), ("decode_end", ctypes.c_void_p),
+                ("force_wg_waves", ctypes.c_int32), ("wg_waves", ctypes.c_int32)]
 
 
 def make_format(mant_bits: int = 0, frac_bits: int = 7, hadamard: bool = False,

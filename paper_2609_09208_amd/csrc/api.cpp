@@ -122,10 +122,10 @@ Plan plan_bound(int B, int Hkv, int T) {
 }
 
 std::atomic<int> g_cus[64];
-// [score mode][value format][G][mant_bits]
-std::atomic<int> g_occ[4][3][9][5];
+// [default / CU-wide variant][score mode][value format][G][mant_bits]
+std::atomic<int> g_occ[2][4][3][9][5];
 
-long device_slots(int mode, int G, int mant_bits, int vf) {
+int device_cus() {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
   int cus = g_cus[dev].load(std::memory_order_relaxed);
@@ -135,15 +135,25 @@ long device_slots(int mode, int G, int mant_bits, int vf) {
       cus = 256;
     g_cus[dev].store(cus, std::memory_order_relaxed);
   }
-  std::atomic<int>& slot = g_occ[mode][vf][G][mant_bits];
+  return cus;
+}
+
+long device_slots(int mode, int G, int mant_bits, int vf, bool pool) {
+  const int cus = device_cus();
+  std::atomic<int>& slot = g_occ[pool ? 1 : 0][mode][vf][G][mant_bits];
   int occ = slot.load(std::memory_order_relaxed);
   if (occ <= 0) {
-    occ = decode_occupancy(mode, G, mant_bits, vf);
-    if (occ <= 0) occ = 2;
+    occ = decode_occupancy(mode, G, mant_bits, vf, pool);
+    if (occ <= 0) occ = pool ? 1 : 2;
     slot.store(occ, std::memory_order_relaxed);
   }
   return (long)cus * occ;
 }
+
+// The CU-wide variant (one workgroup of pool_waves(...) waves per CU, tiles
+// claimed from a shared counter) replaces the four-wave workgroups when its
+// plan still gives every CU a workgroup and every wave two tiles on average.
+constexpr int kPoolTilesPerWave = 2;
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
@@ -221,15 +231,35 @@ pot_status decode_common(int mode, int mant_bits, DecodeArgs& a, const int32_t* 
   if (st != POT_OK) return st;
   const int force = dbg ? dbg->force_splits : 0;
   if (force < 0) return fail(POT_ERR_INVALID_ARG, "force_splits %d < 0", force);
+  const int mbits = (mode == kScorePot || mode == kScoreDs4a) ? mant_bits : 0;
+  const int pw = pool_waves(mode, mbits, vf);
+  const int want = dbg ? dbg->force_wg_waves : 0;
+  if (want != 0 && want != kBlock / 64 && (pw == 0 || want != pw))
+    return fail(POT_ERR_INVALID_ARG, "force_wg_waves %d is neither 0, %d nor %d", want,
+                kBlock / 64, pw);
+  const long units = (long)B * Hkv;
   Plan p;
+  bool pool = false;
   if (force > 0) {
     p = plan_from_count(T, force);
+    pool = pw > 0 && (want == pw || (want == 0 && units * p.n_splits >= device_cus() &&
+                                     p.split_len >= kPoolTilesPerWave * pw * 64));
   } else {
-    const int mbits = (mode == kScorePot || mode == kScoreDs4a) ? mant_bits : 0;
-    const int S = split_count_for_slots((long)B * Hkv, device_slots(mode, G, mbits, vf));
-    const int tiles = (T + kTile - 1) / kTile;
-    const int s_short = split_count_short_ranges((long)B * Hkv, tiles);
-    p = plan_from_count(T, std::min({S, s_short, plan_bound(B, Hkv, T).n_splits}));
+    if (pw > 0 && want != kBlock / 64) {
+      const int S = split_count_for_slots(units, device_slots(mode, G, mbits, vf, true));
+      const Plan pp = plan_from_count(T, std::min(S, plan_bound(B, Hkv, T).n_splits));
+      if (want == pw ||
+          (units * pp.n_splits >= device_cus() && pp.split_len >= kPoolTilesPerWave * pw * 64)) {
+        p = pp;
+        pool = true;
+      }
+    }
+    if (!pool) {
+      const int S = split_count_for_slots(units, device_slots(mode, G, mbits, vf, false));
+      const int tiles = (T + kTile - 1) / kTile;
+      const int s_short = split_count_short_ranges(units, tiles);
+      p = plan_from_count(T, std::min({S, s_short, plan_bound(B, Hkv, T).n_splits}));
+    }
   }
   const WsLayout w = ws_layout(B, Hq, Hkv, p.n_splits);
   if (ws_bytes < w.total)
@@ -248,6 +278,7 @@ pot_status decode_common(int mode, int mant_bits, DecodeArgs& a, const int32_t* 
   a.T = T;
   a.n_splits = p.n_splits;
   a.split_len = p.split_len;
+  a.wg_waves = pool ? pw : kBlock / 64;
   bool debug = false;
   hipEvent_t ev_begin = nullptr, ev_end = nullptr;
   if (dbg) {
@@ -261,6 +292,7 @@ pot_status decode_common(int mode, int mant_bits, DecodeArgs& a, const int32_t* 
     debug = dbg->qhat || dbg->delta || dbg->scores || dbg->m_final || dbg->m_split;
     dbg->n_splits = p.n_splits;
     dbg->split_len = p.split_len;
+    dbg->wg_waves = a.wg_waves;
     if (debug && mode == kScoreFp16)
       return fail(POT_ERR_UNSUPPORTED, "debug taps are not available on the fp16 path");
   }

@@ -280,7 +280,18 @@ __device__ __forceinline__ void sac_heads_mk(int32_t* a, int32_t (*c)[G], int h0
 #undef POT_SAC_SH
 typedef float float4v __attribute__((ext_vector_type(4)));
 
-constexpr int kWaves = kBlock / 64;
+constexpr int kWaves = kBlock / 64;  // waves per workgroup of the default variant
+// Waves per workgroup of the CU-wide variant (0: none). A SIMD issues the
+// oldest of its ready waves first, so of the four equal workgroups that
+// share a CU the first dispatched finishes in about a third of the time of
+// the last, and the CU runs its last stretch with one wave per SIMD. In the
+// CU-wide variant one workgroup holds all of a CU's waves (four per SIMD at
+// k <= 2, three at k = 3 and 4: what the registers of those kernels
+// allow) and its waves take tiles from a counter in LDS, so they all finish
+// within about one tile of each other. Built for the shift-accumulate kernels
+// over fp16 values.
+template <int MODE, int K, int VF>
+constexpr int kPoolWaves = pool_waves(MODE, K, VF);
 constexpr int kWTile = 64;    // keys per wave tile
 constexpr int kXRow = 68;     // floats per head row of the transposed score tile
 constexpr float kPScale = 12.0f;  // p is formed as 2^(x - M + 12) (fp16-normal range)
@@ -533,21 +544,21 @@ __device__ __forceinline__ void append_token(const DecodeArgs& a, int64_t seq, i
     store_value_token_wave(a.app_v + seq * kDim, a.app_v_cache + seq * a.t_cap * kDim, a.T - 1);
 }
 
-// The query elements of the heads this wave prepares (wave w: heads w,
-// w + 4), one per lane; loaded first thing so that their latency overlaps
+// The query elements of the heads this wave prepares (wave w of NW: heads w,
+// w + NW), one per lane; loaded first thing so that their latency overlaps
 // the rest of the prologue.
-template <int G>
+template <int G, int NW>
 struct QueryIn {
-  static constexpr int kHeadsPerWave = (G + kWaves - 1) / kWaves;
+  static constexpr int kHeadsPerWave = (G + NW - 1) / NW;
   float v[kHeadsPerWave];
 };
-template <int G>
-__device__ __forceinline__ QueryIn<G> load_queries(const DecodeArgs& a, int kvh, int b) {
+template <int G, int NW>
+__device__ __forceinline__ QueryIn<G, NW> load_queries(const DecodeArgs& a, int kvh, int b) {
   const int lane = lane_id(), wave = threadIdx.x >> 6;
-  QueryIn<G> qin;
+  QueryIn<G, NW> qin;
 #pragma unroll
-  for (int i = 0; i < QueryIn<G>::kHeadsPerWave; ++i) {
-    const int h = wave + kWaves * i;
+  for (int i = 0; i < QueryIn<G, NW>::kHeadsPerWave; ++i) {
+    const int h = wave + NW * i;
     qin.v[i] = h < G ? a.q[((int64_t)b * a.Hq + a.q_of_kv[kvh * G + h]) * kDim + lane] : 0.0f;
   }
   return qin;
@@ -556,20 +567,20 @@ __device__ __forceinline__ QueryIn<G> load_queries(const DecodeArgs& a, int kvh,
 // Rotates (optionally) and quantises the G query vectors of one (batch, kv
 // head) and writes the operand words and per-head score factors that the
 // score loop reads through the scalar cache, into qb (this workgroup's own
-// slot of the workspace). Called by all four waves of the workgroup; wave w
-// handles heads w, w + 4, whose elements qin holds. taps: also write the q^
+// slot of the workspace). Called by all NW waves of the workgroup; wave w
+// handles heads w, w + NW, whose elements qin holds. taps: also write the q^
 // and Delta debug taps.
-template <int MODE, int G, int K>
+template <int MODE, int G, int K, int NW>
 __device__ __forceinline__ void prepare_queries(const DecodeArgs& a, int kvh, int b,
                                                 int32_t* __restrict__ qb, bool taps,
-                                                const QueryIn<G>& qin) {
+                                                const QueryIn<G, NW>& qin) {
   using QL = QLayout<MODE, G, K>;
   const int lane = lane_id(), wave = threadIdx.x >> 6;
   float* cb = reinterpret_cast<float*>(qb + QL::kWords);
-  constexpr int kHeadsPerWave = QueryIn<G>::kHeadsPerWave;
+  constexpr int kHeadsPerWave = QueryIn<G, NW>::kHeadsPerWave;
 #pragma unroll
   for (int i = 0; i < kHeadsPerWave; ++i) {
-    const int h = wave + kWaves * i;
+    const int h = wave + NW * i;
     if (h >= G) break;
     const int64_t bq = (int64_t)b * a.Hq + a.q_of_kv[kvh * G + h];
     float qv = qin.v[i];
@@ -622,13 +633,15 @@ __device__ __forceinline__ void prepare_queries(const DecodeArgs& a, int kvh, in
 }
 
 // ---- shared memory of the decode kernel -------------------------------------
+template <int NW>
 struct alignas(16) DecodeSmem {
-  alignas(16) float x[kWaves][8][kXRow];  // transposed score tile per wave
-  float wo[kWaves][16][kDim];             // per-wave P.V (rows: heads x {hi, lo})
-  float wl[kWaves][16];
-  float wp[kWaves][64];  // INT8 values: per-lane sums of the unscaled weights
-  int wm[kWaves][8];
-  int gm[kWaves];        // INT8 values: per-wave minimum exponent
+  alignas(16) float x[NW][8][kXRow];  // transposed score tile per wave
+  float wo[NW][16][kDim];             // per-wave P.V (rows: heads x {hi, lo})
+  float wl[NW][16];
+  float wp[NW][64];  // INT8 values: per-lane sums of the unscaled weights
+  int wm[NW][8];
+  int gm[NW];        // INT8 values: per-wave minimum exponent
+  int next;          // CU-wide variant: the next unclaimed tile of the range
 };
 
 // VF: value format, 0 fp16 values, 1 INT8 values, 2 INT8 values with the
@@ -645,15 +658,19 @@ constexpr int kMinWaves = ((MODE == kScoreDs4a && K > 0) || (MODE == kScorePot &
                               ? 4
                               : 1;
 
-template <int MODE, int G, int K, bool DEBUG, int VF>
+// NW: waves per workgroup, kWaves or kPoolWaves<MODE, K, VF> (the CU-wide
+// variant, whose waves take their tiles from the counter sm.next).
+template <int MODE, int G, int K, bool DEBUG, int VF, int NW>
 // qbuf is passed on its own as a restrict parameter: the prepared query
 // operands are never written here, which lets the compiler read them through
 // the scalar cache even in the debug variants that store score taps.
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
-    kMinWaves<MODE, K>))) void decode_kernel(const DecodeArgs a,
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(
+    NW > kWaves ? NW / 4 : kMinWaves<MODE, K>))) void decode_kernel(const DecodeArgs a,
                                                                const int32_t* __restrict__ qbuf) {
   using QL = QLayout<MODE, G, K>;
-  __shared__ DecodeSmem sm;
+  constexpr bool kPool = NW > kWaves;
+  constexpr int kBlk = 64 * NW;
+  __shared__ DecodeSmem<NW> sm;
   constexpr bool V8 = VF != 0;
   constexpr bool kPow2 = VF == 2;
   constexpr int kCols = QL::kCols;
@@ -680,7 +697,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
   const int row = lane & 15, grp = lane >> 4, hrow = row & 7, part = row >> 3;
   const bool hvalid = hrow < G;
 
-  const QueryIn<G> qin = load_queries<G>(a, kvh, b);
+  const QueryIn<G, NW> qin = load_queries<G, NW>(a, kvh, b);
   // The sequence's new token (fused append) is written before any of this
   // workgroup's cache loads: only the workgroup whose range holds row T - 1
   // reads that row.
@@ -730,19 +747,28 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
     else
       load_keys<MODE, K>(a, row0 + min(t0 + lane, t_end - 1), kk);
   };
+  // Tiles: wave w starts with tiles w and w + NW; after that the default
+  // variant takes every NW-th tile and the CU-wide one claims the next
+  // unclaimed tile (from 2 NW on) one tile ahead of its use.
   int j = wave;
+  int jn = wave + NW;  // CU-wide variant: this wave's next tile
+  int jc = 0;          // CU-wide variant: the tile claimed during the current one
   const int j_last = n_tiles - 1;
   if (j < n_tiles) load_keys_tile(j, kr[0]);
+  if constexpr (kPool) {
+    if (tid == 0) sm.next = 2 * NW;
+  }
 
   // Query preparation into this workgroup's slot while the first codes load;
   // with INT8 values also the reference exponent g_ref = min g over this
   // workgroup's keys (Sec. II-E eq. av): weights are formed as p 2^(g_ref -
   // g_j) <= p, so they stay in fp16 range for any g, and the sums are scaled
   // by 2^-g_ref at the end (fp32). One barrier then publishes both.
-  prepare_queries<MODE, G, K>(a, kvh, b, a.qbuf + slot * a.qstride, DEBUG && split == 0, qin);
+  prepare_queries<MODE, G, K, NW>(a, kvh, b, a.qbuf + slot * a.qstride, DEBUG && split == 0,
+                                  qin);
   if constexpr (V8) {
     int gmin = INT_MAX;
-    for (int t = t_begin + 8 * tid; t < t_end; t += 8 * kBlock) {
+    for (int t = t_begin + 8 * tid; t < t_end; t += 8 * kBlk) {
       const uint2 w = *reinterpret_cast<const uint2*>(eseq + t);
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
@@ -756,7 +782,11 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
   }
   wait_stores_in_l2();
   __syncthreads();
-  if constexpr (V8) gref = min(min(sm.gm[0], sm.gm[1]), min(sm.gm[2], sm.gm[3]));
+  if constexpr (V8) {
+    gref = sm.gm[0];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) gref = min(gref, sm.gm[w]);
+  }
   // Fill the scalar cache with the slot's lines now, all at once (one load
   // per 64-byte line), instead of one miss per code word in the first tile.
   {
@@ -783,13 +813,21 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
   auto stage1 = [&](const KeyRegs<MODE, K>& ks, KeyRegs<MODE, K>& knext, ValRegs<V8>& vs,
                     ValRegs<V8>& vnext, int jt) {
     const int t0 = t_begin + kWTile * jt;
-    const int jn = min(jt + kWaves, j_last);
+    // the next tile's keys (past the range: the last tile again, unused)
+    const int jl = min(kPool ? jn : jt + NW, j_last);
     if constexpr (kPrefetchV) {
-      load_keys_tile(jn, knext);
-      load_values_buf<V8>(st, t_begin + kWTile * jn, lane, vnext);
+      load_keys_tile(jl, knext);
+      load_values_buf<V8>(st, t_begin + kWTile * jl, lane, vnext);
     } else {
       load_values_buf<V8>(st, t0, lane, vs);
-      load_keys_tile(jn, knext);
+      load_keys_tile(jl, knext);
+    }
+    if constexpr (kPool) {
+      // claim the tile after jn now; it is needed one tile from now
+      int c = 0;
+      if (lane == 0) c = __hip_atomic_fetch_add(&sm.next, 1, __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_WORKGROUP);
+      jc = __builtin_amdgcn_readfirstlane(c);
     }
     const int t = t0 + lane;
     const bool kvalid = t < t_end;
@@ -1274,7 +1312,12 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
   auto advance = [&]() {
     kr[0] = kr[1];
     if constexpr (kPrefetchV) vr[0] = vr[1];
-    j += kWaves;
+    if constexpr (kPool) {
+      j = jn;
+      jn = jc;
+    } else {
+      j += NW;
+    }
   };
 #pragma nounroll
   while (j < n_tiles) {
@@ -1304,15 +1347,15 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(
   __syncthreads();
 
   const int Sn = a.n_splits;
-  for (int idx = tid; idx < G * kDim; idx += kBlock) {
+  for (int idx = tid; idx < G * kDim; idx += kBlk) {
     const int h = idx / kDim, d = idx % kDim;
     const int64_t bq = (int64_t)b * a.Hq + a.q_of_kv[kvh * G + h];
     int M = INT_MIN;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) M = max(M, sm.wm[w][h]);
+    for (int w = 0; w < NW; ++w) M = max(M, sm.wm[w][h]);
     float o = 0.0f, l = 0.0f;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
+    for (int w = 0; w < NW; ++w) {
       if (sm.wm[w][h] == INT_MIN) continue;
       const float f = __builtin_amdgcn_ldexpf(1.0f, sm.wm[w][h] - M);
       if constexpr (V8) {
@@ -1442,11 +1485,21 @@ static hipError_t launch_t(const DecodeArgs& a, hipStream_t stream, hipEvent_t e
   if constexpr (VF != 0 && MODE != kScorePot && MODE != kScoreDs4a) {
     return hipErrorInvalidValue;
   } else {
+  constexpr int PW = kPoolWaves<MODE, K, VF>;
   hipError_t e = hipSuccess;
   if (ev_begin != nullptr && (e = hipEventRecord(ev_begin, stream)) != hipSuccess) return e;
   const dim3 grid((uint32_t)a.n_splits, (uint32_t)a.Hkv, (uint32_t)a.B);
-  hipLaunchKernelGGL((decode_kernel<MODE, G, K, DEBUG, VF>), grid, dim3(kBlock), 0, stream, a,
-                     static_cast<const int32_t*>(a.qbuf));
+  if constexpr (PW > 0) {
+    if (a.wg_waves == PW)
+      hipLaunchKernelGGL((decode_kernel<MODE, G, K, DEBUG, VF, PW>), grid, dim3(64 * PW), 0,
+                         stream, a, static_cast<const int32_t*>(a.qbuf));
+    else
+      hipLaunchKernelGGL((decode_kernel<MODE, G, K, DEBUG, VF, kWaves>), grid, dim3(kBlock), 0,
+                         stream, a, static_cast<const int32_t*>(a.qbuf));
+  } else {
+    hipLaunchKernelGGL((decode_kernel<MODE, G, K, DEBUG, VF, kWaves>), grid, dim3(kBlock), 0,
+                       stream, a, static_cast<const int32_t*>(a.qbuf));
+  }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (ev_end != nullptr && (e = hipEventRecord(ev_end, stream)) != hipSuccess) return e;
   if (a.n_splits == 1) return hipSuccess;
@@ -1457,13 +1510,25 @@ static hipError_t launch_t(const DecodeArgs& a, hipStream_t stream, hipEvent_t e
 }
 
 template <int MODE, int G, int K, int VF>
-static int occupancy_t() {
+static int occupancy_t(bool pool) {
+  constexpr int PW = kPoolWaves<MODE, K, VF>;
   int n = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
-          &n, reinterpret_cast<const void*>(&decode_kernel<MODE, G, K, false, VF>), kBlock, 0) !=
-      hipSuccess)
-    return 0;
-  return n;
+  hipError_t e;
+  if constexpr (PW > 0) {
+    if (pool)
+      e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+          &n, reinterpret_cast<const void*>(&decode_kernel<MODE, G, K, false, VF, PW>), 64 * PW,
+          0);
+    else
+      e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+          &n, reinterpret_cast<const void*>(&decode_kernel<MODE, G, K, false, VF, kWaves>), kBlock,
+          0);
+  } else {
+    if (pool) return 0;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+        &n, reinterpret_cast<const void*>(&decode_kernel<MODE, G, K, false, VF, kWaves>), kBlock, 0);
+  }
+  return e == hipSuccess ? n : 0;
 }
 
 template <int MODE, int G, bool DEBUG, int VF>
@@ -1509,19 +1574,19 @@ hipError_t launch_mode_vf(int G, int mant_bits, bool debug, const DecodeArgs& a,
 }
 
 template <int MODE, int VF>
-int occupancy_mode_vf(int G, int mant_bits) {
+int occupancy_mode_vf(int G, int mant_bits, bool pool) {
   auto by_k = [&](auto g_tag) -> int {
     constexpr int GG = decltype(g_tag)::value;
     if constexpr (MODE == kScorePot || (MODE == kScoreDs4a && VF == 0)) {
       switch (mant_bits) {
-        case 0: return occupancy_t<MODE, GG, 0, VF>();
-        case 1: return occupancy_t<MODE, GG, 1, VF>();
-        case 2: return occupancy_t<MODE, GG, 2, VF>();
-        case 3: return occupancy_t<MODE, GG, 3, VF>();
-        default: return occupancy_t<MODE, GG, 4, VF>();
+        case 0: return occupancy_t<MODE, GG, 0, VF>(pool);
+        case 1: return occupancy_t<MODE, GG, 1, VF>(pool);
+        case 2: return occupancy_t<MODE, GG, 2, VF>(pool);
+        case 3: return occupancy_t<MODE, GG, 3, VF>(pool);
+        default: return occupancy_t<MODE, GG, 4, VF>(pool);
       }
     } else {
-      return occupancy_t<MODE, GG, 0, VF>();
+      return occupancy_t<MODE, GG, 0, VF>(pool);
     }
   };
   switch (G) {

@@ -4,18 +4,18 @@
 
 namespace potattn {
 
-int decode_occupancy(int mode, int G, int mant_bits, int vf) {
+int decode_occupancy(int mode, int G, int mant_bits, int vf, bool pool) {
   switch (mode) {
     case kScorePot:
-      return vf == 1 ? occupancy_mode_vf<kScorePot, 1>(G, mant_bits)
-             : vf == 2 ? occupancy_mode_vf<kScorePot, 2>(G, mant_bits)
-                       : occupancy_mode_vf<kScorePot, 0>(G, mant_bits);
+      return vf == 1 ? occupancy_mode_vf<kScorePot, 1>(G, mant_bits, pool)
+             : vf == 2 ? occupancy_mode_vf<kScorePot, 2>(G, mant_bits, pool)
+                       : occupancy_mode_vf<kScorePot, 0>(G, mant_bits, pool);
     case kScoreDs4a:
-      return vf == 1 ? occupancy_mode_vf<kScoreDs4a, 1>(G, mant_bits)
-             : vf == 2 ? occupancy_mode_vf<kScoreDs4a, 2>(G, mant_bits)
-                       : occupancy_mode_vf<kScoreDs4a, 0>(G, mant_bits);
-    case kScoreInt8: return occupancy_mode_vf<kScoreInt8, 0>(G, 0);
-    case kScoreFp16: return occupancy_mode_vf<kScoreFp16, 0>(G, 0);
+      return vf == 1 ? occupancy_mode_vf<kScoreDs4a, 1>(G, mant_bits, pool)
+             : vf == 2 ? occupancy_mode_vf<kScoreDs4a, 2>(G, mant_bits, pool)
+                       : occupancy_mode_vf<kScoreDs4a, 0>(G, mant_bits, pool);
+    case kScoreInt8: return occupancy_mode_vf<kScoreInt8, 0>(G, 0, pool);
+    case kScoreFp16: return occupancy_mode_vf<kScoreFp16, 0>(G, 0, pool);
     default: return 0;
   }
 }

@@ -95,8 +95,16 @@ struct DecodeArgs {
   int32_t B, Hq, Hkv, T;
   int32_t n_splits, split_len;
   int32_t frac_bits, hadamard;
+  int32_t wg_waves;            // waves per decode workgroup: 4, or pool_waves(...)
   int32_t q_of_kv[kMaxHqArg];  // [Hkv][G] query heads served by each kv head
 };
+
+// Waves per workgroup of a decode kernel's CU-wide variant, 0 if it has
+// none: the shift-accumulate kernels over fp16 values, four waves per SIMD
+// at k <= 2 and three at k = 3, 4 (their register budgets).
+constexpr int pool_waves(int mode, int mant_bits, int vf) {
+  return (mode == kScorePot && vf == 0) ? (mant_bits <= 2 ? 16 : 12) : 0;
+}
 
 // Longest key range of one decode call: the decode kernel reads each
 // sequence's cache rows through buffer resources with 32-bit byte ranges
@@ -110,8 +118,9 @@ constexpr int kMaxKeys = (1 << 24) - 8;
 constexpr int query_words(int G) { return (33 * G + 63) / 64 * 64; }
 
 // Resident workgroups per CU of the (non-debug) decode kernel for this
-// variant, from the HIP occupancy calculator; 0 if the query fails.
-int decode_occupancy(int mode, int G, int mant_bits, int vf);
+// variant (pool: its CU-wide variant), from the HIP occupancy calculator; 0 if
+// the query fails.
+int decode_occupancy(int mode, int G, int mant_bits, int vf, bool pool);
 
 // vf: value format. 0: fp16 value cache (a.v); 1: INT8 value cache (a.v8,
 // a.v_exp); 2: INT8 values with the power-of-two weights of eq. logsm.
@@ -128,6 +137,6 @@ template <int MODE, int VF>
 hipError_t launch_mode_vf(int G, int mant_bits, bool debug, const DecodeArgs& a,
                           hipStream_t stream, hipEvent_t e0, hipEvent_t e1);
 template <int MODE, int VF>
-int occupancy_mode_vf(int G, int mant_bits);
+int occupancy_mode_vf(int G, int mant_bits, bool pool);
 
 }  // namespace potattn

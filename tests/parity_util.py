@@ -48,7 +48,7 @@ def gpu_encode(k_bits, mant_bits=0, hadamard=False, key_scale=None, frac_bits=7)
 
 
 def gpu_pot_decode(d, codes_se, codes_m, key_scale, mant_bits=0, frac_bits=7,
-                   hadamard=False, taps=True, force_splits=0, engine="sac"):
+                   hadamard=False, taps=True, force_splits=0, engine="sac", wg_waves=0):
     """d: workloads.make_decode_inputs dict; cache arrays are host numpy in the
     row layout. engine "sac" runs pot_decode_attention (shift-accumulate),
     "ds4a" pot_ds4a_decode_attention (byte decode + v_dot4), "dot"
@@ -68,6 +68,7 @@ def gpu_pot_decode(d, codes_se, codes_m, key_scale, mant_bits=0, frac_bits=7,
     res = {}
     dbg = pa.pot_debug()
     dbg.force_splits = force_splits
+    dbg.force_wg_waves = wg_waves
     bufs = {}
     if taps:
         max_s = -(-T // 256)
@@ -91,6 +92,7 @@ def gpu_pot_decode(d, codes_se, codes_m, key_scale, mant_bits=0, frac_bits=7,
     torch.cuda.synchronize()
     res["out"] = out.cpu().numpy()
     res["n_splits"], res["split_len"] = dbg.n_splits, dbg.split_len
+    res["wg_waves"] = dbg.wg_waves
     for k_, t_ in bufs.items():
         res[k_] = t_.cpu().numpy()
     if taps:
@@ -113,7 +115,7 @@ def oracle_pot(d, mant_bits=0, frac_bits=7, hadamard=False, split_len=None,
 
 
 def assert_pot_parity(d, mant_bits=0, frac_bits=7, hadamard=False, force_splits=0,
-                      key_scale=None, taps=True, engine="sac"):
+                      key_scale=None, taps=True, engine="sac", wg_waves=0):
     """Full parity: codes, scales, q^, Delta, scores, M (final and per split)
     bit-exact; O within O_TOL. Returns the max-abs O error."""
     rows = d["k_bits"].reshape(-1, 64)
@@ -125,7 +127,9 @@ def assert_pot_parity(d, mant_bits=0, frac_bits=7, hadamard=False, force_splits=
         assert np.array_equal(g_cm, o_cm), "codes_m differ"
     assert np.array_equal(g_sc.view(np.uint32), o_sc.view(np.uint32)), "key_scale differ"
     g = gpu_pot_decode(d, g_se, g_cm, g_sc, mant_bits, frac_bits, hadamard,
-                       taps=taps, force_splits=force_splits, engine=engine)
+                       taps=taps, force_splits=force_splits, engine=engine, wg_waves=wg_waves)
+    if wg_waves:
+        assert g["wg_waves"] == wg_waves, (g["wg_waves"], wg_waves)
     _, _, _, o = oracle_pot(d, mant_bits, frac_bits, hadamard,
                             split_len=g["split_len"], key_scale=key_scale)
     if taps:

@@ -5,6 +5,8 @@ T - 1 and attends over positions 0 .. T-1. The bar:
 * the cache rows it writes (codes, mantissa planes, scale, values) and its
   output equal, bit for bit, those of the three separate calls it replaces
   (pot_encode_keys on row T - 1, pot_store_values, pot_decode_attention);
+  with the CU-wide decode variant (chosen at B = 64, T = 32768) the output
+  agrees to fp32 rounding instead, as its waves claim tiles dynamically;
 * codes, scales, q^, Delta, int32 scores and integer maxima equal the
   oracle's, which encodes the whole key block itself, and O is within 2e-3.
 Row T - 1 of the cache holds the encoding of a poison key (and a poison value)
@@ -58,14 +60,14 @@ def _fused_and_separate(q, k_new, v_new, base, heads, B, Hq, Hkv, T, t_cap, fmt,
                         taps=True):
     """Runs the fused call on one copy of the cache and the three separate calls
     on another. Returns (fused cache, fused out, fused taps, separate cache,
-    separate out, separate taps, n_splits, split_len)."""
+    separate out, separate taps, n_splits, split_len, waves per workgroup)."""
     fused, sep = _clone(base), _clone(base)
     ws_bytes = pa.pot_decode_workspace_bytes(B, Hq, Hkv, T)
     res = []
     for path, c in (("fused", fused), ("separate", sep)):
         out = torch.empty((B, Hq, 64), dtype=torch.float32, device=DEV)
         ws = pa.alloc_workspace(ws_bytes, DEV)
-        dbg, bufs = _taps(B, Hq, T) if taps else (None, {})
+        dbg, bufs = _taps(B, Hq, T) if taps else (pa.pot_debug(), {})
         if path == "fused":
             pa.pot_append_decode_attention(fmt, q, k_new, v_new, c["se"], c["cm"], c["sc"],
                                            c["v"], t_cap, heads, B, Hq, Hkv, T, out, ws,
@@ -79,17 +81,24 @@ def _fused_and_separate(q, k_new, v_new, base, heads, B, Hq, Hkv, T, t_cap, fmt,
                                     Hq, Hkv, T, out, ws, dbg=dbg)
         torch.cuda.synchronize()
         res.append((c, out, bufs, dbg))
-    (fc, fo, fb, fd), (sc_, so, sb, _) = res
-    n_splits = fd.n_splits if fd is not None else None
-    split_len = fd.split_len if fd is not None else None
-    return fc, fo, fb, sc_, so, sb, n_splits, split_len
+    (fc, fo, fb, fd), (sc_, so, sb, sd) = res
+    assert (fd.n_splits, fd.split_len, fd.wg_waves) == (sd.n_splits, sd.split_len, sd.wg_waves)
+    n_splits = fd.n_splits if taps else None
+    return fc, fo, fb, sc_, so, sb, n_splits, fd.split_len, fd.wg_waves
 
 
-def _assert_same(fc, fo, fb, sc_, so, sb, n_splits):
+def _assert_same(fc, fo, fb, sc_, so, sb, n_splits, wg_waves=4):
+    """Caches and taps bit for bit; O bit for bit with four-wave workgroups,
+    to fp32 rounding (1e-5) with the CU-wide variant, whose waves sum the
+    tiles they claimed in claim order."""
     for k in ("se", "cm", "sc", "v"):
         if fc[k] is not None:
             assert torch.equal(fc[k].view(torch.uint8), sc_[k].view(torch.uint8)), f"cache {k}"
-    assert torch.equal(fo.view(torch.int32), so.view(torch.int32)), "out differs from 3 calls"
+    if wg_waves == 4:
+        assert torch.equal(fo.view(torch.int32), so.view(torch.int32)), "out differs from 3 calls"
+    else:
+        diff = float((fo - so).abs().max())
+        assert diff <= 1e-5, f"out differs from 3 calls by {diff}"
     for k in fb:
         a, b = fb[k], sb[k]
         if k == "m_split":  # [B][Hq][n_splits] densely packed at the buffer's start
@@ -109,9 +118,9 @@ def _run(seed, B, Hq, Hkv, T, t_cap=None, mant_bits=0, hadamard=False):
     k_new = to_dev(np.ascontiguousarray(d["k_bits"][:, :, T - 1])).view(torch.float16)
     v_new = to_dev(np.ascontiguousarray(d["v_bits"][:, :, T - 1])).view(torch.float16)
     q = to_dev(d["q"])
-    fc, fo, fb, sc_, so, sb, n_splits, split_len = _fused_and_separate(
+    fc, fo, fb, sc_, so, sb, n_splits, split_len, waves = _fused_and_separate(
         q, k_new, v_new, base, d["kv_head_of_q"], B, Hq, Hkv, T, t_cap, fmt, mant_bits)
-    _assert_same(fc, fo, fb, sc_, so, sb, n_splits)
+    _assert_same(fc, fo, fb, sc_, so, sb, n_splits, waves)
     # against the oracle, which encodes the whole (unpoisoned) key block itself
     o_se, o_cm, o_sc, o = oracle_pot(d, mant_bits, 7, hadamard, split_len=split_len)
     live = np.zeros((B, Hkv, t_cap), bool)
@@ -213,9 +222,9 @@ def test_append_full_size_b64_t32768():
     k_new = d["k"][:, :, T - 1].contiguous()
     v_new = d["v"][:, :, T - 1].contiguous()
     del d["k"], d["v"]
-    fc, fo, fb, sc_, so, sb, n_splits, _ = _fused_and_separate(
+    fc, fo, fb, sc_, so, sb, n_splits, _, waves = _fused_and_separate(
         d["q"], k_new, v_new, base, d["kv_head_of_q"], B, Hq, Hkv, T, T, fmt, 0, taps=False)
-    _assert_same(fc, fo, fb, sc_, so, sb, n_splits)
+    _assert_same(fc, fo, fb, sc_, so, sb, n_splits, waves)
     o_se, _, o_sc = oracle.encode_keys(k_new.cpu().numpy().view(np.uint16).reshape(-1, 64))
     new_rows = torch.arange(B * Hkv, device=DEV) * T + (T - 1)
     assert np.array_equal(fc["se"][new_rows].cpu().numpy(), o_se)

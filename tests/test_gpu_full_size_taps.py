@@ -7,7 +7,10 @@ appends the token at T - 1 first); the decoded-weight entry point
 pot_dot_decode_attention at Hadamard + PoT-M4 (B = 8) and PoT-M1 (B = 64). Each call runs twice on the same inputs:
 plain (the timed kernel) and with the score taps on (the instrumented build
 of the same kernel source, same split plan). Checked:
-* the two outputs are bit-identical;
+* the two outputs are bit-identical with four-wave workgroups; the CU-wide
+  variant (one workgroup per CU, tiles claimed from a counter) sums each
+  wave's tiles in the order it claimed them, so there the two agree to
+  fp32 rounding (1e-5);
 * on sampled (batch, kv head) slices: q^, Delta, the int32 scores of all G
   query heads over all T keys, the final integer maximum and the maximum of
   every split equal the oracle's bit for bit, and O is within 2e-3.
@@ -93,9 +96,13 @@ def _check(B, T, mant_bits, hadamard, append, samples, seed, engine="sac"):
         setattr(dbg, name, t.data_ptr())
     out_taps = _run(fmt, d, cache, v, append, dbg, engine)
     torch.cuda.synchronize()
-    assert (dbg.n_splits, dbg.split_len) == (n_splits, split_len)
-    assert torch.equal(out_plain.view(torch.int32), out_taps.view(torch.int32)), \
-        "instrumented build differs from the timed one"
+    assert (dbg.n_splits, dbg.split_len, dbg.wg_waves) == (n_splits, split_len, plan.wg_waves)
+    if plan.wg_waves == 4:
+        assert torch.equal(out_plain.view(torch.int32), out_taps.view(torch.int32)), \
+            "instrumented build differs from the timed one"
+    else:
+        diff = float((out_plain - out_taps).abs().max())
+        assert diff <= 1e-5, f"instrumented build differs from the timed one by {diff}"
     m_split = taps["m_split"].view(B, HQ, n_splits)
     worst = 0.0
     for (b, h) in samples:
@@ -123,7 +130,8 @@ def _check(B, T, mant_bits, hadamard, append, samples, seed, engine="sac"):
         err = float(np.abs(out_plain[b, hs].cpu().numpy() - r["out"][0]).max())
         worst = max(worst, err)
     assert worst <= O_TOL, worst
-    print(f"  splits={n_splits} x {split_len} keys, {len(samples)} slices x {G} heads x "
+    print(f"  splits={n_splits} x {split_len} keys, {plan.wg_waves} waves per workgroup, "
+          f"{len(samples)} slices x {G} heads x "
           f"{T} scores bit-exact, O err {worst:.3e}", flush=True)
     del d, cache, v, taps
     torch.cuda.empty_cache()
