@@ -8,7 +8,10 @@ that layer's cache and runs single-token decode attention over the T keys.
 
 32 query heads, 4 kv heads, d = 64. Inputs are synthetic, seeded, and resident
 in HBM before the timed region. Every layer has its own cache, so consecutive
-calls never hit the previous layer's data in the 256 MB last-level cache.
+calls never hit the previous layer's data in the 256 MB last-level cache. Each
+timed phase starts with about 0.3 s of untimed steps, so that the GPU runs at
+the clocks of back-to-back steps rather than those it drops to while the host
+sets a phase up, then the warm-up steps.
 
 The line reports:
 - keys scored per second (B * Hq * T * layers per step);
@@ -339,11 +342,28 @@ class Layers:
                 events[i][1].record()
 
 
+PREHEAT_S = 0.3  # seconds of steps before the warm-up steps of each timed phase
+
+
+def preheat(lay, seconds=PREHEAT_S):
+    """Runs whole steps for about `seconds` and waits for them: the GPU leaves
+    the clock state it drops to while the host prepares a phase (after an
+    idle gap of tens of ms the first ~40 decode calls run 10-20% slower than
+    the steady state of back-to-back steps)."""
+    import torch
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        lay.step()
+        torch.cuda.synchronize()
+
+
 def time_plain(lay, steps, warmup):
     """Wall time of `steps` steps with only the library's calls in the timed
     region (no timing events: each event record costs the step time on the
     device, about 5% for the four per layer of the instrumented pass)."""
     import torch
+    preheat(lay)
     for _ in range(warmup):
         lay.step()
     torch.cuda.synchronize()
@@ -382,6 +402,7 @@ def time_steps(lay, steps, warmup, kernel_times=False):
                 dl.append(d)
             kdbg.append(dl)
         torch.cuda.synchronize()
+    preheat(lay)
     t0 = time.perf_counter()
     for s in range(steps):
         lay.step(ev[s], kdbg[s] if kdbg else None)
@@ -707,10 +728,10 @@ def main() -> int:
                    "B": B, "T": T, "layers": L, "Hq": HQ, "Hkv": HKV, "head_dim": D,
                    "mant_bits": k, "frac_bits": 7, "parallelism": "none (1 GPU)"},
         "roofline": roofline,
-        "timing": {"value": f"{args.steps} steps after {args.warmup} warm-up steps, no events "
-                            "in the timed region",
+        "timing": {"value": f"{args.steps} steps after {PREHEAT_S} s of steps and "
+                            f"{args.warmup} warm-up steps, no events in the timed region",
                    "roofline": f"{args.steps} further steps with HIP events around every "
-                               "call and every decode kernel",
+                               f"call and every decode kernel, after {PREHEAT_S} s of steps",
                    "ms_per_step_with_events": elapsed_ev / args.steps * 1e3},
     }
     graph_ms = time_graph(lay, args.steps, args.warmup)

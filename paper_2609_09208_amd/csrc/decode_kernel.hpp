@@ -303,6 +303,71 @@ __device__ __forceinline__ uint32_t xad_u32(uint32_t a, uint32_t b, uint32_t c) 
   asm("v_xad_u32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
   return r;
 }
+// One 64-bit shift moves a pair of 32-bit words (v_lshrrev_b64 /
+// v_lshlrev_b64 issue at the rate of a 32-bit shift).
+__device__ __forceinline__ uint64_t pack64(uint32_t lo, uint32_t hi) {
+  return ((uint64_t)hi << 32) | lo;
+}
+template <int S>
+__device__ __forceinline__ uint64_t shr64(uint64_t v) {
+  uint64_t r;
+  asm("v_lshrrev_b64 %0, %1, %2" : "=v"(r) : "n"(S), "v"(v));
+  return r;
+}
+template <int S>
+__device__ __forceinline__ uint64_t shl64(uint64_t v) {
+  uint64_t r;
+  asm("v_lshlrev_b64 %0, %1, %2" : "=v"(r) : "n"(S), "v"(v));
+  return r;
+}
+
+// Shift amounts and weight fields of the four element pairs of two PoT code
+// words wa, wb (8 elements each; element m in nibble m = (sign << 3) | e).
+// am[.][n]: the exponents of elements n and n + 4 in bits 3:0 and 19:16,
+// where v_pk_ashrrev_i16 reads its per-half shift amounts (the bits above
+// them in each half may be set: 20 and up hold bits of the other word).
+// wf[.][n]: the weight field of elements n and n + 4, (sign, "not the zero
+// code") in bits 15:14 and 31:30, so that an arithmetic shift of each half
+// by 14 gives 1, -1, or 0 for the zero code (bits below 14 of each half are
+// left as they come). The two words share every shift; sel must hold
+// 0x88888888 (in a register, so that the select runs at the rate of a
+// VGPR-only op).
+struct CodePairFields {
+  uint32_t am[2][4], wf[2][4];
+};
+__device__ __forceinline__ CodePairFields code_pair_fields(uint32_t wa, uint32_t wb,
+                                                           uint32_t sel) {
+  CodePairFields f;
+  const uint32_t xa = wa & 0x77777777u, xb = wb & 0x77777777u;  // e per nibble
+  // e + 1 per nibble (no carry between nibbles): bit 3 is set exactly for
+  // the zero code, e = 7; moved to bit 2 by the pair's shift right by one
+  const uint64_t ys = shr64<1>(pack64(xa + 0x11111111u, xb + 0x11111111u));
+  // bit 3 of each nibble: the sign; bit 2: "not the zero code"
+  const uint32_t swa = (wa & sel) | (~(uint32_t)ys & ~sel);
+  const uint32_t swb = (wb & sel) | (~(uint32_t)(ys >> 32) & ~sel);
+  const uint64_t xx = pack64(xa, xb);
+  const uint64_t a1 = shr64<4>(xx), a2 = shr64<8>(xx), a3 = shr64<12>(xx);
+  f.am[0][0] = xa;
+  f.am[1][0] = xb;
+  f.am[0][1] = (uint32_t)a1;
+  f.am[1][1] = (uint32_t)(a1 >> 32);
+  f.am[0][2] = (uint32_t)a2;
+  f.am[1][2] = (uint32_t)(a2 >> 32);
+  f.am[0][3] = (uint32_t)a3;
+  f.am[1][3] = (uint32_t)(a3 >> 32);
+  const uint64_t ss = pack64(swa, swb);
+  const uint64_t s0 = shl64<12>(ss), s1 = shl64<8>(ss), s2 = shl64<4>(ss);
+  f.wf[0][0] = (uint32_t)s0;
+  f.wf[1][0] = (uint32_t)(s0 >> 32);
+  f.wf[0][1] = (uint32_t)s1;
+  f.wf[1][1] = (uint32_t)(s1 >> 32);
+  f.wf[0][2] = (uint32_t)s2;
+  f.wf[1][2] = (uint32_t)(s2 >> 32);
+  f.wf[0][3] = swa;
+  f.wf[1][3] = swb;
+  return f;
+}
+
 // max(a, b) for scores (never NaN) as v_max_f32 without operand canonicalisation
 __device__ __forceinline__ float max_f32(float a, float b) {
   return __builtin_amdgcn_fmed3f(a, b, __builtin_inff());
@@ -721,6 +786,10 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(
   // -1 kept opaque so that p - hi stays one fma_mix reading hi as fp16
   float neg_one = -1.0f;
   asm("" : "+v"(neg_one));
+  // the sign-bit select of the code fields, kept in a VGPR (a VALU op that
+  // reads an SGPR issues at the slower rate)
+  uint32_t sign_sel = 0x88888888u;
+  asm("" : "+v"(sign_sel));
 
   KeyRegs<MODE, K> kr[2];
   const int g_last = (t_end - 1) & ~7;  // first token of the range's last 8-token group
@@ -874,18 +943,23 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(
       // (sac_heads, sac_heads_m1, sac_heads_mk) over operand chunks (above).
       constexpr bool kRaw = G > 1;
       if constexpr (kRaw) load_chunk(0);
+      // Shift amounts and weight fields: for PoT-4, two code words at a time
+      // with the pair's 64-bit shifts (code_pair_fields); for PoT-Mk, whose
+      // registers hold no second word's fields, one word at a time: x holds
+      // e per nibble, sw the sign in bit 3 and "not the zero code" in bit 2
+      // (bit 3 of e + 1 is set exactly for e = 7; no carry between
+      // nibbles), moved into place per element pair.
+      constexpr bool kPairFields = K == 0;
+      CodePairFields pf;
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        const uint32_t wi = w[i];
-        const uint32_t x = wi & 0x77777777u;  // e per nibble
-        // e + 1 per nibble (no carry between nibbles): bit 3 is set exactly
-        // for the zero code, e = 7
-        const uint32_t y = x + 0x11111111u;
-        // per nibble, bit 3: the sign; bit 2: "not the zero code". Moved to
-        // the top of a 16-bit half and shifted arithmetically by 14 they give
-        // the element's weight: 1, -1, or 0 for the zero code (never
-        // negative)
-        const uint32_t sw = (wi & 0x88888888u) | (~(y >> 1) & 0x44444444u);
+        uint32_t x = 0, sw = 0;
+        if constexpr (kPairFields) {
+          if ((i & 1) == 0) pf = code_pair_fields(w[i], w[i + 1], sign_sel);
+        } else {
+          x = w[i] & 0x77777777u;
+          sw = (w[i] & 0x88888888u) | (~((x + 0x11111111u) >> 1) & 0x44444444u);
+        }
         // the mantissa bits of this code word's 8 elements, one byte per
         // plane, copied into both halves (bit n for element 8c + n in the
         // low half, bit n + 4 in the high half)
@@ -913,9 +987,11 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(
           // exponents of elements 8c + n and 8c + n + 4, one per half (the
           // shifts in sac_heads* read only the low four bits of each half, so
           // the bits above them stay; the one-head C++ path masks them)
-          const uint32_t shr = x >> (4 * n);
+          const uint32_t shr = kPairFields ? pf.am[i & 1][n] : x >> (4 * n);
           // the weights of elements 8c + n and 8c + n + 4
-          const s16x2 sg = __builtin_bit_cast(s16x2, sw << (12 - 4 * n)) >> (short)14;
+          const s16x2 sg =
+              __builtin_bit_cast(s16x2, kPairFields ? pf.wf[i & 1][n] : sw << (12 - 4 * n)) >>
+              (short)14;
           s16x2 mw[KP];
 #pragma unroll
           for (int bb = 0; bb < K; ++bb) {
@@ -1168,8 +1244,9 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(
     // ---- 2. transpose through wave-private LDS ----
     // Lane (row, grp) takes head row & 7 and keys 32 * part + 8 * grp .. + 7
     // of the tile (part = row >> 3), so every weight is computed once. Keys
-    // past the range carry the score of the range's last key (clamped loads):
-    // they cannot raise the maximum and are zeroed below in the tail tile.
+    // past the range carry the score of the range's last key (clamped
+    // loads) or of zero codes (buffer reads past the range): they are masked
+    // below in the tail tile.
 #pragma unroll
     for (int h = 0; h < G; ++h) sm.x[wave][h][lane] = xs[h];
     wave_sync_lds();

@@ -49,6 +49,30 @@
 #define I_PK_LSHL16(x) asm volatile("v_pk_lshlrev_b16 %0, %1, %0" : "+v"(x) : "v"(c));
 #define I_DOT2_U16(x) asm volatile("v_dot2_u32_u16 %0, %1, %2, %0" : "+v"(x) : "v"(b), "v"(c));
 #define I_CVT(x) asm volatile("v_cvt_f32_i32_e32 %0, %0" : "+v"(x));
+#define I_PK_ASHR16_SGPR(x) asm volatile("v_pk_ashrrev_i16 %0, %0, %1" : "+v"(x) : "s"(s));
+#define I_DOT2C_I16(x) asm volatile("v_dot2c_i32_i16 %0, %1, %2" : "+v"(x) : "v"(b), "v"(c));
+#define I_DOT2C_I16_SGPR(x) asm volatile("v_dot2c_i32_i16 %0, %1, %2" : "+v"(x) : "s"(s), "v"(c));
+#define I_BITOP3(x) asm volatile("v_bitop3_b32 %0, %0, %1, %2 bitop3:0x26" : "+v"(x) : "v"(b), "v"(c));
+#define I_BITOP3_SGPR(x) asm volatile("v_bitop3_b32 %0, %0, %1, %2 bitop3:0x26" : "+v"(x) : "s"(s), "v"(c));
+#define I_MUL_F32_SGPR(x) asm volatile("v_mul_f32_e32 %0, %1, %0" : "+v"(x) : "s"(s));
+#define I_EXP_F32(x) asm volatile("v_exp_f32_e32 %0, %0" : "+v"(x));
+#define I_CVT_PKRTZ(x) asm volatile("v_cvt_pkrtz_f16_f32 %0, %0, %1" : "+v"(x) : "v"(b));
+#define I_FMA_MIX(x) asm volatile("v_fma_mix_f32 %0, %1, %2, %0 op_sel_hi:[0,1,0]" : "+v"(x) : "v"(b), "v"(c));
+#define I_DPP_ROR8(x) asm volatile("v_mov_b32_dpp %0, %0 row_ror:8 row_mask:0xf bank_mask:0xf" : "+v"(x));
+// 64-bit shifts: one instruction shifts a register pair (two 32-bit words)
+#define I_LSHL64(x) asm volatile("v_lshlrev_b64 %0, %1, %0" : "+v"(x) : "v"(c));
+#define I_LSHR64(x) asm volatile("v_lshrrev_b64 %0, %1, %0" : "+v"(x) : "v"(c));
+#define KERNEL64(NAME, INS)                                                               \
+  __global__ __launch_bounds__(256) void NAME(unsigned* out, unsigned s, unsigned sh) {    \
+    unsigned long long a0 = threadIdx.x, a1 = a0 + 1, a2 = a0 + 2, a3 = a0 + 3,           \
+                       a4 = a0 + 4, a5 = a0 + 5, a6 = a0 + 6, a7 = a0 + 7;                \
+    unsigned c = sh & 3u;                                                                  \
+    for (int i = 0; i < N; ++i) {                                                          \
+      BODY8(INS)                                                                           \
+    }                                                                                      \
+    out[blockIdx.x * 256 + threadIdx.x] =                                                  \
+        (unsigned)(a0 ^ a1 ^ a2 ^ a3 ^ a4 ^ a5 ^ a6 ^ a7 ^ (a7 >> 32) ^ s);               \
+  }
 
 KERNEL(k_add, I_ADD)
 KERNEL(k_add_sgpr, I_ADD_SGPR)
@@ -70,6 +94,18 @@ KERNEL(k_dot4, I_DOT4)
 KERNEL(k_pk_lshl16, I_PK_LSHL16)
 KERNEL(k_dot2_u16, I_DOT2_U16)
 KERNEL(k_cvt, I_CVT)
+KERNEL(k_pk_ashr16_sgpr, I_PK_ASHR16_SGPR)
+KERNEL(k_dot2c_i16, I_DOT2C_I16)
+KERNEL(k_dot2c_i16_sgpr, I_DOT2C_I16_SGPR)
+KERNEL(k_bitop3, I_BITOP3)
+KERNEL(k_bitop3_sgpr, I_BITOP3_SGPR)
+KERNEL(k_mul_f32_sgpr, I_MUL_F32_SGPR)
+KERNEL(k_exp_f32, I_EXP_F32)
+KERNEL(k_cvt_pkrtz, I_CVT_PKRTZ)
+KERNEL(k_fma_mix, I_FMA_MIX)
+KERNEL(k_dpp_ror8, I_DPP_ROR8)
+KERNEL64(k_lshl64, I_LSHL64)
+KERNEL64(k_lshr64, I_LSHR64)
 
 typedef void (*kfn)(unsigned*, unsigned, unsigned);
 
@@ -91,7 +127,13 @@ int main() {
             {"v_bfe_i32", k_bfe},            {"v_add3_u32", k_add3},
             {"v_lshl_add_u32 (SGPR)", k_lshl_add}, {"v_perm_b32", k_perm},
             {"v_dot4_i32_i8", k_dot4},       {"v_pk_lshlrev_b16", k_pk_lshl16},
-            {"v_dot2_u32_u16", k_dot2_u16},  {"v_cvt_f32_i32_e32", k_cvt}};
+            {"v_dot2_u32_u16", k_dot2_u16},  {"v_cvt_f32_i32_e32", k_cvt},
+            {"v_pk_ashrrev_i16 (SGPR)", k_pk_ashr16_sgpr}, {"v_dot2c_i32_i16", k_dot2c_i16},
+            {"v_dot2c_i32_i16 (SGPR)", k_dot2c_i16_sgpr}, {"v_bitop3_b32", k_bitop3},
+            {"v_bitop3_b32 (SGPR)", k_bitop3_sgpr}, {"v_mul_f32_e32 (SGPR)", k_mul_f32_sgpr},
+            {"v_exp_f32_e32", k_exp_f32},    {"v_cvt_pkrtz_f16_f32", k_cvt_pkrtz},
+            {"v_fma_mix_f32", k_fma_mix},    {"v_mov_b32_dpp row_ror:8", k_dpp_ror8},
+            {"v_lshlrev_b64", k_lshl64},     {"v_lshrrev_b64", k_lshr64}};
   hipEvent_t e0, e1;
   if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) return 1;
   printf("%d CUs; wave64 instructions per ns per CU (2.4 = one per cycle per CU at 2.4 GHz)\n", cus);
