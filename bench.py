@@ -345,6 +345,21 @@ class Layers:
 PREHEAT_S = 0.3  # seconds of steps before the warm-up steps of each timed phase
 
 
+class no_gc:
+    """Python's cyclic garbage collector off inside a timed region (as timeit
+    does): a full collection over the host objects of a run can stall the
+    launch thread for tens of ms while the GPU idles."""
+
+    def __enter__(self):
+        import gc
+        gc.collect()
+        gc.disable()
+
+    def __exit__(self, *exc):
+        import gc
+        gc.enable()
+
+
 def preheat(lay, seconds=PREHEAT_S):
     """Runs whole steps for about `seconds` and waits for them: the GPU leaves
     the clock state it drops to while the host prepares a phase (after an
@@ -367,11 +382,12 @@ def time_plain(lay, steps, warmup):
     for _ in range(warmup):
         lay.step()
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(steps):
-        lay.step()
-    torch.cuda.synchronize()
-    return time.perf_counter() - t0
+    with no_gc():
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            lay.step()
+        torch.cuda.synchronize()
+        return time.perf_counter() - t0
 
 
 def time_steps(lay, steps, warmup, kernel_times=False):
@@ -403,11 +419,12 @@ def time_steps(lay, steps, warmup, kernel_times=False):
             kdbg.append(dl)
         torch.cuda.synchronize()
     preheat(lay)
-    t0 = time.perf_counter()
-    for s in range(steps):
-        lay.step(ev[s], kdbg[s] if kdbg else None)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
+    with no_gc():
+        t0 = time.perf_counter()
+        for s in range(steps):
+            lay.step(ev[s], kdbg[s] if kdbg else None)
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
     us = np.array([a.elapsed_time(b) for row in ev for (a, b) in row]) * 1e3
     if not kernel_times:
         return elapsed, us
@@ -429,11 +446,12 @@ def time_graph(lay, steps, warmup):
         g.replay()
     torch.cuda.synchronize()
     s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    s.record()
-    for _ in range(steps):
-        g.replay()
-    e.record()
-    torch.cuda.synchronize()
+    with no_gc():
+        s.record()
+        for _ in range(steps):
+            g.replay()
+        e.record()
+        torch.cuda.synchronize()
     del g
     return s.elapsed_time(e) / steps
 
@@ -446,12 +464,13 @@ def timed_calls(fn, n_layers, reps=10, warm=2):
             fn(i)
     torch.cuda.synchronize()
     s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    s.record()
-    for _ in range(reps):
-        for i in range(n_layers):
-            fn(i)
-    e.record()
-    torch.cuda.synchronize()
+    with no_gc():
+        s.record()
+        for _ in range(reps):
+            for i in range(n_layers):
+                fn(i)
+        e.record()
+        torch.cuda.synchronize()
     return s.elapsed_time(e) / (reps * n_layers) * 1e3
 
 
