@@ -943,13 +943,14 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(
       // (sac_heads, sac_heads_m1, sac_heads_mk) over operand chunks (above).
       constexpr bool kRaw = G > 1;
       if constexpr (kRaw) load_chunk(0);
-      // Shift amounts and weight fields: for PoT-4, two code words at a time
-      // with the pair's 64-bit shifts (code_pair_fields); for PoT-Mk, whose
-      // registers hold no second word's fields, one word at a time: x holds
+      // Shift amounts and weight fields: for PoT-4 and PoT-M1, two code words
+      // at a time with the pair's 64-bit shifts (code_pair_fields); with two
+      // or more mantissa planes, whose registers hold no second word's
+      // fields, one word at a time: x holds
       // e per nibble, sw the sign in bit 3 and "not the zero code" in bit 2
       // (bit 3 of e + 1 is set exactly for e = 7; no carry between
       // nibbles), moved into place per element pair.
-      constexpr bool kPairFields = K == 0;
+      constexpr bool kPairFields = K <= 1;
       CodePairFields pf;
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
