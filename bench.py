@@ -345,6 +345,14 @@ class Layers:
 PREHEAT_S = 0.3  # seconds of steps before the warm-up steps of each timed phase
 
 
+def collect_garbage():
+    """A full collection of Python's cyclic garbage, before a phase's untimed
+    steps (so that the idle gap it leaves falls before them, not between them
+    and the timed region)."""
+    import gc
+    gc.collect()
+
+
 class no_gc:
     """Python's cyclic garbage collector off inside a timed region (as timeit
     does): a full collection over the host objects of a run can stall the
@@ -352,7 +360,6 @@ class no_gc:
 
     def __enter__(self):
         import gc
-        gc.collect()
         gc.disable()
 
     def __exit__(self, *exc):
@@ -366,6 +373,7 @@ def preheat(lay, seconds=PREHEAT_S):
     idle gap of tens of ms the first ~40 decode calls run 10-20% slower than
     the steady state of back-to-back steps)."""
     import torch
+    collect_garbage()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     while time.perf_counter() - t0 < seconds:
@@ -437,11 +445,17 @@ def time_graph(lay, steps, warmup):
     captured once as a HIP graph and replayed: the launch gaps between the
     kernels shrink, the kernels are the same. Events around all replays."""
     import torch
+    collect_garbage()
     lay.step()  # eager first: the library caches its occupancy queries
     torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
         lay.step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < PREHEAT_S:  # the clocks, as in preheat()
+        g.replay()
+        torch.cuda.synchronize()
     for _ in range(warmup):
         g.replay()
     torch.cuda.synchronize()
@@ -457,7 +471,10 @@ def time_graph(lay, steps, warmup):
 
 
 def timed_calls(fn, n_layers, reps=10, warm=2):
-    """Mean microseconds per call of fn(layer) over reps passes of n_layers."""
+    """Mean microseconds per call of fn(layer) over reps passes of n_layers
+    (no garbage collection before it: the comparators' timed regions follow
+    each other back to back, and an idle gap would lower the next engine's
+    clocks)."""
     import torch
     for _ in range(warm):
         for i in range(n_layers):
