@@ -114,11 +114,14 @@ typedef struct pot_format {
  *               POT_ERR_HIP.
  *  force_wg_waves (in) 0: the planner picks the decode workgroup size; 4:
  *               four-wave workgroups, each wave taking every fourth 64-key
- *               tile of its split; or the wave count of the CU-wide variant
- *               of the shift-accumulate kernels over fp16 values (16 at
- *               k <= 2, 12 at k = 3 and 4): one workgroup per CU whose
- *               waves claim the split's tiles from a counter in LDS. Other
- *               values return POT_ERR_INVALID_ARG. Scores and maxima do not
+ *               tile of its split; or the wave count of the engine's
+ *               CU-wide variant: one workgroup per CU whose waves claim the
+ *               split's tiles from a counter in LDS (shift-accumulate
+ *               kernels, fp16 or INT8 values: 16 at k <= 2, 12 at k = 3
+ *               and 4; decoded-code engines: 16, or 12 for PoT-4 bytes over
+ *               fp16 values or with power-of-two weights; INT8 comparator:
+ *               12; the fp16 comparator has none). Other values return
+ *               POT_ERR_INVALID_ARG. Scores and maxima do not
  *               depend on it; O does to fp32 rounding (with claimed tiles the
  *               order of the sums varies from call to call).
  *  wg_waves     (out) the waves per workgroup used (written on the host)

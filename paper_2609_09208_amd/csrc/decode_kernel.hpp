@@ -285,11 +285,10 @@ constexpr int kWaves = kBlock / 64;  // waves per workgroup of the default varia
 // oldest of its ready waves first, so of the four equal workgroups that
 // share a CU the first dispatched finishes in about a third of the time of
 // the last, and the CU runs its last stretch with one wave per SIMD. In the
-// CU-wide variant one workgroup holds all of a CU's waves (four per SIMD at
-// k <= 2, three at k = 3 and 4: what the registers of those kernels
-// allow) and its waves take tiles from a counter in LDS, so they all finish
-// within about one tile of each other. Built for the shift-accumulate kernels
-// over fp16 values.
+// CU-wide variant one workgroup holds all of a CU's waves (as many per SIMD
+// as the kernel's registers allow: pool_waves) and its waves take tiles from
+// a counter in LDS, so they all finish within about one tile of each other.
+// Every engine but the fp16 comparator has it.
 template <int MODE, int K, int VF>
 constexpr int kPoolWaves = pool_waves(MODE, K, VF);
 constexpr int kWTile = 64;    // keys per wave tile

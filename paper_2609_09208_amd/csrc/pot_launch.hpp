@@ -100,10 +100,18 @@ struct DecodeArgs {
 };
 
 // Waves per workgroup of a decode kernel's CU-wide variant, 0 if it has
-// none: the shift-accumulate kernels over fp16 values, four waves per SIMD
-// at k <= 2 and three at k = 3, 4 (their register budgets).
+// none: four SIMDs times the waves per SIMD that the kernel's registers
+// allow (512 per lane and SIMD): the shift-accumulate kernels 4 at k <= 2
+// and 3 at k = 3, 4 (fp16 or INT8 values); the decoded-code engines 4, or 3
+// for PoT-4 bytes over fp16 values or with power-of-two weights; the INT8
+// comparator 3. The fp16 comparator has none: at its two waves per SIMD a
+// CU-wide workgroup of 8 waves measured slower than two four-wave ones
+// (B = 64, T = 32768: 339.6 against 318.4 us per call).
 constexpr int pool_waves(int mode, int mant_bits, int vf) {
-  return (mode == kScorePot && vf == 0) ? (mant_bits <= 2 ? 16 : 12) : 0;
+  return mode == kScorePot    ? (mant_bits <= 2 ? 16 : 12)
+         : mode == kScoreDs4a ? ((mant_bits > 0 || vf == 1) ? 16 : 12)
+         : mode == kScoreInt8 ? 12
+                              : 0;
 }
 
 // Longest key range of one decode call: the decode kernel reads each

@@ -56,7 +56,7 @@ def _taps(B, Hq, T):
 
 
 def assert_v8_parity(d, engine=0, mant_bits=0, hadamard=False, force_splits=0, tol=O_TOL,
-                     pow2=False):
+                     pow2=False, wg_waves=0):
     B, Hq, Hkv, T, t_cap = d["B"], d["Hq"], d["Hkv"], d["T"], d["t_cap"]
     rows = d["k_bits"].reshape(-1, 64)
     se, cm, sc = gpu_encode(rows, mant_bits, hadamard)
@@ -75,10 +75,13 @@ def assert_v8_parity(d, engine=0, mant_bits=0, hadamard=False, force_splits=0, t
     ws = pa.alloc_workspace(nws, DEV)
     dbg, bufs = _taps(B, Hq, T)
     dbg.force_splits = force_splits
+    dbg.force_wg_waves = wg_waves
     call = pa.pot_decode_attention_v8_pow2 if pow2 else pa.pot_decode_attention_v8
     call(fmt, engine, to_dev(d["q"]), to_dev(se), to_dev(cm) if cm is not None else None,
          to_dev(sc), vu, ve, t_cap, d["kv_head_of_q"], B, Hq, Hkv, T, out, ws, dbg=dbg)
     torch.cuda.synchronize()
+    if wg_waves:
+        assert dbg.wg_waves == wg_waves, (dbg.wg_waves, wg_waves)
     o = oracle.pot_decode_v8(d["q"], o_se, o_cm, o_sc, o_vh, o_g, t_cap, d["kv_head_of_q"],
                              B, Hq, Hkv, T, mant_bits=mant_bits, hadamard=hadamard,
                              split_len=dbg.split_len, pow2=pow2)
