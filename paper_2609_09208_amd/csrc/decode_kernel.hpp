@@ -1,12 +1,15 @@
 // Split-K decode attention for gfx950 over a PoT / INT8 / fp16 key cache.
 //
-// Grid (n_splits, Hkv, B), 256 threads = 4 wave64. A workgroup owns one key
+// Grid (n_splits, Hkv, B), 256 threads = 4 wave64, or in the CU-wide variant
+// one workgroup of pool_waves(...) waves per CU. A workgroup owns one key
 // range of one (batch, kv-head) sequence and all G query heads sharing that
 // kv head (GQA), so every code and value byte is read from HBM once and used
 // G times. Inside the workgroup each wave streams its own 64-key tiles
-// (tile j of the range goes to wave j % 4) with the next tile's codes and
-// value fragments prefetched into registers while the current one is
-// processed; waves only meet at the end to merge their partial sums.
+// (tile j of the range goes to wave j % 4; in the CU-wide variant the waves
+// claim tiles from a counter in LDS) with the next tile's codes (and, for
+// the short score cores, value fragments) prefetched into registers while
+// the current one is processed; waves only meet at the end to merge their
+// partial sums.
 //
 // Per 64-key tile and wave:
 //  1. Scores, one key per lane (Sec. II-B eq. sac). PoT-4: the key's 32 code
