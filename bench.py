@@ -21,7 +21,8 @@ The line reports:
   with median and best; the whole call (query prep with the append, decode,
   split combine) is reported beside it as call_us / frac_call;
 - the same step captured once as a HIP graph and replayed (graph);
-- speed-up over the in-repo fp16 and INT8 kernels on the same shape;
+- speed-up over the in-repo fp16 and INT8 kernels on the same shape (each
+  engine timed as HIP graph replays of a pass over the layers);
 - the CPU oracle timed on host cores on a bounded sample, with one thread and
   with all threads.
 
@@ -470,24 +471,40 @@ def time_graph(lay, steps, warmup):
     return s.elapsed_time(e) / steps
 
 
-def timed_calls(fn, n_layers, reps=10, warm=2):
+def timed_calls(fn, n_layers, reps=10, warm=2, graph=False):
     """Mean microseconds per call of fn(layer) over reps passes of n_layers
     (no garbage collection before it: the comparators' timed regions follow
     each other back to back, and an idle gap would lower the next engine's
-    clocks)."""
+    clocks). graph: one pass over the layers is captured as a HIP graph and
+    the timed passes replay it, so the figure is the device's time per call
+    even where a call takes less than its Python and ctypes launch path on
+    the host (the small single-layer configurations)."""
     import torch
     for _ in range(warm):
         for i in range(n_layers):
             fn(i)
     torch.cuda.synchronize()
+    g = None
+    if graph:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for i in range(n_layers):
+                fn(i)
+        for _ in range(warm):
+            g.replay()
+        torch.cuda.synchronize()
     s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     with no_gc():
         s.record()
         for _ in range(reps):
-            for i in range(n_layers):
-                fn(i)
+            if g is not None:
+                g.replay()
+            else:
+                for i in range(n_layers):
+                    fn(i)
         e.record()
         torch.cuda.synchronize()
+    del g
     return s.elapsed_time(e) / (reps * n_layers) * 1e3
 
 
@@ -562,7 +579,7 @@ def comparators(pa, lay, dev):
     runs = {name: [] for name in engines}
     for _ in range(COMPARE_ROUNDS):
         for name, fn in engines.items():
-            runs[name].append(timed_calls(fn, len(cl), reps=10, warm=4))
+            runs[name].append(timed_calls(fn, len(cl), reps=10, warm=4, graph=True))
     med = {name: float(sorted(v)[len(v) // 2]) for name, v in runs.items()}
     pot_us, f16_us, i8_us, ds4a_us = med["pot"], med["fp16"], med["int8"], med.get("ds4a")
     pv8_us, dv8_us, pw_us = med["pot_v8"], med.get("ds4a_v8"), med["pot_v8_pow2"]
@@ -599,7 +616,8 @@ def comparators(pa, lay, dev):
                         "pow2 weights: both products by powers of two "
                         "(pot_decode_attention_v8_pow2)"},
             "timing": f"median of {COMPARE_ROUNDS} interleaved rounds of 10 passes over the "
-                      f"{len(cl)} layers per engine"}
+                      f"{len(cl)} layers per engine, each pass one HIP graph replay (device "
+                      "time per call, free of the host's launch path)"}
 
 
 def fmt_name(k: int, had: bool) -> str:
